@@ -1,0 +1,19 @@
+"""Plain, slow, fp64 CPU oracle of the DraftExpert MoE draft/verify hot path.
+
+TEST INFRASTRUCTURE ONLY.  It exists to check the HIP path, never to serve
+it: only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg
+of ``bench.py`` may import it.  It shares no code with the HIP library and
+imports nothing from it.
+
+Modules
+    moe     one MoE layer: routing (Eq. 1), union and token lists (Eq. 2-3),
+            target output (Eq. 4), draft output (Eq. 5), RMSNorm, greedy accept
+    decode  the stacked model, the exact draft/verify step and greedy AR
+            decoding (Algorithm 1)
+    cache   the expert cache with draft-router prefetch (Section 3.5)
+
+Pins (tests/test_oracle_*.py) tie every function to the paper or to
+mathematics independent of this code; functions without such a pin say
+"parity unpinned" in their docstring.
+"""
+from . import decode, moe  # noqa: F401
