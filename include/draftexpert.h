@@ -1,0 +1,202 @@
+/*
+ * draftexpert.h - C ABI of the MoE draft/verify hot path of DraftExpert
+ * (expansion-aware self-speculative decoding for expert-offloaded MoE
+ * inference), hand-written HIP for gfx950 (MI355X).
+ *
+ * Conventions shared by every call
+ *   - All tensor pointers are DEVICE pointers unless a parameter says "host".
+ *     The caller owns every buffer; the layer calls never allocate device
+ *     memory: their scratch comes in through (ws, ws_bytes), sized by
+ *     de_workspace_bytes().
+ *   - Activations (x, y, logits, gates) are fp32, row-major [T, H] etc.
+ *     Router weights are fp32 [N, H].  Expert weights are fp32 or bf16
+ *     (raw uint16 bit patterns) as de_moe_desc.wdtype says.
+ *   - An expert block is one contiguous region [G: I x H][U: I x H][D: H x I],
+ *     each matrix row-major [out, in].  The shared path of a layer is one
+ *     block whose I is the concatenated n_shared * I_shared (a sum of SwiGLU
+ *     experts equals one SwiGLU over the concatenated intermediate).
+ *     Weight pointers and strides must be 16-byte aligned.
+ *   - Every call enqueues work on `stream` and returns without synchronising
+ *     the host.  Data-dependent sizes (the union size) stay in device memory.
+ *   - Argument checks run on the host before any HIP call, so an invalid call
+ *     returns DE_ERR_INVALID / DE_ERR_UNSUPPORTED / DE_ERR_WORKSPACE and
+ *     enqueues nothing.  Device pointers are only checked for NULL and
+ *     alignment.  A launch failure returns DE_ERR_HIP.
+ *   - Limits: 1 <= T <= 64 block positions; 1 <= k <= min(N, 32);
+ *     1 <= N <= 256; H, I multiples of 8 for bf16 and of 4 for fp32 weights.
+ *
+ * Notation follows the paper: TopK_l(h) (Eq. 1), the block union U_l(B)
+ * (Eq. 2, Eq. 3), the target MoE output y* (Eq. 4) and the fixed-footprint
+ * draft output y^d (Eq. 5); acceptance follows Algorithm 1.
+ */
+#ifndef DRAFTEXPERT_H
+#define DRAFTEXPERT_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define DE_ABI_VERSION 1
+
+/* Return codes. */
+#define DE_OK 0
+#define DE_ERR_INVALID (-1)      /* NULL / misaligned pointer, size out of range */
+#define DE_ERR_UNSUPPORTED (-2)  /* dtype or option combination not implemented */
+#define DE_ERR_HIP (-3)          /* a HIP launch or runtime call failed */
+#define DE_ERR_WORKSPACE (-4)    /* ws NULL or smaller than de_workspace_bytes() */
+#define DE_ERR_NOT_RESIDENT (-5) /* expert cache: a needed expert has no slot */
+
+/* Router score functions (the router distribution R_l of Section 3.2). */
+#define DE_SOFTMAX 0 /* scores softmax(z + b); selection key z + b */
+#define DE_SIGMOID 1 /* scores sigmoid(z); selection key sigmoid(z) + b */
+
+/* Expert weight element types. */
+#define DE_F32 0
+#define DE_BF16 1
+
+/* Shape and options of one MoE layer. */
+typedef struct de_moe_desc {
+  int32_t hidden;       /* H */
+  int32_t n_experts;    /* N routed experts */
+  int32_t top_k;        /* k */
+  int32_t inter;        /* I of each routed expert */
+  int32_t shared_inter; /* concatenated shared intermediate (0: no shared path) */
+  int32_t draft_inter;  /* I_d of the draft expert (0: none) */
+  int32_t score_func;   /* DE_SOFTMAX or DE_SIGMOID */
+  int32_t norm_topk;    /* 1: divide the k gates by their sum */
+  float routed_scale;   /* multiplies every routed gate */
+  int32_t wdtype;       /* DE_F32 or DE_BF16 expert weights */
+} de_moe_desc;
+
+/* Where routed expert e lives: base + slot_of_expert[e] * slot_stride_bytes.
+ * slot_of_expert NULL means slot e (all experts resident, in order).
+ * A slot < 0 or >= n_slots marks an expert that is not resident: its work is
+ * skipped (the expert cache guarantees residency before it launches). */
+typedef struct de_expert_table {
+  const void* base;              /* device: slot 0 */
+  int64_t slot_stride_bytes;     /* >= 3*I*H*elem, multiple of 16 */
+  const int32_t* slot_of_expert; /* device [N] or NULL */
+  int32_t n_slots;               /* number of valid slots */
+} de_expert_table;
+
+/* Optional fused epilogue of a layer call.  With residual != NULL the layer
+ * writes y = residual + layer(x) (the pre-norm residual stack); with
+ * normed != NULL it also writes RMSNorm(y) = y / sqrt(mean(y^2) + eps), the
+ * next layer's input.  residual may alias y. */
+typedef struct de_epilogue {
+  const float* residual; /* device [T, H] or NULL */
+  float* normed;         /* device [T, H] or NULL */
+  float eps;
+} de_epilogue;
+
+int de_abi_version(void);
+const char* de_error_string(int code);
+
+/* Host-only validation of a layer descriptor (DE_OK or an error code). */
+int de_check_desc(const de_moe_desc* d);
+
+/* Scratch bytes needed by de_route_topk, de_grouped_swiglu, de_draft_layer
+ * and de_verify_layer for blocks of up to T positions (0 on an invalid desc). */
+size_t de_workspace_bytes(const de_moe_desc* d, int T);
+
+/* Router scoring and top-k selection (Eq. 1) with the gates of Eq. (4).
+ *   x [T, H], w_router [N, H], bias [N] or NULL.
+ *   topk_idx [T, k] int32: expert ids in descending selection key, ties to the
+ *   lower id.  topk_gate [T, k]: softmax probability (or unbiased sigmoid) of
+ *   each chosen expert, divided by the k-sum if norm_topk, times routed_scale.
+ * Logits are accumulated in fp32. */
+int de_route_topk(const de_moe_desc* d, int T, const float* x, const float* w_router,
+                  const float* bias, int32_t* topk_idx, float* topk_gate, void* ws,
+                  size_t ws_bytes, hipStream_t stream);
+
+/* Union of the block's top-k sets with per-expert token lists (Eq. 2, Eq. 3).
+ * Integer only, so deterministic.
+ *   n_union [1]: |U|; union_ids [N]: members ascending, the tail set to -1;
+ *   offsets [N+1]: list bounds, offsets[u]..offsets[u+1] for member u, entries
+ *   past n_union equal to T*k; tok_list [T*k]: block positions, ascending
+ *   within each member; gate_list [T*k]: the matching gates; pair_pos [T, k]:
+ *   where (topk_idx[t,j], t) sits in the lists.
+ * An id outside [0, N) or repeated within one position makes n_union = -1 and
+ * leaves the other outputs unspecified. */
+int de_expert_union(int T, int k, int N, const int32_t* topk_idx, const float* topk_gate,
+                    int32_t* n_union, int32_t* union_ids, int32_t* offsets, int32_t* tok_list,
+                    float* gate_list, int32_t* pair_pos, hipStream_t stream);
+
+/* Grouped SwiGLU over the union plus the shared path (Eq. 4 without routing):
+ *   y[t] = S(x_t) + sum_j gate[t,j] E_{idx[t,j]}(x_t),   E(v) = D(silu(Gv) * (Uv)).
+ * Each union expert's weights are streamed from HBM once for all of its
+ * positions.  Inputs are de_expert_union's outputs; shared_w may be NULL
+ * when desc.shared_inter is 0.  Partial sums are combined in a fixed order
+ * (no float atomics), so repeated calls are bitwise identical. */
+int de_grouped_swiglu(const de_moe_desc* d, int T, const float* x, const de_expert_table* routed,
+                      const int32_t* n_union, const int32_t* union_ids, const int32_t* offsets,
+                      const int32_t* tok_list, const float* gate_list, const int32_t* pair_pos,
+                      const void* shared_w, float* y, const de_epilogue* epi, void* ws,
+                      size_t ws_bytes, hipStream_t stream);
+
+/* Fixed-footprint draft layer (Eq. 5):
+ *   y^d_t = S(x_t) + g_{t,e1} E_{e1}(x_t) + gamma * E^d(x_t),
+ * e1 the top-1 expert and g_{t,e1} its target gate.  Only e1 of the routed
+ * experts is read.  pred_idx / pred_gate [T, k] (may be NULL) receive the full
+ * top-k of the draft router: the predicted verifier experts (Section 3.4).
+ * draft_w NULL (or desc.draft_inter 0) drops the draft-expert term. */
+int de_draft_layer(const de_moe_desc* d, int T, const float* x, const float* w_router,
+                   const float* bias, const de_expert_table* routed, const void* shared_w,
+                   const void* draft_w, float gamma, float* y, int32_t* pred_idx,
+                   float* pred_gate, const de_epilogue* epi, void* ws, size_t ws_bytes,
+                   hipStream_t stream);
+
+/* Target MoE layer over a verify block of T positions (Eq. 4): routing,
+ * union build and the grouped SwiGLU in one call.  Every intermediate output
+ * pointer (topk_idx .. pair_pos) may be NULL; non-NULL ones receive the same
+ * values as de_route_topk / de_expert_union. */
+int de_verify_layer(const de_moe_desc* d, int T, const float* x, const float* w_router,
+                    const float* bias, const de_expert_table* routed, const void* shared_w,
+                    float* y, int32_t* topk_idx, float* topk_gate, int32_t* n_union,
+                    int32_t* union_ids, int32_t* offsets, int32_t* tok_list, float* gate_list,
+                    int32_t* pair_pos, const de_epilogue* epi, void* ws, size_t ws_bytes,
+                    hipStream_t stream);
+
+/* Greedy exact acceptance (Algorithm 1, verify and accept):
+ *   target_argmax[j] = argmax_v target_logits[j, v] (ties to the lowest v),
+ *   j = 0..K; out[0] = n = largest m <= K with draft_tokens[i-1] ==
+ *   target_argmax[i-1] for all i <= m; out[1] = target_argmax[n] (the bonus
+ *   token).  K = 0 gives the argmax of one row.  draft_tokens may be NULL
+ *   when K is 0. */
+int de_accept_len(int K, int V, const float* target_logits, const int32_t* draft_tokens,
+                  int32_t* target_argmax, int32_t* out, hipStream_t stream);
+
+/* ---- Stacked-model glue (a pre-norm residual stack without attention) ---- */
+
+/* logits [T, V] = x [T, H] . W^T with W bf16 [V, H] (the LM head). */
+int de_lm_head(int T, int H, int V, const float* x, const void* w_lm, float* logits,
+               hipStream_t stream);
+
+/* out [T, H] = x / sqrt(mean(x^2) + eps) per row (unit gain). out may alias x. */
+int de_rmsnorm(int T, int H, const float* x, float eps, float* out, hipStream_t stream);
+
+/* h [T, H] = fp32(emb[tokens[t]]) with emb bf16 [V, H]; tokens is a device
+ * int32 array (ids are clamped into [0, V)).  normed (may be NULL) receives
+ * RMSNorm(h). */
+int de_embed_gather(int T, int H, int V, const int32_t* tokens, const void* emb, float* h,
+                    float* normed, float eps, hipStream_t stream);
+
+/* Dense SwiGLU layer y = E(x) of intermediate I (layer 0 of the stack), with
+ * the optional epilogue.  Scratch: de_dense_workspace_bytes(T, I). */
+size_t de_dense_workspace_bytes(int T, int H, int I);
+int de_dense_swiglu(int T, int H, int I, int wdtype, const float* x, const void* w, float* y,
+                    const de_epilogue* epi, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Pure streaming read of `bytes` (multiple of 16) from buf: the measured HBM
+ * read ceiling.  sink [1] receives a value that depends on every byte. */
+int de_stream_probe(const void* buf, size_t bytes, float* sink, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DRAFTEXPERT_H */

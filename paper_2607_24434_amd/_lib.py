@@ -1,0 +1,230 @@
+"""ctypes binding of libdraftexpert.so: argument marshalling only.
+
+Every function below has the name of the C entry point it calls, takes torch
+tensors (device memory) or None for optional pointers, passes their
+``data_ptr()`` and the current HIP stream, and raises ``DEError`` on a
+non-zero return code.  There is no fallback: if the library is missing the
+import of this module fails.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+# torch first: its HIP runtime (SONAME libamdhip64.so.7) must be the one the
+# dynamic linker resolves for this library too, so that one runtime owns the
+# device memory and streams torch hands over.
+import torch  # noqa: F401
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libdraftexpert.so")
+
+DE_SOFTMAX = 0
+DE_SIGMOID = 1
+DE_F32 = 0
+DE_BF16 = 1
+
+C_FUNCS = [
+    "de_abi_version", "de_error_string", "de_check_desc", "de_workspace_bytes", "de_route_topk",
+    "de_expert_union", "de_grouped_swiglu", "de_draft_layer", "de_verify_layer", "de_accept_len",
+    "de_lm_head", "de_rmsnorm", "de_embed_gather", "de_dense_workspace_bytes", "de_dense_swiglu",
+    "de_stream_probe",
+]
+
+
+class DEError(RuntimeError):
+    def __init__(self, fn: str, code: int, msg: str):
+        super().__init__(f"{fn} failed with {code}: {msg}")
+        self.code = code
+
+
+class MoEDesc(ctypes.Structure):
+    _fields_ = [
+        ("hidden", ctypes.c_int32), ("n_experts", ctypes.c_int32), ("top_k", ctypes.c_int32),
+        ("inter", ctypes.c_int32), ("shared_inter", ctypes.c_int32),
+        ("draft_inter", ctypes.c_int32), ("score_func", ctypes.c_int32),
+        ("norm_topk", ctypes.c_int32), ("routed_scale", ctypes.c_float),
+        ("wdtype", ctypes.c_int32),
+    ]
+
+
+class ExpertTable(ctypes.Structure):
+    _fields_ = [
+        ("base", ctypes.c_void_p), ("slot_stride_bytes", ctypes.c_int64),
+        ("slot_of_expert", ctypes.c_void_p), ("n_slots", ctypes.c_int32),
+    ]
+
+
+class Epilogue(ctypes.Structure):
+    _fields_ = [("residual", ctypes.c_void_p), ("normed", ctypes.c_void_p), ("eps", ctypes.c_float)]
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2607_24434_amd.build`")
+    lib = ctypes.CDLL(LIB_PATH)
+    P = ctypes.c_void_p
+    I = ctypes.c_int
+    F = ctypes.c_float
+    SZ = ctypes.c_size_t
+    DP = ctypes.POINTER(MoEDesc)
+    TP = ctypes.POINTER(ExpertTable)
+    EP = ctypes.POINTER(Epilogue)
+    sig = {
+        "de_abi_version": (I, []),
+        "de_error_string": (ctypes.c_char_p, [I]),
+        "de_check_desc": (I, [DP]),
+        "de_workspace_bytes": (SZ, [DP, I]),
+        "de_route_topk": (I, [DP, I, P, P, P, P, P, P, SZ, P]),
+        "de_expert_union": (I, [I, I, I, P, P, P, P, P, P, P, P, P]),
+        "de_grouped_swiglu": (I, [DP, I, P, TP, P, P, P, P, P, P, P, P, EP, P, SZ, P]),
+        "de_draft_layer": (I, [DP, I, P, P, P, TP, P, P, F, P, P, P, EP, P, SZ, P]),
+        "de_verify_layer": (I, [DP, I, P, P, P, TP, P, P, P, P, P, P, P, P, P, P, EP, P, SZ, P]),
+        "de_accept_len": (I, [I, I, P, P, P, P, P]),
+        "de_lm_head": (I, [I, I, I, P, P, P, P]),
+        "de_rmsnorm": (I, [I, I, P, F, P, P]),
+        "de_embed_gather": (I, [I, I, I, P, P, P, P, F, P]),
+        "de_dense_workspace_bytes": (SZ, [I, I, I]),
+        "de_dense_swiglu": (I, [I, I, I, I, P, P, P, EP, P, SZ, P]),
+        "de_stream_probe": (I, [P, SZ, P, P]),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    return lib
+
+
+LIB = _load()
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    return t.data_ptr()
+
+
+def _stream(stream):
+    if stream is not None:
+        return stream if isinstance(stream, int) else stream.cuda_stream
+    return torch.cuda.current_stream().cuda_stream
+
+
+def _check(fn: str, rc: int):
+    if rc != 0:
+        raise DEError(fn, rc, LIB.de_error_string(rc).decode())
+
+
+def make_desc(hidden, n_experts, top_k, inter, shared_inter, draft_inter, score_func, norm_topk,
+              routed_scale=1.0, wdtype=DE_BF16) -> MoEDesc:
+    return MoEDesc(int(hidden), int(n_experts), int(top_k), int(inter), int(shared_inter),
+                   int(draft_inter), int(score_func), int(bool(norm_topk)), float(routed_scale),
+                   int(wdtype))
+
+
+def make_table(base, slot_stride_bytes: int, slot_of_expert=None, n_slots: int = 0) -> ExpertTable:
+    return ExpertTable(_ptr(base), int(slot_stride_bytes), _ptr(slot_of_expert), int(n_slots))
+
+
+def make_epilogue(residual=None, normed=None, eps: float = 1e-6):
+    if residual is None and normed is None:
+        return None
+    return Epilogue(_ptr(residual), _ptr(normed), float(eps))
+
+
+def _epi_arg(epi):
+    return None if epi is None else ctypes.byref(epi)
+
+
+def de_abi_version() -> int:
+    return LIB.de_abi_version()
+
+
+def de_error_string(code: int) -> str:
+    return LIB.de_error_string(code).decode()
+
+
+def de_check_desc(desc: MoEDesc) -> int:
+    return LIB.de_check_desc(ctypes.byref(desc))
+
+
+def de_workspace_bytes(desc: MoEDesc, T: int) -> int:
+    return LIB.de_workspace_bytes(ctypes.byref(desc), int(T))
+
+
+def de_route_topk(desc, T, x, w_router, bias, topk_idx, topk_gate, ws, stream=None):
+    _check("de_route_topk", LIB.de_route_topk(
+        ctypes.byref(desc), int(T), _ptr(x), _ptr(w_router), _ptr(bias), _ptr(topk_idx),
+        _ptr(topk_gate), _ptr(ws), ws.numel() if ws is not None else 0, _stream(stream)))
+
+
+def de_expert_union(T, k, N, topk_idx, topk_gate, n_union, union_ids, offsets, tok_list,
+                    gate_list, pair_pos, stream=None):
+    _check("de_expert_union", LIB.de_expert_union(
+        int(T), int(k), int(N), _ptr(topk_idx), _ptr(topk_gate), _ptr(n_union), _ptr(union_ids),
+        _ptr(offsets), _ptr(tok_list), _ptr(gate_list), _ptr(pair_pos), _stream(stream)))
+
+
+def de_grouped_swiglu(desc, T, x, table, n_union, union_ids, offsets, tok_list, gate_list,
+                      pair_pos, shared_w, y, ws, epi=None, stream=None):
+    _check("de_grouped_swiglu", LIB.de_grouped_swiglu(
+        ctypes.byref(desc), int(T), _ptr(x), ctypes.byref(table), _ptr(n_union), _ptr(union_ids),
+        _ptr(offsets), _ptr(tok_list), _ptr(gate_list), _ptr(pair_pos), _ptr(shared_w), _ptr(y),
+        _epi_arg(epi), _ptr(ws), ws.numel(), _stream(stream)))
+
+
+def de_draft_layer(desc, T, x, w_router, bias, table, shared_w, draft_w, gamma, y, pred_idx,
+                   pred_gate, ws, epi=None, stream=None):
+    _check("de_draft_layer", LIB.de_draft_layer(
+        ctypes.byref(desc), int(T), _ptr(x), _ptr(w_router), _ptr(bias), ctypes.byref(table),
+        _ptr(shared_w), _ptr(draft_w), float(gamma), _ptr(y), _ptr(pred_idx), _ptr(pred_gate),
+        _epi_arg(epi), _ptr(ws), ws.numel(), _stream(stream)))
+
+
+def de_verify_layer(desc, T, x, w_router, bias, table, shared_w, y, topk_idx=None, topk_gate=None,
+                    n_union=None, union_ids=None, offsets=None, tok_list=None, gate_list=None,
+                    pair_pos=None, ws=None, epi=None, stream=None):
+    _check("de_verify_layer", LIB.de_verify_layer(
+        ctypes.byref(desc), int(T), _ptr(x), _ptr(w_router), _ptr(bias), ctypes.byref(table),
+        _ptr(shared_w), _ptr(y), _ptr(topk_idx), _ptr(topk_gate), _ptr(n_union), _ptr(union_ids),
+        _ptr(offsets), _ptr(tok_list), _ptr(gate_list), _ptr(pair_pos), _epi_arg(epi), _ptr(ws),
+        ws.numel() if ws is not None else 0, _stream(stream)))
+
+
+def de_accept_len(K, V, target_logits, draft_tokens, target_argmax, out, stream=None):
+    _check("de_accept_len", LIB.de_accept_len(
+        int(K), int(V), _ptr(target_logits), _ptr(draft_tokens), _ptr(target_argmax), _ptr(out),
+        _stream(stream)))
+
+
+def de_lm_head(T, H, V, x, w_lm, logits, stream=None):
+    _check("de_lm_head", LIB.de_lm_head(int(T), int(H), int(V), _ptr(x), _ptr(w_lm), _ptr(logits),
+                                        _stream(stream)))
+
+
+def de_rmsnorm(T, H, x, eps, out, stream=None):
+    _check("de_rmsnorm", LIB.de_rmsnorm(int(T), int(H), _ptr(x), float(eps), _ptr(out),
+                                        _stream(stream)))
+
+
+def de_embed_gather(T, H, V, tokens, emb, h, normed=None, eps=1e-6, stream=None):
+    _check("de_embed_gather", LIB.de_embed_gather(int(T), int(H), int(V), _ptr(tokens), _ptr(emb),
+                                                  _ptr(h), _ptr(normed), float(eps),
+                                                  _stream(stream)))
+
+
+def de_dense_workspace_bytes(T, H, I) -> int:
+    return LIB.de_dense_workspace_bytes(int(T), int(H), int(I))
+
+
+def de_dense_swiglu(T, H, I, wdtype, x, w, y, ws, epi=None, stream=None):
+    _check("de_dense_swiglu", LIB.de_dense_swiglu(
+        int(T), int(H), int(I), int(wdtype), _ptr(x), _ptr(w), _ptr(y), _epi_arg(epi), _ptr(ws),
+        ws.numel(), _stream(stream)))
+
+
+def de_stream_probe(buf, nbytes, sink, stream=None):
+    _check("de_stream_probe", LIB.de_stream_probe(_ptr(buf), int(nbytes), _ptr(sink),
+                                                  _stream(stream)))

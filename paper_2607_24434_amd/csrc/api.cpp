@@ -1,0 +1,494 @@
+// C ABI of the draft/verify hot path: argument checks (host only, before any
+// HIP call), scratch layout, and the launch sequence of each layer call.
+#include "../../include/draftexpert.h"
+#include "de_common.h"
+
+#include <cmath>
+#include <cstring>
+
+namespace de {
+
+const DevInfo& dev_info() {
+  static DevInfo info[64];
+  static bool ready[64] = {false};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) dev = 0;
+  if (!ready[dev]) {
+    int cus = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        cus < 1)
+      cus = 256;
+    info[dev].device = dev;
+    info[dev].num_cus = cus;
+    ready[dev] = true;
+  }
+  return info[dev];
+}
+
+}  // namespace de
+
+namespace {
+
+constexpr int kMaxT = 64;
+constexpr int kMaxK = 32;
+constexpr int kMaxN = 256;
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+size_t up256(size_t v) { return (v + 255) & ~size_t(255); }
+int elem_bytes(int wdtype) { return wdtype == DE_BF16 ? 2 : 4; }
+int elem_align(int wdtype) { return wdtype == DE_BF16 ? 8 : 4; }
+
+struct Layout {
+  size_t z, idx, gate, nu, uids, offs, tok, glist, ppos;
+  size_t a_r, a_s, a_d, p_r, p_s, p_d;
+  size_t total;
+};
+
+Layout layout(const de_moe_desc& d, int T) {
+  Layout L{};
+  size_t o = 0;
+  auto take = [&](size_t bytes) {
+    const size_t r = o;
+    o += up256(bytes);
+    return r;
+  };
+  const size_t tk = (size_t)T * d.top_k;
+  L.z = take((size_t)T * d.n_experts * 4);
+  L.idx = take(tk * 4);
+  L.gate = take(tk * 4);
+  L.nu = take(4);
+  L.uids = take((size_t)d.n_experts * 4);
+  L.offs = take(((size_t)d.n_experts + 1) * 4);
+  L.tok = take(tk * 4);
+  L.glist = take(tk * 4);
+  L.ppos = take(tk * 4);
+  L.a_r = take(tk * d.inter * 4);
+  L.a_s = take((size_t)T * d.shared_inter * 4);
+  L.a_d = take((size_t)T * d.draft_inter * 4);
+  L.p_r = take(tk * d.hidden * 4);
+  L.p_s = take((size_t)T * d.hidden * 4);
+  L.p_d = take((size_t)T * d.hidden * 4);
+  L.total = o;
+  return L;
+}
+
+int check_T(int T) { return (T >= 1 && T <= kMaxT) ? DE_OK : DE_ERR_INVALID; }
+
+int check_ws(const de_moe_desc& d, int T, const void* ws, size_t ws_bytes) {
+  if (ws == nullptr || (reinterpret_cast<uintptr_t>(ws) & 255u) != 0) return DE_ERR_WORKSPACE;
+  if (ws_bytes < layout(d, T).total) return DE_ERR_WORKSPACE;
+  return DE_OK;
+}
+
+int check_table(const de_moe_desc& d, const de_expert_table* t) {
+  if (t == nullptr || t->base == nullptr || !aligned16(t->base)) return DE_ERR_INVALID;
+  const int64_t need = 3ll * d.inter * d.hidden * elem_bytes(d.wdtype);
+  if (t->slot_stride_bytes < need || (t->slot_stride_bytes & 15) != 0) return DE_ERR_INVALID;
+  if (t->n_slots < 1) return DE_ERR_INVALID;
+  if (t->slot_of_expert == nullptr && t->n_slots < d.n_experts) return DE_ERR_INVALID;
+  return DE_OK;
+}
+
+int check_epi(const de_epilogue* epi) {
+  if (epi == nullptr) return DE_OK;
+  if (epi->normed != nullptr && !(epi->eps >= 0.f)) return DE_ERR_INVALID;
+  return DE_OK;
+}
+
+int hip_status(hipError_t e) { return e == hipSuccess ? DE_OK : DE_ERR_HIP; }
+
+template <typename T>
+T* at(void* ws, size_t off) {
+  return reinterpret_cast<T*>(static_cast<char*>(ws) + off);
+}
+
+de::RoutedSrc routed_src(const de_moe_desc& d, int T, const de_expert_table* tab, const int32_t* nu,
+                         const int32_t* uids, const int32_t* offs, const int32_t* tok,
+                         const float* glist, float* a_r, float* p_r) {
+  de::RoutedSrc r{};
+  r.base = static_cast<const char*>(tab->base);
+  r.stride = tab->slot_stride_bytes;
+  r.slot_of_expert = tab->slot_of_expert;
+  r.n_slots = tab->n_slots;
+  r.n_union = nu;
+  r.union_ids = uids;
+  r.offsets = offs;
+  r.tok_list = tok;
+  r.gate_list = glist;
+  r.max_union = d.n_experts;
+  r.pairs_max = T * d.top_k;  // capacity of the lists, A_r and P_r
+  r.inter = d.inter;
+  r.a = a_r;
+  r.p = p_r;
+  return r;
+}
+
+// gate/up + down + combine over the union (kk entries per position) and the
+// dense sources (shared path with gate 1, optionally the draft expert).
+int run_grouped(const de_moe_desc& d, int T, const float* x, const de::RoutedSrc& r,
+                const int32_t* pair_pos, int kk, const void* shared_w, const void* draft_w,
+                float gamma, float* y, const de_epilogue* epi, const Layout& L, void* ws,
+                hipStream_t s) {
+  const size_t esz = elem_bytes(d.wdtype);
+  de::GroupedArgs g{};
+  g.T = T;
+  g.H = d.hidden;
+  g.x = x;
+  g.has_routed = 1;
+  g.r = r;
+  g.n_dense = 0;
+  de::CombineArgs c{};
+  c.T = T;
+  c.H = d.hidden;
+  c.n_dense = 0;
+  if (shared_w != nullptr && d.shared_inter > 0) {
+    de::DenseSrc& ds = g.dense[g.n_dense++];
+    ds.w = shared_w;
+    ds.inter = d.shared_inter;
+    ds.out = at<float>(ws, L.a_s);
+    c.dense_p[c.n_dense++] = at<float>(ws, L.p_s);
+  }
+  if (draft_w != nullptr && d.draft_inter > 0) {
+    de::DenseSrc& ds = g.dense[g.n_dense++];
+    ds.w = draft_w;
+    ds.inter = d.draft_inter;
+    ds.out = at<float>(ws, L.a_d);
+    c.dense_p[c.n_dense++] = at<float>(ws, L.p_d);
+  }
+  hipError_t e = de::launch_gateup(g, d.wdtype, s);
+  if (e != hipSuccess) return DE_ERR_HIP;
+  // The down pass reads the gate/up activations of each dense source.
+  int nd = 0;
+  if (shared_w != nullptr && d.shared_inter > 0) {
+    de::DenseSrc& ds = g.dense[nd++];
+    ds.w = static_cast<const char*>(shared_w) + 2 * (size_t)d.shared_inter * d.hidden * esz;
+    ds.rows = d.hidden;
+    ds.gate = 1.0f;
+    ds.vin = at<float>(ws, L.a_s);
+    ds.vin_stride = d.shared_inter;
+    ds.out = at<float>(ws, L.p_s);
+    ds.out_stride = d.hidden;
+  }
+  if (draft_w != nullptr && d.draft_inter > 0) {
+    de::DenseSrc& ds = g.dense[nd++];
+    ds.w = static_cast<const char*>(draft_w) + 2 * (size_t)d.draft_inter * d.hidden * esz;
+    ds.rows = d.hidden;
+    ds.gate = gamma;
+    ds.vin = at<float>(ws, L.a_d);
+    ds.vin_stride = d.draft_inter;
+    ds.out = at<float>(ws, L.p_d);
+    ds.out_stride = d.hidden;
+  }
+  e = de::launch_down(g, d.wdtype, s);
+  if (e != hipSuccess) return DE_ERR_HIP;
+  c.p_r = r.p;
+  c.pair_pos = pair_pos;
+  c.kk = kk;
+  c.pairs_max = r.pairs_max;
+  c.y = y;
+  c.residual = epi ? epi->residual : nullptr;
+  c.normed = epi ? epi->normed : nullptr;
+  c.eps = epi ? epi->eps : 0.f;
+  return hip_status(de::launch_combine(c, s));
+}
+
+}  // namespace
+
+extern "C" {
+
+int de_abi_version(void) { return DE_ABI_VERSION; }
+
+const char* de_error_string(int code) {
+  switch (code) {
+    case DE_OK: return "ok";
+    case DE_ERR_INVALID: return "invalid argument (null or misaligned pointer, or a size out of range)";
+    case DE_ERR_UNSUPPORTED: return "unsupported dtype or option combination";
+    case DE_ERR_HIP: return "HIP launch or runtime error";
+    case DE_ERR_WORKSPACE: return "workspace missing, misaligned (256 B) or too small";
+    case DE_ERR_NOT_RESIDENT: return "a needed expert is not resident in the expert cache";
+    default: return "unknown error code";
+  }
+}
+
+int de_check_desc(const de_moe_desc* d) {
+  if (d == nullptr) return DE_ERR_INVALID;
+  if (d->wdtype != DE_F32 && d->wdtype != DE_BF16) return DE_ERR_UNSUPPORTED;
+  if (d->score_func != DE_SOFTMAX && d->score_func != DE_SIGMOID) return DE_ERR_UNSUPPORTED;
+  if (d->norm_topk != 0 && d->norm_topk != 1) return DE_ERR_INVALID;
+  if (d->n_experts < 1 || d->n_experts > kMaxN) return DE_ERR_INVALID;
+  if (d->top_k < 1 || d->top_k > kMaxK || d->top_k > d->n_experts) return DE_ERR_INVALID;
+  const int al = elem_align(d->wdtype);
+  if (d->hidden < al || d->hidden > (1 << 16) || d->hidden % al) return DE_ERR_INVALID;
+  if (d->inter < al || d->inter > (1 << 17) || d->inter % al) return DE_ERR_INVALID;
+  if (d->shared_inter < 0 || d->shared_inter > (1 << 17) || d->shared_inter % al) return DE_ERR_INVALID;
+  if (d->draft_inter < 0 || d->draft_inter > (1 << 17) || d->draft_inter % al) return DE_ERR_INVALID;
+  if (!std::isfinite(d->routed_scale)) return DE_ERR_INVALID;
+  return DE_OK;
+}
+
+size_t de_workspace_bytes(const de_moe_desc* d, int T) {
+  if (de_check_desc(d) != DE_OK || check_T(T) != DE_OK) return 0;
+  return layout(*d, T).total;
+}
+
+int de_route_topk(const de_moe_desc* d, int T, const float* x, const float* w_router,
+                  const float* bias, int32_t* topk_idx, float* topk_gate, void* ws,
+                  size_t ws_bytes, hipStream_t stream) {
+  int rc = de_check_desc(d);
+  if (rc != DE_OK) return rc;
+  if ((rc = check_T(T)) != DE_OK) return rc;
+  if (x == nullptr || w_router == nullptr || topk_idx == nullptr || topk_gate == nullptr)
+    return DE_ERR_INVALID;
+  if (!aligned16(x) || !aligned16(w_router) || d->hidden % 4) return DE_ERR_INVALID;
+  if ((rc = check_ws(*d, T, ws, ws_bytes)) != DE_OK) return rc;
+  const Layout L = layout(*d, T);
+  float* z = at<float>(ws, L.z);
+  if (de::launch_router_logits(x, w_router, T, d->hidden, d->n_experts, z, stream) != hipSuccess)
+    return DE_ERR_HIP;
+  de::TopkUnionArgs a{};
+  a.T = T;
+  a.N = d->n_experts;
+  a.k = d->top_k;
+  a.z = z;
+  a.bias = bias;
+  a.score_func = d->score_func;
+  a.norm_topk = d->norm_topk;
+  a.routed_scale = d->routed_scale;
+  a.idx_out = topk_idx;
+  a.gate_out = topk_gate;
+  a.ucols = d->top_k;
+  return hip_status(de::launch_topk_union(a, stream));
+}
+
+int de_expert_union(int T, int k, int N, const int32_t* topk_idx, const float* topk_gate,
+                    int32_t* n_union, int32_t* union_ids, int32_t* offsets, int32_t* tok_list,
+                    float* gate_list, int32_t* pair_pos, hipStream_t stream) {
+  if (check_T(T) != DE_OK || N < 1 || N > kMaxN || k < 1 || k > kMaxK || k > N)
+    return DE_ERR_INVALID;
+  if (!topk_idx || !topk_gate || !n_union || !union_ids || !offsets || !tok_list || !gate_list ||
+      !pair_pos)
+    return DE_ERR_INVALID;
+  de::TopkUnionArgs a{};
+  a.T = T;
+  a.N = N;
+  a.k = k;
+  a.z = nullptr;
+  a.idx_in = topk_idx;
+  a.gate_in = topk_gate;
+  a.ucols = k;
+  a.n_union = n_union;
+  a.union_ids = union_ids;
+  a.offsets = offsets;
+  a.tok_list = tok_list;
+  a.gate_list = gate_list;
+  a.pair_pos = pair_pos;
+  return hip_status(de::launch_topk_union(a, stream));
+}
+
+int de_grouped_swiglu(const de_moe_desc* d, int T, const float* x, const de_expert_table* routed,
+                      const int32_t* n_union, const int32_t* union_ids, const int32_t* offsets,
+                      const int32_t* tok_list, const float* gate_list, const int32_t* pair_pos,
+                      const void* shared_w, float* y, const de_epilogue* epi, void* ws,
+                      size_t ws_bytes, hipStream_t stream) {
+  int rc = de_check_desc(d);
+  if (rc != DE_OK) return rc;
+  if ((rc = check_T(T)) != DE_OK) return rc;
+  if (!x || !y || !n_union || !union_ids || !offsets || !tok_list || !gate_list || !pair_pos)
+    return DE_ERR_INVALID;
+  if (!aligned16(x)) return DE_ERR_INVALID;
+  if (d->shared_inter > 0 && (shared_w == nullptr || !aligned16(shared_w))) return DE_ERR_INVALID;
+  if ((rc = check_table(*d, routed)) != DE_OK) return rc;
+  if ((rc = check_epi(epi)) != DE_OK) return rc;
+  if ((rc = check_ws(*d, T, ws, ws_bytes)) != DE_OK) return rc;
+  const Layout L = layout(*d, T);
+  const de::RoutedSrc r = routed_src(*d, T, routed, n_union, union_ids, offsets, tok_list, gate_list,
+                                     at<float>(ws, L.a_r), at<float>(ws, L.p_r));
+  return run_grouped(*d, T, x, r, pair_pos, d->top_k, shared_w, nullptr, 0.f, y, epi, L, ws,
+                     stream);
+}
+
+int de_draft_layer(const de_moe_desc* d, int T, const float* x, const float* w_router,
+                   const float* bias, const de_expert_table* routed, const void* shared_w,
+                   const void* draft_w, float gamma, float* y, int32_t* pred_idx,
+                   float* pred_gate, const de_epilogue* epi, void* ws, size_t ws_bytes,
+                   hipStream_t stream) {
+  int rc = de_check_desc(d);
+  if (rc != DE_OK) return rc;
+  if ((rc = check_T(T)) != DE_OK) return rc;
+  if (!x || !w_router || !y || !aligned16(x) || !aligned16(w_router) || d->hidden % 4)
+    return DE_ERR_INVALID;
+  if (d->shared_inter > 0 && (shared_w == nullptr || !aligned16(shared_w))) return DE_ERR_INVALID;
+  if (draft_w != nullptr && !aligned16(draft_w)) return DE_ERR_INVALID;
+  if (!std::isfinite(gamma)) return DE_ERR_INVALID;
+  if ((rc = check_table(*d, routed)) != DE_OK) return rc;
+  if ((rc = check_epi(epi)) != DE_OK) return rc;
+  if ((rc = check_ws(*d, T, ws, ws_bytes)) != DE_OK) return rc;
+  const Layout L = layout(*d, T);
+  float* z = at<float>(ws, L.z);
+  if (de::launch_router_logits(x, w_router, T, d->hidden, d->n_experts, z, stream) != hipSuccess)
+    return DE_ERR_HIP;
+  de::TopkUnionArgs a{};
+  a.T = T;
+  a.N = d->n_experts;
+  a.k = d->top_k;
+  a.z = z;
+  a.bias = bias;
+  a.score_func = d->score_func;
+  a.norm_topk = d->norm_topk;
+  a.routed_scale = d->routed_scale;
+  a.idx_out = pred_idx ? pred_idx : at<int32_t>(ws, L.idx);
+  a.gate_out = pred_gate ? pred_gate : at<float>(ws, L.gate);
+  a.ucols = 1;  // the drafter reads only the top-1 expert of each position
+  a.n_union = at<int32_t>(ws, L.nu);
+  a.union_ids = at<int32_t>(ws, L.uids);
+  a.offsets = at<int32_t>(ws, L.offs);
+  a.tok_list = at<int32_t>(ws, L.tok);
+  a.gate_list = at<float>(ws, L.glist);
+  a.pair_pos = at<int32_t>(ws, L.ppos);
+  if (de::launch_topk_union(a, stream) != hipSuccess) return DE_ERR_HIP;
+  const de::RoutedSrc r = routed_src(*d, T, routed, a.n_union, a.union_ids, a.offsets, a.tok_list,
+                                     a.gate_list, at<float>(ws, L.a_r), at<float>(ws, L.p_r));
+  return run_grouped(*d, T, x, r, a.pair_pos, 1, shared_w, draft_w, gamma, y, epi, L, ws, stream);
+}
+
+int de_verify_layer(const de_moe_desc* d, int T, const float* x, const float* w_router,
+                    const float* bias, const de_expert_table* routed, const void* shared_w,
+                    float* y, int32_t* topk_idx, float* topk_gate, int32_t* n_union,
+                    int32_t* union_ids, int32_t* offsets, int32_t* tok_list, float* gate_list,
+                    int32_t* pair_pos, const de_epilogue* epi, void* ws, size_t ws_bytes,
+                    hipStream_t stream) {
+  int rc = de_check_desc(d);
+  if (rc != DE_OK) return rc;
+  if ((rc = check_T(T)) != DE_OK) return rc;
+  if (!x || !w_router || !y || !aligned16(x) || !aligned16(w_router) || d->hidden % 4)
+    return DE_ERR_INVALID;
+  if (d->shared_inter > 0 && (shared_w == nullptr || !aligned16(shared_w))) return DE_ERR_INVALID;
+  if ((rc = check_table(*d, routed)) != DE_OK) return rc;
+  if ((rc = check_epi(epi)) != DE_OK) return rc;
+  if ((rc = check_ws(*d, T, ws, ws_bytes)) != DE_OK) return rc;
+  const Layout L = layout(*d, T);
+  float* z = at<float>(ws, L.z);
+  if (de::launch_router_logits(x, w_router, T, d->hidden, d->n_experts, z, stream) != hipSuccess)
+    return DE_ERR_HIP;
+  de::TopkUnionArgs a{};
+  a.T = T;
+  a.N = d->n_experts;
+  a.k = d->top_k;
+  a.z = z;
+  a.bias = bias;
+  a.score_func = d->score_func;
+  a.norm_topk = d->norm_topk;
+  a.routed_scale = d->routed_scale;
+  a.idx_out = topk_idx ? topk_idx : at<int32_t>(ws, L.idx);
+  a.gate_out = topk_gate ? topk_gate : at<float>(ws, L.gate);
+  a.ucols = d->top_k;
+  a.n_union = n_union ? n_union : at<int32_t>(ws, L.nu);
+  a.union_ids = union_ids ? union_ids : at<int32_t>(ws, L.uids);
+  a.offsets = offsets ? offsets : at<int32_t>(ws, L.offs);
+  a.tok_list = tok_list ? tok_list : at<int32_t>(ws, L.tok);
+  a.gate_list = gate_list ? gate_list : at<float>(ws, L.glist);
+  a.pair_pos = pair_pos ? pair_pos : at<int32_t>(ws, L.ppos);
+  if (de::launch_topk_union(a, stream) != hipSuccess) return DE_ERR_HIP;
+  const de::RoutedSrc r = routed_src(*d, T, routed, a.n_union, a.union_ids, a.offsets, a.tok_list,
+                                     a.gate_list, at<float>(ws, L.a_r), at<float>(ws, L.p_r));
+  return run_grouped(*d, T, x, r, a.pair_pos, d->top_k, shared_w, nullptr, 0.f, y, epi, L, ws,
+                     stream);
+}
+
+int de_accept_len(int K, int V, const float* target_logits, const int32_t* draft_tokens,
+                  int32_t* target_argmax, int32_t* out, hipStream_t stream) {
+  if (K < 0 || K > 1024 || V < 1 || !target_logits || !target_argmax || !out) return DE_ERR_INVALID;
+  if (K > 0 && draft_tokens == nullptr) return DE_ERR_INVALID;
+  if (de::launch_argmax_rows(target_logits, K + 1, V, target_argmax, stream) != hipSuccess)
+    return DE_ERR_HIP;
+  return hip_status(de::launch_accept(K, target_argmax, draft_tokens, out, stream));
+}
+
+int de_lm_head(int T, int H, int V, const float* x, const void* w_lm, float* logits,
+               hipStream_t stream) {
+  if (check_T(T) != DE_OK || H < 8 || H % 8 || V < 1 || !x || !w_lm || !logits) return DE_ERR_INVALID;
+  if (!aligned16(x) || !aligned16(w_lm)) return DE_ERR_INVALID;
+  de::GroupedArgs g{};
+  g.T = T;
+  g.H = H;
+  g.x = x;
+  g.has_routed = 0;
+  g.n_dense = 1;
+  g.dense[0].w = w_lm;
+  g.dense[0].inter = H;
+  g.dense[0].rows = V;
+  g.dense[0].gate = 1.0f;
+  g.dense[0].vin = x;
+  g.dense[0].vin_stride = H;
+  g.dense[0].out = logits;
+  g.dense[0].out_stride = V;
+  return hip_status(de::launch_down(g, DE_BF16, stream));
+}
+
+int de_rmsnorm(int T, int H, const float* x, float eps, float* out, hipStream_t stream) {
+  if (T < 1 || T > 65536 || H < 1 || !x || !out || !(eps >= 0.f)) return DE_ERR_INVALID;
+  return hip_status(de::launch_rmsnorm(T, H, x, eps, out, stream));
+}
+
+int de_embed_gather(int T, int H, int V, const int32_t* tokens, const void* emb, float* h,
+                    float* normed, float eps, hipStream_t stream) {
+  if (T < 1 || T > 65536 || H < 1 || V < 1 || !tokens || !emb || !h || !(eps >= 0.f))
+    return DE_ERR_INVALID;
+  return hip_status(de::launch_embed(T, H, V, tokens, static_cast<const uint16_t*>(emb), h, normed,
+                                     eps, stream));
+}
+
+size_t de_dense_workspace_bytes(int T, int H, int I) {
+  if (check_T(T) != DE_OK || H < 1 || I < 1) return 0;
+  return up256((size_t)T * I * 4) + up256((size_t)T * H * 4);
+}
+
+int de_dense_swiglu(int T, int H, int I, int wdtype, const float* x, const void* w, float* y,
+                    const de_epilogue* epi, void* ws, size_t ws_bytes, hipStream_t stream) {
+  if (wdtype != DE_F32 && wdtype != DE_BF16) return DE_ERR_UNSUPPORTED;
+  const int al = elem_align(wdtype);
+  if (check_T(T) != DE_OK || H < al || H % al || I < al || I % al || I > (1 << 17))
+    return DE_ERR_INVALID;
+  if (!x || !w || !y || !aligned16(x) || !aligned16(w)) return DE_ERR_INVALID;
+  if (check_epi(epi) != DE_OK) return DE_ERR_INVALID;
+  if (ws == nullptr || (reinterpret_cast<uintptr_t>(ws) & 255u) != 0 ||
+      ws_bytes < de_dense_workspace_bytes(T, H, I))
+    return DE_ERR_WORKSPACE;
+  float* A = static_cast<float*>(ws);
+  float* P = at<float>(ws, up256((size_t)T * I * 4));
+  de::GroupedArgs g{};
+  g.T = T;
+  g.H = H;
+  g.x = x;
+  g.has_routed = 0;
+  g.n_dense = 1;
+  g.dense[0].w = w;
+  g.dense[0].inter = I;
+  g.dense[0].out = A;
+  if (de::launch_gateup(g, wdtype, stream) != hipSuccess) return DE_ERR_HIP;
+  g.dense[0].w = static_cast<const char*>(w) + 2 * (size_t)I * H * elem_bytes(wdtype);
+  g.dense[0].rows = H;
+  g.dense[0].gate = 1.0f;
+  g.dense[0].vin = A;
+  g.dense[0].vin_stride = I;
+  g.dense[0].out = P;
+  g.dense[0].out_stride = H;
+  if (de::launch_down(g, wdtype, stream) != hipSuccess) return DE_ERR_HIP;
+  de::CombineArgs c{};
+  c.T = T;
+  c.H = H;
+  c.n_dense = 1;
+  c.dense_p[0] = P;
+  c.y = y;
+  c.residual = epi ? epi->residual : nullptr;
+  c.normed = epi ? epi->normed : nullptr;
+  c.eps = epi ? epi->eps : 0.f;
+  return hip_status(de::launch_combine(c, stream));
+}
+
+int de_stream_probe(const void* buf, size_t bytes, float* sink, hipStream_t stream) {
+  if (!buf || !sink || bytes == 0 || bytes % 16 || !aligned16(buf)) return DE_ERR_INVALID;
+  return hip_status(de::launch_stream_probe(buf, bytes, sink, stream));
+}
+
+}  // extern "C"

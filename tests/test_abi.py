@@ -1,0 +1,138 @@
+"""The C ABI loads, exports every declared symbol, and rejects bad calls on the host.
+
+No call here reaches a HIP API: every case fails argument validation first,
+so the suite runs without a GPU.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2607_24434_amd as de
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "draftexpert.h")
+
+FAKE = 0x7F0000000000  # aligned, never dereferenced (validation fails first)
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(de_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    names = declared_functions()
+    assert len(names) >= 14
+    lib = ctypes.CDLL(de.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(names) == set(de.C_FUNCS)
+
+
+def test_version_and_error_strings():
+    assert de.de_abi_version() == 1
+    for code in (0, -1, -2, -3, -4, -5):
+        assert de.de_error_string(code) != "unknown error code"
+    assert de.de_error_string(42) == "unknown error code"
+
+
+def cfg2_desc(**kw):
+    base = dict(hidden=2048, n_experts=64, top_k=6, inter=1408, shared_inter=2816,
+                draft_inter=1408, score_func=de.DE_SOFTMAX, norm_topk=0, routed_scale=1.0,
+                wdtype=de.DE_BF16)
+    base.update(kw)
+    return de.make_desc(**base)
+
+
+@pytest.mark.parametrize("kw,code", [
+    ({}, 0),
+    ({"wdtype": 7}, -2),
+    ({"score_func": 5}, -2),
+    ({"n_experts": 0}, -1),
+    ({"n_experts": 257}, -1),
+    ({"top_k": 0}, -1),
+    ({"top_k": 65}, -1),
+    ({"top_k": 33, "n_experts": 64}, -1),
+    ({"hidden": 2044}, -1),           # not a multiple of 8 for bf16
+    ({"hidden": 2044, "wdtype": de.DE_F32}, 0),
+    ({"inter": 1404}, -1),
+    ({"shared_inter": -8}, -1),
+    ({"draft_inter": 0}, 0),
+    ({"norm_topk": 2}, -1),
+    ({"routed_scale": float("inf")}, -1),
+])
+def test_check_desc(kw, code):
+    d = cfg2_desc(**kw)
+    d.norm_topk = kw.get("norm_topk", d.norm_topk)
+    assert de.de_check_desc(d) == code
+
+
+def test_workspace_bytes():
+    d = cfg2_desc()
+    sizes = [de.de_workspace_bytes(d, T) for T in (1, 5, 9, 17, 64)]
+    assert all(s > 0 for s in sizes) and sizes == sorted(sizes)
+    assert de.de_workspace_bytes(d, 0) == 0 and de.de_workspace_bytes(d, 65) == 0
+    assert de.de_workspace_bytes(cfg2_desc(n_experts=0), 9) == 0
+    # A_r + P_r + shared/draft activations dominate: T*k*(I+H)*4 + T*(Is+Id+2H)*4
+    assert sizes[2] >= 9 * 6 * (1408 + 2048) * 4 + 9 * (2816 + 1408 + 2 * 2048) * 4
+
+
+def raw_verify(d, T, x=FAKE, w=FAKE, y=FAKE, table=None, ws=FAKE, ws_bytes=1 << 30, epi=None):
+    if table is None:
+        table = de.make_table(FAKE, 3 * 1408 * 2048 * 2, None, 64)
+    return de.LIB.de_verify_layer(ctypes.byref(d), T, x, w, None, ctypes.byref(table), FAKE, y,
+                                  None, None, None, None, None, None, None, None,
+                                  None if epi is None else ctypes.byref(epi), ws, ws_bytes, None)
+
+
+def test_verify_layer_rejects_bad_arguments_on_host():
+    d = cfg2_desc()
+    assert raw_verify(d, 0) == -1
+    assert raw_verify(d, 65) == -1
+    assert raw_verify(d, 9, x=None) == -1
+    assert raw_verify(d, 9, x=FAKE + 4) == -1          # misaligned activations
+    assert raw_verify(d, 9, y=None) == -1
+    assert raw_verify(d, 9, ws=None) == -4
+    assert raw_verify(d, 9, ws=FAKE + 16) == -4        # ws must be 256-B aligned
+    assert raw_verify(d, 9, ws_bytes=1024) == -4
+    assert raw_verify(d, 9, table=de.make_table(FAKE, 1024, None, 64)) == -1   # stride too small
+    assert raw_verify(d, 9, table=de.make_table(FAKE + 8, 3 * 1408 * 2048 * 2, None, 64)) == -1
+    assert raw_verify(d, 9, table=de.make_table(FAKE, 3 * 1408 * 2048 * 2, None, 32)) == -1
+    assert raw_verify(cfg2_desc(wdtype=9), 9) == -2
+    bad_epi = de.Epilogue(None, FAKE, float("nan"))
+    assert raw_verify(d, 9, epi=bad_epi) == -1
+
+
+def test_other_entry_points_reject_bad_arguments_on_host():
+    L = de.LIB
+    d = cfg2_desc()
+    tab = de.make_table(FAKE, 3 * 1408 * 2048 * 2, None, 64)
+    assert L.de_route_topk(ctypes.byref(d), 9, None, FAKE, None, FAKE, FAKE, FAKE, 1 << 30, None) == -1
+    assert L.de_route_topk(ctypes.byref(d), 9, FAKE, FAKE, None, FAKE, FAKE, FAKE, 16, None) == -4
+    assert L.de_expert_union(0, 6, 64, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None) == -1
+    assert L.de_expert_union(9, 6, 64, None, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None) == -1
+    assert L.de_expert_union(9, 7, 6, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None) == -1
+    assert L.de_grouped_swiglu(ctypes.byref(d), 9, FAKE, ctypes.byref(tab), None, FAKE, FAKE, FAKE,
+                               FAKE, FAKE, FAKE, FAKE, None, FAKE, 1 << 30, None) == -1
+    assert L.de_draft_layer(ctypes.byref(d), 1, FAKE, FAKE, None, ctypes.byref(tab), FAKE, FAKE,
+                            float("nan"), FAKE, None, None, None, FAKE, 1 << 30, None) == -1
+    assert L.de_accept_len(-1, 10, FAKE, FAKE, FAKE, FAKE, None) == -1
+    assert L.de_accept_len(3, 10, FAKE, None, FAKE, FAKE, None) == -1
+    assert L.de_accept_len(0, 0, FAKE, None, FAKE, FAKE, None) == -1
+    assert L.de_lm_head(9, 2044, 1000, FAKE, FAKE, FAKE, None) == -1
+    assert L.de_rmsnorm(0, 16, FAKE, 1e-6, FAKE, None) == -1
+    assert L.de_embed_gather(1, 16, 0, FAKE, FAKE, FAKE, None, 1e-6, None) == -1
+    assert L.de_dense_swiglu(9, 2048, 10944, 3, FAKE, FAKE, FAKE, None, FAKE, 1 << 30, None) == -2
+    assert L.de_dense_swiglu(9, 2048, 10944, 1, FAKE, FAKE, FAKE, None, FAKE, 64, None) == -4
+    assert L.de_stream_probe(FAKE, 100, FAKE, None) == -1
+    assert de.de_dense_workspace_bytes(9, 2048, 10944) >= 9 * (10944 + 2048) * 4
+
+
+def test_binding_raises_on_error_codes():
+    d = cfg2_desc(n_experts=0)
+    with pytest.raises(de.DEError) as ei:
+        de._lib._check("de_verify_layer", raw_verify(d, 9))
+    assert ei.value.code == -1

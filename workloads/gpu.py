@@ -1,0 +1,97 @@
+"""Device-side fills of the synthetic streams (bit-identical to ``workloads.rng``).
+
+Large weight sets (a 64-expert layer is 1.1 GB in bf16, a 26-layer model
+29 GB) are drawn directly in HBM by ``libdesynth.so`` instead of being copied
+from the host.  Small tensors (activations, routers, biases) come from the
+CPU generator and are copied.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+import torch
+
+from . import gen, rng
+from .configs import BF16, MoECfg, ModelCfg
+
+_LIB = None
+
+
+def _lib():
+    global _LIB
+    if _LIB is None:
+        path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libdesynth.so")
+        if not os.path.exists(path):
+            raise ImportError(f"{path} is missing: build it with `python -m workloads.build`")
+        lib = ctypes.CDLL(path)
+        lib.synth_fill_normal.restype = ctypes.c_int
+        lib.synth_fill_normal.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int,
+                                          ctypes.c_uint64, ctypes.c_uint64, ctypes.c_double,
+                                          ctypes.c_void_p]
+        _LIB = lib
+    return _LIB
+
+
+def fill_normal(out: torch.Tensor, key: int, std: float, start: int = 0) -> torch.Tensor:
+    """Fill a contiguous device tensor (float32, or uint16/int16 holding bf16 bits)."""
+    assert out.is_cuda and out.is_contiguous()
+    bf16 = out.dtype in (torch.int16, torch.uint16, torch.bfloat16)
+    assert bf16 or out.dtype == torch.float32
+    rc = _lib().synth_fill_normal(out.data_ptr(), out.numel(), int(bf16), key, start,
+                                  float(std) / rng.IH_STD, torch.cuda.current_stream().cuda_stream)
+    if rc != 0:
+        raise RuntimeError(f"synth_fill_normal failed ({rc})")
+    return out
+
+
+def _wtensor(n: int, wdtype: int, device) -> torch.Tensor:
+    return torch.empty(n, dtype=torch.int16 if wdtype == BF16 else torch.float32, device=device)
+
+
+def routed_experts(cfg: MoECfg, layer: int, device="cuda", redraw: int = 0,
+                   n_experts: int | None = None) -> torch.Tensor:
+    """[N, 3*I*H] expert blocks, expert e in row e (the resident layout)."""
+    n = cfg.n_experts if n_experts is None else n_experts
+    out = _wtensor(n * cfg.expert_elems(), cfg.wdtype, device).view(n, -1)
+    for e in range(n):
+        fill_normal(out[e], rng.key_for(cfg.cfg_id, redraw, "routed", layer, e), cfg.weight_std)
+    return out
+
+
+def shared_block(cfg: MoECfg, layer: int, device="cuda", redraw: int = 0) -> torch.Tensor:
+    out = _wtensor(cfg.expert_elems(cfg.shared_inter), cfg.wdtype, device)
+    return fill_normal(out, rng.key_for(cfg.cfg_id, redraw, "shared", layer, 0), cfg.weight_std)
+
+
+def draft_block(cfg: MoECfg, layer: int, device="cuda", redraw: int = 0) -> torch.Tensor:
+    out = _wtensor(cfg.expert_elems(cfg.draft_inter), cfg.wdtype, device)
+    return fill_normal(out, rng.key_for(cfg.cfg_id, redraw, "draft", layer, 0), cfg.weight_std)
+
+
+def dense_block(model: ModelCfg, device="cuda", redraw: int = 0) -> torch.Tensor:
+    out = _wtensor(3 * model.dense_inter * model.moe.hidden, BF16, device)
+    return fill_normal(out, rng.key_for(model.cfg_id, redraw, "dense", 0, 0), model.moe.weight_std)
+
+
+def embedding(model: ModelCfg, device="cuda", redraw: int = 0) -> torch.Tensor:
+    out = _wtensor(model.vocab * model.moe.hidden, BF16, device).view(model.vocab, -1)
+    return fill_normal(out, rng.key_for(model.cfg_id, redraw, "emb", 0, 0), model.emb_std)
+
+
+def lm_head(cfg_id: int, vocab: int, hidden: int, std: float = 0.02, device="cuda",
+            redraw: int = 0) -> torch.Tensor:
+    out = torch.empty(vocab * hidden, dtype=torch.int16, device=device).view(vocab, hidden)
+    return fill_normal(out, rng.key_for(cfg_id, redraw, "lm", 0, 0), std)
+
+
+def to_device(a: np.ndarray, device="cuda") -> torch.Tensor:
+    a = np.ascontiguousarray(a)
+    if a.dtype == np.uint16:
+        a = a.view(np.int16)
+    return torch.from_numpy(a).to(device)
+
+
+def router(cfg: MoECfg, layer: int, device="cuda", redraw: int = 0) -> torch.Tensor:
+    return to_device(gen.router_weight(cfg, layer, redraw), device)

@@ -27,6 +27,10 @@ This module holds no arithmetic of the method itself: it only draws numbers.
 """
 from __future__ import annotations
 
+import ctypes
+import os
+from concurrent.futures import ThreadPoolExecutor
+
 import numpy as np
 
 MASK64 = (1 << 64) - 1
@@ -88,8 +92,8 @@ def raw_bits(key: int, start: int, n: int) -> np.ndarray:
         return _mix64(z)
 
 
-def normal_f32(key: int, n: int, std: float, start: int = 0) -> np.ndarray:
-    """n approximately N(0, std^2) fp32 values from stream ``key``."""
+def normal_f32_ref(key: int, n: int, std: float, start: int = 0) -> np.ndarray:
+    """n approximately N(0, std^2) fp32 values from stream ``key`` (NumPy definition)."""
     out = np.empty(n, dtype=np.float32)
     chunk = 1 << 22
     scale = float(std) / IH_STD
@@ -115,9 +119,63 @@ def bf16_bits_to_f32(b: np.ndarray) -> np.ndarray:
     return (np.ascontiguousarray(b, dtype=np.uint16).astype(np.uint32) << np.uint32(16)).view(np.float32)
 
 
+def normal_bf16_ref(key: int, n: int, std: float, start: int = 0) -> np.ndarray:
+    """bf16 bits of normal_f32_ref (NumPy definition)."""
+    return f32_to_bf16_bits(normal_f32_ref(key, n, std, start))
+
+
+# ---- fast path: the same streams from a small C library, run on several threads
+
+_CLIB = None
+_THREADS = max(1, min(16, len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else 4))
+
+
+def _clib():
+    global _CLIB
+    if _CLIB is None:
+        path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libdesynth_cpu.so")
+        if not os.path.exists(path):
+            _CLIB = False
+        else:
+            lib = ctypes.CDLL(path)
+            for name in ("synth_normal_f32", "synth_normal_bf16"):
+                fn = getattr(lib, name)
+                fn.restype = None
+                fn.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_uint64, ctypes.c_uint64,
+                               ctypes.c_double]
+            _CLIB = lib
+    return _CLIB
+
+
+def _fill_c(fn, out: np.ndarray, key: int, std: float, start: int):
+    n = out.size
+    scale = float(std) / IH_STD
+    esz = out.itemsize
+    base = out.ctypes.data
+    chunk = 1 << 20
+    spans = [(c0, min(n, c0 + chunk)) for c0 in range(0, n, chunk)]
+    if len(spans) <= 1:
+        fn(base, n, key, start, scale)
+        return out
+    with ThreadPoolExecutor(max_workers=_THREADS) as ex:
+        list(ex.map(lambda sp: fn(base + sp[0] * esz, sp[1] - sp[0], key, start + sp[0], scale), spans))
+    return out
+
+
+def normal_f32(key: int, n: int, std: float, start: int = 0) -> np.ndarray:
+    """n approximately N(0, std^2) fp32 values from stream ``key``."""
+    lib = _clib()
+    if not lib:
+        return normal_f32_ref(key, n, std, start)
+    return _fill_c(lib.synth_normal_f32, np.empty(n, dtype=np.float32), key, std, start)
+
+
 def normal_bf16(key: int, n: int, std: float, start: int = 0) -> np.ndarray:
     """n approximately N(0, std^2) values, rounded to bf16, as uint16 bits."""
-    return f32_to_bf16_bits(normal_f32(key, n, std, start))
+    lib = _clib()
+    if not lib:
+        return normal_bf16_ref(key, n, std, start)
+    return _fill_c(lib.synth_normal_bf16, np.empty(n, dtype=np.uint16), key, std, start)
 
 
 def uniform_int(key: int, n: int, high: int, start: int = 0) -> np.ndarray:
