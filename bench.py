@@ -1,0 +1,293 @@
+#!/usr/bin/env python3
+"""Benchmark of the DraftExpert MoE draft/verify hot path on one MI355X.
+
+Workload: one DeepSeek-V2-Lite-shaped MoE layer (H=2048, 64 routed SwiGLU
+experts of I=1408, 2 shared experts, softmax top-6, bf16 expert weights, fp32
+router, one draft expert of I=1408) with K=8 drafts.  One step is the whole hot
+path over one block:
+
+  * 8 draft-layer passes (Eq. 5), one position each;
+  * one verify-layer pass over the 9-position block (Eq. 4: routing, union,
+    grouped SwiGLU over the union, shared path);
+  * the 102400-vocab bf16 LM head over the 8 draft positions and the 9 verify
+    positions (teacher-forced, RMSNorm(x + y) as in a one-layer model) and the
+    greedy accept length (Algorithm 1).
+
+Weights are drawn in HBM before timing.  Every layer call in a step uses a
+different copy of the layer weights (8 copies rotated), so no call finds its
+weights in the 256 MB Infinity Cache left behind by the previous one.
+
+Reported: ``value`` = achieved GB/s over the union expert weights of the verify
+layer (n_union x 17,301,504 B / verify-layer time), plus per-stage times, a
+``roofline`` object for the dominant kernel (the grouped gate/up GEMV of the
+verify layer, timed live with HIP events around its launch) and the CPU
+oracle's rate on the host cores.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import statistics
+import sys
+import time
+
+METRIC = "verify-layer µs + achieved HBM GB/s over union expert weights (K=8, V2-Lite shape)"
+PEAK_HBM_GBS = 8000.0
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=30)
+    p.add_argument("--warmup", type=int, default=5)
+    p.add_argument("--copies", type=int, default=8)
+    p.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    p.add_argument("--cpu-seconds", type=float, default=12.0)
+    p.add_argument("--no-probe", action="store_true", help="skip the HBM read-ceiling probe")
+    return p.parse_args()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU: --gpus {args.gpus} is not supported (this build has no "
+              f"multi-GPU path; see the sharding notes in DESIGN.md)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2607_24434_amd as de
+    from workloads import configs, gen
+    from workloads import gpu as wgpu
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a HIP device", file=sys.stderr)
+        sys.exit(1)
+    torch.cuda.set_device(0)
+    dev = "cuda"
+    cfg = configs.CFG2
+    K = 8
+    T = K + 1
+    H = cfg.hidden
+    V = configs.CFG4.vocab
+    R = args.copies
+
+    desc = de.make_desc(H, cfg.n_experts, cfg.top_k, cfg.inter, cfg.shared_inter,
+                        cfg.draft_inter, cfg.score_func, cfg.norm_topk, cfg.routed_scale,
+                        cfg.wdtype)
+    stride = cfg.expert_bytes()
+    copies = []
+    for c in range(R):
+        routed = wgpu.routed_experts(cfg, 0, dev, redraw=c)
+        copies.append(dict(
+            routed=routed,
+            table=de.make_table(routed, stride, None, cfg.n_experts),
+            shared=wgpu.shared_block(cfg, 0, dev, redraw=c),
+            draft=wgpu.draft_block(cfg, 0, dev, redraw=c),
+            router=wgpu.router(cfg, 0, dev, redraw=c),
+        ))
+    w_lm = wgpu.lm_head(configs.CFG4.cfg_id, V, H, configs.CFG4.lm_std, dev)
+    x_ver = wgpu.to_device(gen.x_rows(cfg, T, block=0), dev)
+    x_dr = wgpu.to_device(gen.x_rows(cfg, K, block=1), dev)
+
+    ws = de.workspace(desc, T, dev)
+    aws = de.accept_workspace(K, V, dev)
+    y_dr = torch.empty(K, H, dtype=torch.float32, device=dev)
+    n_dr = torch.empty(K, H, dtype=torch.float32, device=dev)
+    pred = torch.empty(K, cfg.top_k, dtype=torch.int32, device=dev)
+    y_ver = torch.empty(T, H, dtype=torch.float32, device=dev)
+    n_ver = torch.empty(T, H, dtype=torch.float32, device=dev)
+    lg_dr = torch.empty(K, V, dtype=torch.float32, device=dev)
+    lg_ver = torch.empty(T, V, dtype=torch.float32, device=dev)
+    dtok = torch.empty(K, dtype=torch.int32, device=dev)
+    tmax = torch.empty(T, dtype=torch.int32, device=dev)
+    acc_dummy = torch.empty(2, dtype=torch.int32, device=dev)
+    total = args.warmup + args.steps
+    nu_all = torch.zeros(total, dtype=torch.int32, device=dev)
+    acc_all = torch.zeros(total, 2, dtype=torch.int32, device=dev)
+    zero_tok = torch.zeros(K, dtype=torch.int32, device=dev)
+
+    def ev():
+        e = torch.cuda.Event(enable_timing=True)
+        e.record()
+        return e
+
+    def step(s, evs):
+        base = s * (K + 1)
+        evs["s0"].record()
+        for i in range(K):
+            cp = copies[(base + i) % R]
+            epi = de.make_epilogue(residual=x_dr[i:i + 1], normed=n_dr[i:i + 1])
+            de.de_draft_layer(desc, 1, x_dr[i:i + 1], cp["router"], None, cp["table"], cp["shared"],
+                              cp["draft"], cfg.gamma, y_dr[i:i + 1], pred[i:i + 1], None, ws, epi=epi)
+        evs["d1"].record()
+        de.de_lm_head(K, H, V, n_dr, w_lm, lg_dr)
+        de.de_accept_len(K - 1, V, lg_dr, zero_tok, dtok, acc_dummy, aws)  # row argmax = drafts
+        evs["v0"].record()
+        cp = copies[(base + K) % R]
+        de.de_time_next_phase(de.DE_PHASE_GATEUP, evs["g0"], evs["g1"])
+        de.de_time_next_phase(de.DE_PHASE_DOWN, evs["p0"], evs["p1"])
+        de.de_verify_layer(desc, T, x_ver, cp["router"], None, cp["table"], cp["shared"], y_ver,
+                           n_union=nu_all[s:s + 1], ws=ws,
+                           epi=de.make_epilogue(residual=x_ver, normed=n_ver))
+        evs["v1"].record()
+        de.de_lm_head(T, H, V, n_ver, w_lm, lg_ver)
+        de.de_accept_len(K, V, lg_ver, dtok, tmax, acc_all[s], aws)
+        evs["s1"].record()
+
+    names = ["s0", "d1", "v0", "v1", "s1", "g0", "g1", "p0", "p1"]
+    for s in range(args.warmup):
+        step(s, {n: ev() for n in names})
+    torch.cuda.synchronize()
+
+    rec = [{n: ev() for n in names} for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t_wall0 = time.perf_counter()
+    for i in range(args.steps):
+        step(args.warmup + i, rec[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_wall0
+
+    nu = nu_all[args.warmup:].cpu().numpy().astype(np.int64)
+    accs = acc_all[args.warmup:].cpu().numpy()
+    step_ms = [r["s0"].elapsed_time(r["s1"]) for r in rec]
+    draft_ms = [r["s0"].elapsed_time(r["d1"]) / K for r in rec]
+    ver_ms = [r["v0"].elapsed_time(r["v1"]) for r in rec]
+    gu_ms = [r["g0"].elapsed_time(r["g1"]) for r in rec]
+    dn_ms = [r["p0"].elapsed_time(r["p1"]) for r in rec]
+
+    eb = stride
+    union_bytes = nu * eb
+    value = float(union_bytes.sum() / (sum(ver_ms) * 1e-3) / 1e9)
+    # Algorithmic bytes of one gate/up launch: G and U of every union expert and
+    # of the shared path, the block's activations read once and A written once.
+    gu_bytes = (nu * 2 * cfg.inter * H * 2 + 2 * cfg.shared_inter * H * 2 + T * H * 4
+                + (T * cfg.top_k * cfg.inter + T * cfg.shared_inter) * 4)
+    gu_gbs = float(gu_bytes.sum() / (sum(gu_ms) * 1e-3) / 1e9)
+    dn_bytes = (nu * cfg.inter * H * 2 + cfg.shared_inter * H * 2
+                + (T * cfg.top_k * cfg.inter + T * cfg.shared_inter) * 4 + (T * cfg.top_k + T) * H * 4)
+    dn_gbs = float(dn_bytes.sum() / (sum(dn_ms) * 1e-3) / 1e9)
+
+    probe_gbs = None
+    if not args.no_probe:
+        nbytes = 4 << 30
+        buf = torch.empty(nbytes // 2, dtype=torch.int16, device=dev)
+        wgpu.fill_normal(buf, 12345, 1.0)
+        sink = torch.zeros(1, dtype=torch.float32, device=dev)
+        for _ in range(2):
+            de.de_stream_probe(buf, nbytes, sink)
+        e0, e1 = ev(), ev()
+        reps = 10
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(reps):
+            de.de_stream_probe(buf, nbytes, sink)
+        e1.record()
+        torch.cuda.synchronize()
+        probe_gbs = nbytes * reps / (e0.elapsed_time(e1) * 1e-3) / 1e9
+        del buf
+
+    cpu = None
+    if not args.no_cpu:
+        cpu = cpu_baseline(cfg, gen.x_rows(cfg, T, block=0), args.cpu_seconds)
+
+    med = statistics.median
+    out = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(med(step_ms), 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": "v2lite-moe-layer-K8: H=2048, 64 routed + 2 shared SwiGLU experts (I=1408), "
+                        "softmax top-6, draft expert I=1408, bf16 expert weights, fp32 router and "
+                        "activations; 8 draft positions + 9-position verify block; 102400-vocab bf16 "
+                        "LM head; 8 rotated weight copies",
+            "hidden": H, "n_experts": cfg.n_experts, "top_k": cfg.top_k, "inter": cfg.inter,
+            "shared_inter": cfg.shared_inter, "draft_inter": cfg.draft_inter, "k_draft": K,
+            "verify_block": T, "vocab": V, "weights": "bf16",
+        },
+        "verify_layer_us": round(1e3 * med(ver_ms), 2),
+        "verify_layer_us_p10_p90": [round(1e3 * float(np.percentile(ver_ms, 10)), 2),
+                                    round(1e3 * float(np.percentile(ver_ms, 90)), 2)],
+        "draft_layer_us": round(1e3 * med(draft_ms), 2),
+        "gateup_us": round(1e3 * med(gu_ms), 2),
+        "down_us": round(1e3 * med(dn_ms), 2),
+        "down_gbs": round(dn_gbs, 1),
+        "union_mean": round(float(nu.mean()), 2),
+        "accept_mean": round(float(accs[:, 0].mean()), 3),
+        "wall_s_timed": round(wall, 4),
+        "hbm_read_ceiling_gbs": None if probe_gbs is None else round(probe_gbs, 1),
+        "roofline": {
+            "kernel": "gateup_kernel (verify layer)",
+            "bound": "hbm",
+            "achieved": round(gu_gbs, 1),
+            "peak": PEAK_HBM_GBS,
+            "unit": "GB/s",
+            "frac": round(gu_gbs / PEAK_HBM_GBS, 4),
+            "traffic": None,
+            "algorithmic_bytes_per_launch": int(round(float(gu_bytes.mean()))),
+        },
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+def cpu_baseline(cfg, x, budget_s):
+    """The oracle's verify layer on the host cores, weights already in memory."""
+    import numpy as np
+
+    from oracle import moe
+    from workloads import gen
+
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:  # noqa: BLE001
+        cores = len(os.sched_getaffinity(0))
+    w_router = gen.router_weight(cfg, 0).astype(np.float64)
+    idx, gate, _ = moe.route_topk(x, w_router, None, cfg.top_k, cfg.score_func, cfg.norm_topk)
+    members = sorted(set(int(e) for e in idx.ravel()))
+    raw = {e: gen.routed_block(cfg, 0, e) for e in members}
+    shared_raw = gen.shared_block(cfg, 0)
+
+    def run():
+        shared = moe.split_shared(shared_raw, cfg.n_shared, cfg.shared_each, cfg.hidden)
+        routed = {}
+
+        def get(e):
+            if e not in routed:
+                routed[e] = moe.split_expert(raw[e], cfg.inter, cfg.hidden)
+            return routed[e]
+        moe.moe_target(x, w_router, None, get, shared, cfg.top_k, cfg.score_func, cfg.norm_topk)
+
+    times = []
+    t_end = time.perf_counter() + budget_s
+    while True:
+        t0 = time.perf_counter()
+        run()
+        times.append(time.perf_counter() - t0)
+        if time.perf_counter() > t_end or len(times) >= 50:
+            break
+    t = statistics.median(times)
+    return {
+        "value": round(len(members) * cfg.expert_bytes() / t / 1e9, 4),
+        "unit": "GB/s",
+        "cores": int(cores),
+        "kind": "oracle",
+        "sample": f"fp64 oracle verify layer (T={x.shape[0]}, |U|={len(members)}) on the V2-Lite "
+                  f"shape, bf16 weights in host memory, {len(times)} runs, median {t * 1e3:.1f} ms",
+    }
+
+
+if __name__ == "__main__":
+    main()

@@ -103,6 +103,12 @@ int de_check_desc(const de_moe_desc* d);
  * and de_verify_layer for blocks of up to T positions (0 on an invalid desc). */
 size_t de_workspace_bytes(const de_moe_desc* d, int T);
 
+/* Zeroes the control words at the start of a freshly allocated workspace
+ * (enqueued on `stream`).  Required once per allocation before its first use
+ * by a layer call; every layer call leaves them zero again.  Calls that share
+ * one workspace must not run concurrently. */
+int de_workspace_init(void* ws, size_t ws_bytes, hipStream_t stream);
+
 /* Router scoring and top-k selection (Eq. 1) with the gates of Eq. (4).
  *   x [T, H], w_router [N, H], bias [N] or NULL.
  *   topk_idx [T, k] int32: expert ids in descending selection key, ties to the
@@ -162,13 +168,18 @@ int de_verify_layer(const de_moe_desc* d, int T, const float* x, const float* w_
                     hipStream_t stream);
 
 /* Greedy exact acceptance (Algorithm 1, verify and accept):
- *   target_argmax[j] = argmax_v target_logits[j, v] (ties to the lowest v),
- *   j = 0..K; out[0] = n = largest m <= K with draft_tokens[i-1] ==
- *   target_argmax[i-1] for all i <= m; out[1] = target_argmax[n] (the bonus
- *   token).  K = 0 gives the argmax of one row.  draft_tokens may be NULL
- *   when K is 0. */
+ *   target_argmax[j] = argmax_v target_logits[j, v] (ties to the lowest v,
+ *   NaN treated as -inf), j = 0..K; out[0] = n = largest m <= K with
+ *   draft_tokens[i-1] == target_argmax[i-1] for all i <= m; out[1] =
+ *   target_argmax[n] (the bonus token).  K = 0 gives the argmax of one row.
+ *   draft_tokens may be NULL when K is 0.  One launch: rows are split in
+ *   4096-logit chunks reduced in a fixed order (deterministic).  Scratch: ws
+ *   of de_accept_workspace_bytes(K, V) bytes, zero-filled once by
+ *   de_workspace_init. */
+size_t de_accept_workspace_bytes(int K, int V);
 int de_accept_len(int K, int V, const float* target_logits, const int32_t* draft_tokens,
-                  int32_t* target_argmax, int32_t* out, hipStream_t stream);
+                  int32_t* target_argmax, int32_t* out, void* ws, size_t ws_bytes,
+                  hipStream_t stream);
 
 /* ---- Stacked-model glue (a pre-norm residual stack without attention) ---- */
 
@@ -194,6 +205,19 @@ int de_dense_swiglu(int T, int H, int I, int wdtype, const float* x, const void*
 /* Pure streaming read of `bytes` (multiple of 16) from buf: the measured HBM
  * read ceiling.  sink [1] receives a value that depends on every byte. */
 int de_stream_probe(const void* buf, size_t bytes, float* sink, hipStream_t stream);
+
+/* ---- Instrumentation ---- */
+
+/* Kernel phases that can be bracketed by caller-owned HIP events. */
+#define DE_PHASE_GATEUP 0 /* the grouped gate/up kernel (Eq. 4 first half) */
+#define DE_PHASE_DOWN 1   /* the grouped down-projection kernel */
+
+/* Arms a one-shot timer: the next layer call (de_grouped_swiglu,
+ * de_draft_layer, de_verify_layer, de_dense_swiglu) made on this host thread
+ * records `start` on its stream right before launching the kernel of `phase`
+ * and `stop` right after it, then disarms.  Either event may be NULL.  The
+ * events are created and read by the caller (e.g. hipEventElapsedTime). */
+int de_time_next_phase(int phase, hipEvent_t start, hipEvent_t stop);
 
 #ifdef __cplusplus
 }

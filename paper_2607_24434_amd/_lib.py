@@ -25,11 +25,14 @@ DE_F32 = 0
 DE_BF16 = 1
 
 C_FUNCS = [
-    "de_abi_version", "de_error_string", "de_check_desc", "de_workspace_bytes", "de_route_topk",
-    "de_expert_union", "de_grouped_swiglu", "de_draft_layer", "de_verify_layer", "de_accept_len",
+    "de_abi_version", "de_error_string", "de_check_desc", "de_workspace_bytes",
+    "de_workspace_init", "de_route_topk",
+    "de_expert_union", "de_grouped_swiglu", "de_draft_layer", "de_verify_layer", "de_accept_workspace_bytes", "de_accept_len",
     "de_lm_head", "de_rmsnorm", "de_embed_gather", "de_dense_workspace_bytes", "de_dense_swiglu",
-    "de_stream_probe",
+    "de_stream_probe", "de_time_next_phase",
 ]
+DE_PHASE_GATEUP = 0
+DE_PHASE_DOWN = 1
 
 
 class DEError(RuntimeError):
@@ -61,7 +64,7 @@ class Epilogue(ctypes.Structure):
 
 def _load():
     if not os.path.exists(LIB_PATH):
-        raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2607_24434_amd.build`")
+        raise ImportError(f"{LIB_PATH} is missing: build it with `python paper_2607_24434_amd/build.py`")
     lib = ctypes.CDLL(LIB_PATH)
     P = ctypes.c_void_p
     I = ctypes.c_int
@@ -75,18 +78,21 @@ def _load():
         "de_error_string": (ctypes.c_char_p, [I]),
         "de_check_desc": (I, [DP]),
         "de_workspace_bytes": (SZ, [DP, I]),
+        "de_workspace_init": (I, [P, SZ, P]),
         "de_route_topk": (I, [DP, I, P, P, P, P, P, P, SZ, P]),
         "de_expert_union": (I, [I, I, I, P, P, P, P, P, P, P, P, P]),
         "de_grouped_swiglu": (I, [DP, I, P, TP, P, P, P, P, P, P, P, P, EP, P, SZ, P]),
         "de_draft_layer": (I, [DP, I, P, P, P, TP, P, P, F, P, P, P, EP, P, SZ, P]),
         "de_verify_layer": (I, [DP, I, P, P, P, TP, P, P, P, P, P, P, P, P, P, P, EP, P, SZ, P]),
-        "de_accept_len": (I, [I, I, P, P, P, P, P]),
+        "de_accept_workspace_bytes": (SZ, [I, I]),
+        "de_accept_len": (I, [I, I, P, P, P, P, P, SZ, P]),
         "de_lm_head": (I, [I, I, I, P, P, P, P]),
         "de_rmsnorm": (I, [I, I, P, F, P, P]),
         "de_embed_gather": (I, [I, I, I, P, P, P, P, F, P]),
         "de_dense_workspace_bytes": (SZ, [I, I, I]),
         "de_dense_swiglu": (I, [I, I, I, I, P, P, P, EP, P, SZ, P]),
         "de_stream_probe": (I, [P, SZ, P, P]),
+        "de_time_next_phase": (I, [I, P, P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -154,6 +160,17 @@ def de_workspace_bytes(desc: MoEDesc, T: int) -> int:
     return LIB.de_workspace_bytes(ctypes.byref(desc), int(T))
 
 
+def de_workspace_init(ws, stream=None):
+    _check("de_workspace_init", LIB.de_workspace_init(_ptr(ws), ws.numel(), _stream(stream)))
+
+
+def workspace(desc, T, device="cuda"):
+    """A zero-initialised workspace tensor for layer calls of up to T positions."""
+    ws = torch.empty(de_workspace_bytes(desc, T), dtype=torch.uint8, device=device)
+    de_workspace_init(ws)
+    return ws
+
+
 def de_route_topk(desc, T, x, w_router, bias, topk_idx, topk_gate, ws, stream=None):
     _check("de_route_topk", LIB.de_route_topk(
         ctypes.byref(desc), int(T), _ptr(x), _ptr(w_router), _ptr(bias), _ptr(topk_idx),
@@ -193,10 +210,21 @@ def de_verify_layer(desc, T, x, w_router, bias, table, shared_w, y, topk_idx=Non
         ws.numel() if ws is not None else 0, _stream(stream)))
 
 
-def de_accept_len(K, V, target_logits, draft_tokens, target_argmax, out, stream=None):
+def de_accept_workspace_bytes(K, V) -> int:
+    return LIB.de_accept_workspace_bytes(int(K), int(V))
+
+
+def accept_workspace(K, V, device="cuda"):
+    """A zero-initialised scratch tensor for de_accept_len with up to K drafts."""
+    ws = torch.empty(de_accept_workspace_bytes(K, V), dtype=torch.uint8, device=device)
+    de_workspace_init(ws)
+    return ws
+
+
+def de_accept_len(K, V, target_logits, draft_tokens, target_argmax, out, ws, stream=None):
     _check("de_accept_len", LIB.de_accept_len(
         int(K), int(V), _ptr(target_logits), _ptr(draft_tokens), _ptr(target_argmax), _ptr(out),
-        _stream(stream)))
+        _ptr(ws), ws.numel(), _stream(stream)))
 
 
 def de_lm_head(T, H, V, x, w_lm, logits, stream=None):
@@ -228,3 +256,10 @@ def de_dense_swiglu(T, H, I, wdtype, x, w, y, ws, epi=None, stream=None):
 def de_stream_probe(buf, nbytes, sink, stream=None):
     _check("de_stream_probe", LIB.de_stream_probe(_ptr(buf), int(nbytes), _ptr(sink),
                                                   _stream(stream)))
+
+
+def de_time_next_phase(phase, start_event, stop_event):
+    """Arm the one-shot phase timer with torch.cuda.Event objects (already recorded once)."""
+    _check("de_time_next_phase", LIB.de_time_next_phase(
+        int(phase), None if start_event is None else start_event.cuda_event,
+        None if stop_event is None else stop_event.cuda_event))

@@ -1,6 +1,7 @@
 """Builds libdraftexpert.so in-tree with hipcc for gfx950.
 
-Usage: python -m paper_2607_24434_amd.build   (or call build()).
+Usage: python paper_2607_24434_amd/build.py   (runs without importing the package,
+whose import loads the library this script produces).
 Every source compiles to its own object under _build/ in parallel, then one
 shared library is linked next to this file.
 """

@@ -39,7 +39,7 @@ int elem_bytes(int wdtype) { return wdtype == DE_BF16 ? 2 : 4; }
 int elem_align(int wdtype) { return wdtype == DE_BF16 ? 8 : 4; }
 
 struct Layout {
-  size_t z, idx, gate, nu, uids, offs, tok, glist, ppos;
+  size_t ctl, z, idx, gate, nu, uids, offs, tok, glist, ppos;
   size_t a_r, a_s, a_d, p_r, p_s, p_d;
   size_t total;
 };
@@ -53,6 +53,7 @@ Layout layout(const de_moe_desc& d, int T) {
     return r;
   };
   const size_t tk = (size_t)T * d.top_k;
+  L.ctl = take(256);  // counters: zero after de_workspace_init and after every call
   L.z = take((size_t)T * d.n_experts * 4);
   L.idx = take(tk * 4);
   L.gate = take(tk * 4);
@@ -96,6 +97,35 @@ int check_epi(const de_epilogue* epi) {
 }
 
 int hip_status(hipError_t e) { return e == hipSuccess ? DE_OK : DE_ERR_HIP; }
+
+hipError_t route(const de_moe_desc& d, int T, const float* x, const float* w_router,
+                 const Layout& L, void* ws, const de::TopkUnionArgs& sel, hipStream_t s) {
+  de::RouteArgs r{};
+  r.sel = sel;
+  r.x = x;
+  r.w = w_router;
+  r.H = d.hidden;
+  r.z = reinterpret_cast<float*>(static_cast<char*>(ws) + L.z);
+  r.sel.z = r.z;
+  r.counter = reinterpret_cast<unsigned*>(static_cast<char*>(ws) + L.ctl);
+  return de::launch_route(r, s);
+}
+
+// One-shot phase timers armed by de_time_next_phase (per host thread).
+thread_local hipEvent_t t_start[2] = {nullptr, nullptr};
+thread_local hipEvent_t t_stop[2] = {nullptr, nullptr};
+
+// Launches one phase with its armed events (if any) around it.
+template <typename F>
+hipError_t timed_phase(int phase, hipStream_t s, F launch) {
+  hipEvent_t a = t_start[phase], b = t_stop[phase];
+  t_start[phase] = t_stop[phase] = nullptr;
+  if (a != nullptr && hipEventRecord(a, s) != hipSuccess) return hipErrorInvalidValue;
+  const hipError_t e = launch();
+  if (e != hipSuccess) return e;
+  if (b != nullptr && hipEventRecord(b, s) != hipSuccess) return hipErrorInvalidValue;
+  return hipSuccess;
+}
 
 template <typename T>
 T* at(void* ws, size_t off) {
@@ -155,7 +185,7 @@ int run_grouped(const de_moe_desc& d, int T, const float* x, const de::RoutedSrc
     ds.out = at<float>(ws, L.a_d);
     c.dense_p[c.n_dense++] = at<float>(ws, L.p_d);
   }
-  hipError_t e = de::launch_gateup(g, d.wdtype, s);
+  hipError_t e = timed_phase(DE_PHASE_GATEUP, s, [&] { return de::launch_gateup(g, d.wdtype, s); });
   if (e != hipSuccess) return DE_ERR_HIP;
   // The down pass reads the gate/up activations of each dense source.
   int nd = 0;
@@ -179,7 +209,7 @@ int run_grouped(const de_moe_desc& d, int T, const float* x, const de::RoutedSrc
     ds.out = at<float>(ws, L.p_d);
     ds.out_stride = d.hidden;
   }
-  e = de::launch_down(g, d.wdtype, s);
+  e = timed_phase(DE_PHASE_DOWN, s, [&] { return de::launch_down(g, d.wdtype, s); });
   if (e != hipSuccess) return DE_ERR_HIP;
   c.p_r = r.p;
   c.pair_pos = pair_pos;
@@ -231,6 +261,12 @@ size_t de_workspace_bytes(const de_moe_desc* d, int T) {
   return layout(*d, T).total;
 }
 
+int de_workspace_init(void* ws, size_t ws_bytes, hipStream_t stream) {
+  if (ws == nullptr || (reinterpret_cast<uintptr_t>(ws) & 255u) != 0 || ws_bytes < 256)
+    return DE_ERR_WORKSPACE;
+  return hip_status(hipMemsetAsync(ws, 0, ws_bytes, stream));
+}
+
 int de_route_topk(const de_moe_desc* d, int T, const float* x, const float* w_router,
                   const float* bias, int32_t* topk_idx, float* topk_gate, void* ws,
                   size_t ws_bytes, hipStream_t stream) {
@@ -242,14 +278,10 @@ int de_route_topk(const de_moe_desc* d, int T, const float* x, const float* w_ro
   if (!aligned16(x) || !aligned16(w_router) || d->hidden % 4) return DE_ERR_INVALID;
   if ((rc = check_ws(*d, T, ws, ws_bytes)) != DE_OK) return rc;
   const Layout L = layout(*d, T);
-  float* z = at<float>(ws, L.z);
-  if (de::launch_router_logits(x, w_router, T, d->hidden, d->n_experts, z, stream) != hipSuccess)
-    return DE_ERR_HIP;
   de::TopkUnionArgs a{};
   a.T = T;
   a.N = d->n_experts;
   a.k = d->top_k;
-  a.z = z;
   a.bias = bias;
   a.score_func = d->score_func;
   a.norm_topk = d->norm_topk;
@@ -257,7 +289,7 @@ int de_route_topk(const de_moe_desc* d, int T, const float* x, const float* w_ro
   a.idx_out = topk_idx;
   a.gate_out = topk_gate;
   a.ucols = d->top_k;
-  return hip_status(de::launch_topk_union(a, stream));
+  return hip_status(route(*d, T, x, w_router, L, ws, a, stream));
 }
 
 int de_expert_union(int T, int k, int N, const int32_t* topk_idx, const float* topk_gate,
@@ -282,7 +314,7 @@ int de_expert_union(int T, int k, int N, const int32_t* topk_idx, const float* t
   a.tok_list = tok_list;
   a.gate_list = gate_list;
   a.pair_pos = pair_pos;
-  return hip_status(de::launch_topk_union(a, stream));
+  return hip_status(de::launch_union(a, stream));
 }
 
 int de_grouped_swiglu(const de_moe_desc* d, int T, const float* x, const de_expert_table* routed,
@@ -324,14 +356,10 @@ int de_draft_layer(const de_moe_desc* d, int T, const float* x, const float* w_r
   if ((rc = check_epi(epi)) != DE_OK) return rc;
   if ((rc = check_ws(*d, T, ws, ws_bytes)) != DE_OK) return rc;
   const Layout L = layout(*d, T);
-  float* z = at<float>(ws, L.z);
-  if (de::launch_router_logits(x, w_router, T, d->hidden, d->n_experts, z, stream) != hipSuccess)
-    return DE_ERR_HIP;
   de::TopkUnionArgs a{};
   a.T = T;
   a.N = d->n_experts;
   a.k = d->top_k;
-  a.z = z;
   a.bias = bias;
   a.score_func = d->score_func;
   a.norm_topk = d->norm_topk;
@@ -345,7 +373,7 @@ int de_draft_layer(const de_moe_desc* d, int T, const float* x, const float* w_r
   a.tok_list = at<int32_t>(ws, L.tok);
   a.gate_list = at<float>(ws, L.glist);
   a.pair_pos = at<int32_t>(ws, L.ppos);
-  if (de::launch_topk_union(a, stream) != hipSuccess) return DE_ERR_HIP;
+  if (route(*d, T, x, w_router, L, ws, a, stream) != hipSuccess) return DE_ERR_HIP;
   const de::RoutedSrc r = routed_src(*d, T, routed, a.n_union, a.union_ids, a.offsets, a.tok_list,
                                      a.gate_list, at<float>(ws, L.a_r), at<float>(ws, L.p_r));
   return run_grouped(*d, T, x, r, a.pair_pos, 1, shared_w, draft_w, gamma, y, epi, L, ws, stream);
@@ -367,14 +395,10 @@ int de_verify_layer(const de_moe_desc* d, int T, const float* x, const float* w_
   if ((rc = check_epi(epi)) != DE_OK) return rc;
   if ((rc = check_ws(*d, T, ws, ws_bytes)) != DE_OK) return rc;
   const Layout L = layout(*d, T);
-  float* z = at<float>(ws, L.z);
-  if (de::launch_router_logits(x, w_router, T, d->hidden, d->n_experts, z, stream) != hipSuccess)
-    return DE_ERR_HIP;
   de::TopkUnionArgs a{};
   a.T = T;
   a.N = d->n_experts;
   a.k = d->top_k;
-  a.z = z;
   a.bias = bias;
   a.score_func = d->score_func;
   a.norm_topk = d->norm_topk;
@@ -388,20 +412,40 @@ int de_verify_layer(const de_moe_desc* d, int T, const float* x, const float* w_
   a.tok_list = tok_list ? tok_list : at<int32_t>(ws, L.tok);
   a.gate_list = gate_list ? gate_list : at<float>(ws, L.glist);
   a.pair_pos = pair_pos ? pair_pos : at<int32_t>(ws, L.ppos);
-  if (de::launch_topk_union(a, stream) != hipSuccess) return DE_ERR_HIP;
+  if (route(*d, T, x, w_router, L, ws, a, stream) != hipSuccess) return DE_ERR_HIP;
   const de::RoutedSrc r = routed_src(*d, T, routed, a.n_union, a.union_ids, a.offsets, a.tok_list,
                                      a.gate_list, at<float>(ws, L.a_r), at<float>(ws, L.p_r));
   return run_grouped(*d, T, x, r, a.pair_pos, d->top_k, shared_w, nullptr, 0.f, y, epi, L, ws,
                      stream);
 }
 
+size_t de_accept_workspace_bytes(int K, int V) {
+  if (K < 0 || K > 1024 || V < 1) return 0;
+  const size_t rows = (size_t)K + 1, ch = (size_t)de::accept_chunks(V);
+  return 256 + up256(rows * 4) + 2 * up256(rows * ch * 4);
+}
+
 int de_accept_len(int K, int V, const float* target_logits, const int32_t* draft_tokens,
-                  int32_t* target_argmax, int32_t* out, hipStream_t stream) {
+                  int32_t* target_argmax, int32_t* out, void* ws, size_t ws_bytes,
+                  hipStream_t stream) {
   if (K < 0 || K > 1024 || V < 1 || !target_logits || !target_argmax || !out) return DE_ERR_INVALID;
   if (K > 0 && draft_tokens == nullptr) return DE_ERR_INVALID;
-  if (de::launch_argmax_rows(target_logits, K + 1, V, target_argmax, stream) != hipSuccess)
-    return DE_ERR_HIP;
-  return hip_status(de::launch_accept(K, target_argmax, draft_tokens, out, stream));
+  if (ws == nullptr || (reinterpret_cast<uintptr_t>(ws) & 255u) != 0 ||
+      ws_bytes < de_accept_workspace_bytes(K, V))
+    return DE_ERR_WORKSPACE;
+  const size_t rows = (size_t)K + 1, ch = (size_t)de::accept_chunks(V);
+  de::AcceptArgs a{};
+  a.K = K;
+  a.V = V;
+  a.logits = target_logits;
+  a.drafts = draft_tokens;
+  a.amax = target_argmax;
+  a.out = out;
+  a.done_cnt = at<unsigned>(ws, 0);
+  a.row_cnt = at<unsigned>(ws, 256);
+  a.part_v = at<float>(ws, 256 + up256(rows * 4));
+  a.part_i = at<int32_t>(ws, 256 + up256(rows * 4) + up256(rows * ch * 4));
+  return hip_status(de::launch_argmax_accept(a, stream));
 }
 
 int de_lm_head(int T, int H, int V, const float* x, const void* w_lm, float* logits,
@@ -465,7 +509,9 @@ int de_dense_swiglu(int T, int H, int I, int wdtype, const float* x, const void*
   g.dense[0].w = w;
   g.dense[0].inter = I;
   g.dense[0].out = A;
-  if (de::launch_gateup(g, wdtype, stream) != hipSuccess) return DE_ERR_HIP;
+  if (timed_phase(DE_PHASE_GATEUP, stream, [&] { return de::launch_gateup(g, wdtype, stream); }) !=
+      hipSuccess)
+    return DE_ERR_HIP;
   g.dense[0].w = static_cast<const char*>(w) + 2 * (size_t)I * H * elem_bytes(wdtype);
   g.dense[0].rows = H;
   g.dense[0].gate = 1.0f;
@@ -473,7 +519,9 @@ int de_dense_swiglu(int T, int H, int I, int wdtype, const float* x, const void*
   g.dense[0].vin_stride = I;
   g.dense[0].out = P;
   g.dense[0].out_stride = H;
-  if (de::launch_down(g, wdtype, stream) != hipSuccess) return DE_ERR_HIP;
+  if (timed_phase(DE_PHASE_DOWN, stream, [&] { return de::launch_down(g, wdtype, stream); }) !=
+      hipSuccess)
+    return DE_ERR_HIP;
   de::CombineArgs c{};
   c.T = T;
   c.H = H;
@@ -484,6 +532,13 @@ int de_dense_swiglu(int T, int H, int I, int wdtype, const float* x, const void*
   c.normed = epi ? epi->normed : nullptr;
   c.eps = epi ? epi->eps : 0.f;
   return hip_status(de::launch_combine(c, stream));
+}
+
+int de_time_next_phase(int phase, hipEvent_t start, hipEvent_t stop) {
+  if (phase != DE_PHASE_GATEUP && phase != DE_PHASE_DOWN) return DE_ERR_INVALID;
+  t_start[phase] = start;
+  t_stop[phase] = stop;
+  return DE_OK;
 }
 
 int de_stream_probe(const void* buf, size_t bytes, float* sink, hipStream_t stream) {

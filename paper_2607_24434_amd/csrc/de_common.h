@@ -40,12 +40,23 @@ __device__ __forceinline__ float wave_max(float v) {
 
 __device__ __forceinline__ float silu_f(float v) { return v / (1.0f + expf(-v)); }
 
-// Native 128-bit vector (the builtins below need a clang vector type).
+// Native 128-bit vectors (the builtins and address-space casts below need
+// clang vector types rather than HIP's vector classes).
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// Pointers known to be in global memory.  Loads through generic pointers
+// compile to flat loads, which also count against the LDS wait counter and so
+// serialise with LDS reads; every weight and activation stream here is global.
+#define DE_GLOBAL __attribute__((address_space(1)))
+template <typename T>
+__device__ __forceinline__ const DE_GLOBAL T* gptr(const void* p) {
+  return (const DE_GLOBAL T*)(p);
+}
 
 // 16-byte load of weights that are streamed once (non-temporal hint).
 __device__ __forceinline__ u32x4 load_stream16(const void* p) {
-  return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+  return __builtin_nontemporal_load(gptr<u32x4>(p));
 }
 
 // ---------------------------------------------------------------- kernel arguments
@@ -90,6 +101,7 @@ struct GroupedArgs {
   RoutedSrc r;
   int n_dense;
   DenseSrc dense[3];
+  int lds_floats;      // set by the launcher: staged-input capacity of a block
 };
 
 // ---------------------------------------------------------------- launchers (HIP side)
@@ -99,9 +111,6 @@ struct DevInfo {
   int num_cus;
 };
 const DevInfo& dev_info();
-
-hipError_t launch_router_logits(const float* x, const float* w, int T, int H, int N, float* z,
-                                hipStream_t s);
 
 struct TopkUnionArgs {
   int T, N, k;
@@ -121,7 +130,18 @@ struct TopkUnionArgs {
   float* gate_list;
   int32_t* pair_pos;       // [T, ucols]
 };
-hipError_t launch_topk_union(const TopkUnionArgs& a, hipStream_t s);
+// Router scoring + top-k (+ union when sel.n_union is set) in one launch.
+struct RouteArgs {
+  TopkUnionArgs sel;       // sel.z is the logits scratch [T, N]
+  const float* x;          // [T, H]
+  const float* w;          // [N, H] fp32 router
+  int H;
+  float* z;                // == sel.z
+  unsigned* counter;       // zero between calls (last-block election)
+};
+hipError_t launch_route(const RouteArgs& r, hipStream_t s);
+// Union only, from caller-supplied lists (sel.idx_in / sel.gate_in).
+hipError_t launch_union(const TopkUnionArgs& a, hipStream_t s);
 
 hipError_t launch_gateup(const GroupedArgs& a, int wdtype, hipStream_t s);
 hipError_t launch_down(const GroupedArgs& a, int wdtype, hipStream_t s);
@@ -141,9 +161,19 @@ struct CombineArgs {
 };
 hipError_t launch_combine(const CombineArgs& a, hipStream_t s);
 
-hipError_t launch_argmax_rows(const float* logits, int rows, int V, int32_t* amax, hipStream_t s);
-hipError_t launch_accept(int K, const int32_t* amax, const int32_t* drafts, int32_t* out,
-                         hipStream_t s);
+struct AcceptArgs {
+  int K, V;
+  const float* logits;     // [K+1, V]
+  const int32_t* drafts;   // [K]
+  int32_t* amax;           // [K+1]
+  int32_t* out;            // [2]: n, bonus
+  float* part_v;           // [K+1, chunks] scratch
+  int32_t* part_i;
+  unsigned* row_cnt;       // [K+1], zero between calls
+  unsigned* done_cnt;      // [1], zero between calls
+};
+int accept_chunks(int V);
+hipError_t launch_argmax_accept(const AcceptArgs& a, hipStream_t s);
 hipError_t launch_rmsnorm(int T, int H, const float* x, float eps, float* out, hipStream_t s);
 hipError_t launch_embed(int T, int H, int V, const int32_t* tokens, const uint16_t* emb, float* h,
                         float* normed, float eps, hipStream_t s);

@@ -7,27 +7,44 @@
 namespace de {
 namespace {
 
-constexpr int kArgmaxThreads = 1024;
+constexpr int kAmThreads = 256;
+constexpr int kAmPer = 16;                        // logits per thread
+constexpr int kAmChunk = kAmThreads * kAmPer;     // logits per block
 
 // (value, index) ordering for argmax: larger value, then lower index; a NaN
-// counts as -infinity.
+// counts as -infinity; index INT_MAX marks "none".
 __device__ __forceinline__ bool am_better(float va, int ia, float vb, int ib) {
+  if (ia == INT_MAX) return false;
+  if (ib == INT_MAX) return true;
   return va > vb || (va == vb && ia < ib);
 }
 
-__global__ __launch_bounds__(kArgmaxThreads) void argmax_rows_kernel(const float* __restrict__ logits,
-                                                                     int V, int32_t* __restrict__ amax) {
-  __shared__ float sv[kArgmaxThreads / 64];
-  __shared__ int si[kArgmaxThreads / 64];
-  const int row = blockIdx.x;
-  const float* p = logits + (size_t)row * V;
+// Grid (chunks, K+1).  Each block finds the argmax of one 4096-logit chunk of
+// one row; the last block of a row (device-scope counter) reduces the row's
+// chunk results in chunk order, and the last row to finish applies the greedy
+// accept rule.  Counters are left at zero.
+__global__ __launch_bounds__(kAmThreads) void argmax_accept_kernel(AcceptArgs a) {
+  __shared__ float sv[kAmThreads / 64];
+  __shared__ int si[kAmThreads / 64];
+  __shared__ int s_flag;
+  const int row = blockIdx.y, chunk = blockIdx.x, nch = gridDim.x;
+  const float* p = a.logits + (size_t)row * a.V;
+  const int base = chunk * kAmChunk;
+  float x[kAmPer];
+#pragma unroll
+  for (int i = 0; i < kAmPer; ++i) {
+    const int v = base + threadIdx.x + i * kAmThreads;
+    x[i] = v < a.V ? p[v] : -INFINITY;
+  }
   float bv = -INFINITY;
   int bi = INT_MAX;
-  for (int v = threadIdx.x; v < V; v += blockDim.x) {
-    float x = p[v];
-    if (!(x == x)) x = -INFINITY;
-    if (bi == INT_MAX || am_better(x, v, bv, bi)) {
-      bv = x;
+#pragma unroll
+  for (int i = 0; i < kAmPer; ++i) {
+    const int v = base + threadIdx.x + i * kAmThreads;
+    float xv = x[i];
+    if (!(xv == xv)) xv = -INFINITY;
+    if (v < a.V && am_better(xv, v, bv, bi)) {
+      bv = xv;
       bi = v;
     }
   }
@@ -35,7 +52,7 @@ __global__ __launch_bounds__(kArgmaxThreads) void argmax_rows_kernel(const float
   for (int o = 32; o > 0; o >>= 1) {
     const float ov = __shfl_xor(bv, o, kWave);
     const int oi = __shfl_xor(bi, o, kWave);
-    if (oi != INT_MAX && (bi == INT_MAX || am_better(ov, oi, bv, bi))) {
+    if (am_better(ov, oi, bv, bi)) {
       bv = ov;
       bi = oi;
     }
@@ -46,25 +63,39 @@ __global__ __launch_bounds__(kArgmaxThreads) void argmax_rows_kernel(const float
     si[wave] = bi;
   }
   __syncthreads();
-  if (threadIdx.x == 0) {
-    float v = sv[0];
-    int i = si[0];
-    for (int w = 1; w < (int)(blockDim.x >> 6); ++w)
-      if (si[w] != INT_MAX && (i == INT_MAX || am_better(sv[w], si[w], v, i))) {
-        v = sv[w];
-        i = si[w];
-      }
-    amax[row] = i == INT_MAX ? 0 : i;
-  }
-}
-
-__global__ void accept_kernel(int K, const int32_t* __restrict__ amax,
-                              const int32_t* __restrict__ drafts, int32_t* __restrict__ out) {
   if (threadIdx.x != 0) return;
+  for (int w = 1; w < kAmThreads / 64; ++w)
+    if (am_better(sv[w], si[w], sv[0], si[0])) {
+      sv[0] = sv[w];
+      si[0] = si[w];
+    }
+  a.part_v[row * nch + chunk] = sv[0];
+  a.part_i[row * nch + chunk] = si[0];
+  __threadfence();
+  const unsigned prev = __hip_atomic_fetch_add(&a.row_cnt[row], 1u, __ATOMIC_ACQ_REL,
+                                               __HIP_MEMORY_SCOPE_AGENT);
+  if (prev != (unsigned)nch - 1) return;
+  __threadfence();
+  float v = -INFINITY;
+  int i = INT_MAX;
+  for (int c = 0; c < nch; ++c)
+    if (am_better(a.part_v[row * nch + c], a.part_i[row * nch + c], v, i)) {
+      v = a.part_v[row * nch + c];
+      i = a.part_i[row * nch + c];
+    }
+  a.amax[row] = i == INT_MAX ? 0 : i;
+  __hip_atomic_store(&a.row_cnt[row], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  __threadfence();
+  const unsigned done = __hip_atomic_fetch_add(a.done_cnt, 1u, __ATOMIC_ACQ_REL,
+                                               __HIP_MEMORY_SCOPE_AGENT);
+  if (done != (unsigned)gridDim.y - 1) return;
+  __threadfence();
+  __hip_atomic_store(a.done_cnt, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   int n = 0;
-  while (n < K && drafts[n] == amax[n]) ++n;
-  out[0] = n;
-  out[1] = amax[n];
+  while (n < a.K && a.drafts[n] == a.amax[n]) ++n;
+  a.out[0] = n;
+  a.out[1] = a.amax[n];
+  (void)s_flag;
 }
 
 __device__ float block_sum256(float v, float* red) {
@@ -130,14 +161,11 @@ __global__ __launch_bounds__(256) void stream_probe_kernel(const u32x4* __restri
 
 }  // namespace
 
-hipError_t launch_argmax_rows(const float* logits, int rows, int V, int32_t* amax, hipStream_t s) {
-  hipLaunchKernelGGL(argmax_rows_kernel, dim3(rows), dim3(kArgmaxThreads), 0, s, logits, V, amax);
-  return hipGetLastError();
-}
+int accept_chunks(int V) { return (V + kAmChunk - 1) / kAmChunk; }
 
-hipError_t launch_accept(int K, const int32_t* amax, const int32_t* drafts, int32_t* out,
-                         hipStream_t s) {
-  hipLaunchKernelGGL(accept_kernel, dim3(1), dim3(64), 0, s, K, amax, drafts, out);
+hipError_t launch_argmax_accept(const AcceptArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(argmax_accept_kernel, dim3(accept_chunks(a.V), a.K + 1), dim3(kAmThreads), 0,
+                     s, a);
   return hipGetLastError();
 }
 

@@ -41,7 +41,7 @@ class DevLayer:
         self.device = device
 
     def ws(self, T: int) -> torch.Tensor:
-        return torch.empty(de.de_workspace_bytes(self.desc, T), dtype=torch.uint8, device=self.device)
+        return de.workspace(self.desc, T, self.device)
 
 
 _LAYERS: dict = {}

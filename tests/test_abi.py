@@ -119,9 +119,14 @@ def test_other_entry_points_reject_bad_arguments_on_host():
                                FAKE, FAKE, FAKE, FAKE, None, FAKE, 1 << 30, None) == -1
     assert L.de_draft_layer(ctypes.byref(d), 1, FAKE, FAKE, None, ctypes.byref(tab), FAKE, FAKE,
                             float("nan"), FAKE, None, None, None, FAKE, 1 << 30, None) == -1
-    assert L.de_accept_len(-1, 10, FAKE, FAKE, FAKE, FAKE, None) == -1
-    assert L.de_accept_len(3, 10, FAKE, None, FAKE, FAKE, None) == -1
-    assert L.de_accept_len(0, 0, FAKE, None, FAKE, FAKE, None) == -1
+    assert L.de_accept_len(-1, 10, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 20, None) == -1
+    assert L.de_accept_len(3, 10, FAKE, None, FAKE, FAKE, FAKE, 1 << 20, None) == -1
+    assert L.de_accept_len(0, 0, FAKE, None, FAKE, FAKE, FAKE, 1 << 20, None) == -1
+    assert L.de_accept_len(8, 102400, FAKE, FAKE, FAKE, FAKE, FAKE, 64, None) == -4
+    assert L.de_accept_len(8, 102400, FAKE, FAKE, FAKE, FAKE, FAKE + 8, 1 << 20, None) == -4
+    assert de.de_accept_workspace_bytes(8, 102400) >= 9 * 25 * 8
+    assert L.de_workspace_init(None, 1024, None) == -4
+    assert L.de_workspace_init(FAKE, 16, None) == -4
     assert L.de_lm_head(9, 2044, 1000, FAKE, FAKE, FAKE, None) == -1
     assert L.de_rmsnorm(0, 16, FAKE, 1e-6, FAKE, None) == -1
     assert L.de_embed_gather(1, 16, 0, FAKE, FAKE, FAKE, None, 1e-6, None) == -1

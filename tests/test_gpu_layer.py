@@ -314,7 +314,8 @@ def test_lm_head_and_argmax(V, H, T):
     assert rel_err(got, want) <= 1e-4
     amax = torch.empty(T, dtype=torch.int32, device="cuda")
     out = torch.empty(2, dtype=torch.int32, device="cuda")
-    de.de_accept_len(T - 1, V, logits, i32(np.zeros(max(T - 1, 1), np.int32)), amax, out)
+    de.de_accept_len(T - 1, V, logits, i32(np.zeros(max(T - 1, 1), np.int32)), amax, out,
+                     de.accept_workspace(T - 1, V))
     top2 = np.sort(want, axis=1)[:, -2:]
     clear = (top2[:, 1] - top2[:, 0]) > 1e-4
     np.testing.assert_array_equal(amax.cpu().numpy()[clear], np.argmax(want, axis=1)[clear])
@@ -329,12 +330,13 @@ def test_accept_len_planted_prefix(K, V):
     lg = f32(logits)
     amax = torch.empty(K + 1, dtype=torch.int32, device="cuda")
     out = torch.empty(2, dtype=torch.int32, device="cuda")
+    ws = de.accept_workspace(K, V)
     for m in range(K + 1):
         drafts = t[:K].copy()
         if m < K:
             drafts[m] = (drafts[m] + 1) % V
         n_o, bonus_o, t_o = moe.accept_len(logits, drafts)
-        de.de_accept_len(K, V, lg, i32(drafts) if K else None, amax, out)
+        de.de_accept_len(K, V, lg, i32(drafts) if K else None, amax, out, ws)
         o = out.cpu().numpy()
         assert (int(o[0]), int(o[1])) == (n_o, bonus_o) == (m, int(t[m]))
         np.testing.assert_array_equal(amax.cpu().numpy(), t_o)
@@ -348,6 +350,6 @@ def test_argmax_ties_go_to_lowest_index():
     logits[2, [V - 1]] = 2.0
     amax = torch.empty(3, dtype=torch.int32, device="cuda")
     out = torch.empty(2, dtype=torch.int32, device="cuda")
-    de.de_accept_len(2, V, f32(logits), i32([17, 0]), amax, out)
+    de.de_accept_len(2, V, f32(logits), i32([17, 0]), amax, out, de.accept_workspace(2, V))
     np.testing.assert_array_equal(amax.cpu().numpy(), [17, 0, V - 1])
     assert out.cpu().tolist() == [2, V - 1]
