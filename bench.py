@@ -114,7 +114,7 @@ def main():
         e.record()
         return e
 
-    def step(s, evs):
+    def step(s, evs, phases=False):
         base = s * (K + 1)
         evs["s0"].record()
         for i in range(K):
@@ -127,8 +127,9 @@ def main():
         de.de_accept_len(K - 1, V, lg_dr, zero_tok, dtok, acc_dummy, aws)  # row argmax = drafts
         evs["v0"].record()
         cp = copies[(base + K) % R]
-        de.de_time_next_phase(de.DE_PHASE_GATEUP, evs["g0"], evs["g1"])
-        de.de_time_next_phase(de.DE_PHASE_DOWN, evs["p0"], evs["p1"])
+        if phases:
+            de.de_time_next_phase(de.DE_PHASE_GATEUP, evs["g0"], evs["g1"])
+            de.de_time_next_phase(de.DE_PHASE_DOWN, evs["p0"], evs["p1"])
         de.de_verify_layer(desc, T, x_ver, cp["router"], None, cp["table"], cp["shared"], y_ver,
                            n_union=nu_all[s:s + 1], ws=ws,
                            epi=de.make_epilogue(residual=x_ver, normed=n_ver))
@@ -150,13 +151,23 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - t_wall0
 
+    # Kernel durations for the roofline: the same steps again, with HIP events
+    # recorded around the grouped gate/up and down launches of the verify layer
+    # on the library's stream.  They are kept out of the timed steps above
+    # because the extra event records add gaps between the layer's kernels.
+    prec = [{n: ev() for n in names} for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    for i in range(args.steps):
+        step(args.warmup + i, prec[i], phases=True)
+    torch.cuda.synchronize()
+
     nu = nu_all[args.warmup:].cpu().numpy().astype(np.int64)
     accs = acc_all[args.warmup:].cpu().numpy()
     step_ms = [r["s0"].elapsed_time(r["s1"]) for r in rec]
     draft_ms = [r["s0"].elapsed_time(r["d1"]) / K for r in rec]
     ver_ms = [r["v0"].elapsed_time(r["v1"]) for r in rec]
-    gu_ms = [r["g0"].elapsed_time(r["g1"]) for r in rec]
-    dn_ms = [r["p0"].elapsed_time(r["p1"]) for r in rec]
+    gu_ms = [r["g0"].elapsed_time(r["g1"]) for r in prec]
+    dn_ms = [r["p0"].elapsed_time(r["p1"]) for r in prec]
 
     eb = stride
     union_bytes = nu * eb

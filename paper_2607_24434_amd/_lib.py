@@ -62,10 +62,10 @@ class Epilogue(ctypes.Structure):
     _fields_ = [("residual", ctypes.c_void_p), ("normed", ctypes.c_void_p), ("eps", ctypes.c_float)]
 
 
-def _load():
-    if not os.path.exists(LIB_PATH):
-        raise ImportError(f"{LIB_PATH} is missing: build it with `python paper_2607_24434_amd/build.py`")
-    lib = ctypes.CDLL(LIB_PATH)
+def _load(path: str = LIB_PATH):
+    if not os.path.exists(path):
+        raise ImportError(f"{path} is missing: build it with `python paper_2607_24434_amd/build.py`")
+    lib = ctypes.CDLL(path)
     P = ctypes.c_void_p
     I = ctypes.c_int
     F = ctypes.c_float
