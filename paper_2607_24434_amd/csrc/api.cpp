@@ -38,6 +38,23 @@ size_t up256(size_t v) { return (v + 255) & ~size_t(255); }
 int elem_bytes(int wdtype) { return wdtype == DE_BF16 ? 2 : 4; }
 int elem_align(int wdtype) { return wdtype == DE_BF16 ? 8 : 4; }
 
+// The shared path's down projection runs as up to this many dense sources
+// (intermediate chunks), each with its own [T, H] partial.
+constexpr int kMaxSharedChunks = 3;
+
+// Chunks of the shared intermediate for the down pass: the fewest (up to
+// max_chunks) whose T input rows fit 64 KB, each a whole number of 16-byte
+// weight units; when none fits, the valid split with the smallest chunk.
+int shared_chunks(int inter, int T, int max_chunks, int align) {
+  int best = 1;
+  for (int c = 1; c <= max_chunks; ++c) {
+    if (inter % c != 0 || (inter / c) % align != 0) continue;
+    if ((size_t)T * (inter / c) * 4 <= 64 * 1024) return c;
+    best = c;
+  }
+  return best;
+}
+
 struct Layout {
   size_t ctl, z, idx, gate, nu, uids, offs, tok, glist, ppos;
   size_t a_r, a_s, a_d, p_r, p_s, p_d;
@@ -67,7 +84,7 @@ Layout layout(const de_moe_desc& d, int T) {
   L.a_s = take((size_t)T * d.shared_inter * 4);
   L.a_d = take((size_t)T * d.draft_inter * 4);
   L.p_r = take(tk * d.hidden * 4);
-  L.p_s = take((size_t)T * d.hidden * 4);
+  L.p_s = take((size_t)kMaxSharedChunks * T * d.hidden * 4);
   L.p_d = take((size_t)T * d.hidden * 4);
   L.total = o;
   return L;
@@ -107,7 +124,6 @@ hipError_t route(const de_moe_desc& d, int T, const float* x, const float* w_rou
   r.H = d.hidden;
   r.z = reinterpret_cast<float*>(static_cast<char*>(ws) + L.z);
   r.sel.z = r.z;
-  r.counter = reinterpret_cast<unsigned*>(static_cast<char*>(ws) + L.ctl);
   return de::launch_route(r, s);
 }
 
@@ -176,39 +192,55 @@ int run_grouped(const de_moe_desc& d, int T, const float* x, const de::RoutedSrc
     ds.w = shared_w;
     ds.inter = d.shared_inter;
     ds.out = at<float>(ws, L.a_s);
-    c.dense_p[c.n_dense++] = at<float>(ws, L.p_s);
   }
   if (draft_w != nullptr && d.draft_inter > 0) {
     de::DenseSrc& ds = g.dense[g.n_dense++];
     ds.w = draft_w;
     ds.inter = d.draft_inter;
     ds.out = at<float>(ws, L.a_d);
-    c.dense_p[c.n_dense++] = at<float>(ws, L.p_d);
   }
   hipError_t e = timed_phase(DE_PHASE_GATEUP, s, [&] { return de::launch_gateup(g, d.wdtype, s); });
   if (e != hipSuccess) return DE_ERR_HIP;
-  // The down pass reads the gate/up activations of each dense source.
+  // The down pass reads the gate/up activations of each dense source.  The
+  // shared path's down projection is split along its intermediate dimension
+  // into chunks whose block of input rows fits a down block's LDS staging
+  // (two chunks for two 1408-wide shared experts at T = 9); each chunk writes
+  // its own partial, and the combine sums them.
   int nd = 0;
   if (shared_w != nullptr && d.shared_inter > 0) {
-    de::DenseSrc& ds = g.dense[nd++];
-    ds.w = static_cast<const char*>(shared_w) + 2 * (size_t)d.shared_inter * d.hidden * esz;
-    ds.rows = d.hidden;
-    ds.gate = 1.0f;
-    ds.vin = at<float>(ws, L.a_s);
-    ds.vin_stride = d.shared_inter;
-    ds.out = at<float>(ws, L.p_s);
-    ds.out_stride = d.hidden;
+    const int max_chunks = kMaxSharedChunks - ((draft_w != nullptr && d.draft_inter > 0) ? 1 : 0);
+    const int chunks = shared_chunks(d.shared_inter, T, max_chunks, elem_align(d.wdtype));
+    const int cl = d.shared_inter / chunks;
+    c.n_dense = 0;
+    for (int i = 0; i < chunks; ++i) {
+      de::DenseSrc& ds = g.dense[nd++];
+      ds.w = static_cast<const char*>(shared_w) + 2 * (size_t)d.shared_inter * d.hidden * esz +
+             (size_t)i * cl * esz;
+      ds.inter = cl;
+      ds.ld = d.shared_inter;
+      ds.rows = d.hidden;
+      ds.gate = 1.0f;
+      ds.vin = at<float>(ws, L.a_s) + (size_t)i * cl;
+      ds.vin_stride = d.shared_inter;
+      ds.out = at<float>(ws, L.p_s) + (size_t)i * T * d.hidden;
+      ds.out_stride = d.hidden;
+      c.dense_p[c.n_dense++] = ds.out;
+    }
   }
   if (draft_w != nullptr && d.draft_inter > 0) {
     de::DenseSrc& ds = g.dense[nd++];
     ds.w = static_cast<const char*>(draft_w) + 2 * (size_t)d.draft_inter * d.hidden * esz;
+    ds.inter = d.draft_inter;
+    ds.ld = d.draft_inter;
     ds.rows = d.hidden;
     ds.gate = gamma;
     ds.vin = at<float>(ws, L.a_d);
     ds.vin_stride = d.draft_inter;
     ds.out = at<float>(ws, L.p_d);
     ds.out_stride = d.hidden;
+    c.dense_p[c.n_dense++] = ds.out;
   }
+  g.n_dense = nd;
   e = timed_phase(DE_PHASE_DOWN, s, [&] { return de::launch_down(g, d.wdtype, s); });
   if (e != hipSuccess) return DE_ERR_HIP;
   c.p_r = r.p;

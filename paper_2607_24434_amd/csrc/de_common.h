@@ -67,6 +67,7 @@ __device__ __forceinline__ u32x4 load_stream16(const void* p) {
 struct DenseSrc {
   const void* w;     // gate/up: the [G|U|D] block; down/rowdot: the [rows, len] matrix
   int inter;         // gate/up: rows of G and U.  down: reduction length
+  int ld;            // down: row stride of the matrix in elements (0: inter)
   int rows;          // down: output rows (H for experts, V for the LM head)
   float gate;        // down: scale of the result
   const float* vin;  // down: input vectors [T, vin_stride]
@@ -130,14 +131,14 @@ struct TopkUnionArgs {
   float* gate_list;
   int32_t* pair_pos;       // [T, ucols]
 };
-// Router scoring + top-k (+ union when sel.n_union is set) in one launch.
+// Router scoring, then top-k (+ union when sel.n_union is set): two launches.
 struct RouteArgs {
   TopkUnionArgs sel;       // sel.z is the logits scratch [T, N]
   const float* x;          // [T, H]
   const float* w;          // [N, H] fp32 router
   int H;
   float* z;                // == sel.z
-  unsigned* counter;       // zero between calls (last-block election)
+  int tok_per_block;       // set by the launcher
 };
 hipError_t launch_route(const RouteArgs& r, hipStream_t s);
 // Union only, from caller-supplied lists (sel.idx_in / sel.gate_in).

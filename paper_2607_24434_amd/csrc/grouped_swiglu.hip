@@ -1,56 +1,47 @@
 // Grouped SwiGLU over the expert union plus the shared / draft / dense
 // sources (Eq. 4 and Eq. 5 without the routing), the fixed-order combine, and
-// the row-dot kernel used for the LM head.
+// the row-dot used for the LM head.
 //
 // With a few block positions per expert the work is a batch of skinny GEMVs:
 // every weight byte meets only |T_e| positions, so the kernels are bound by
-// HBM bandwidth, not arithmetic.  The design keeps many 128-bit loads in
-// flight and touches each weight byte once:
+// HBM bandwidth, not arithmetic.  The design keeps the memory system busy
+// without pause and touches each weight byte once:
 //
-//  * Persistent 512-thread blocks.  The tiles of a launch (union members
-//    first, then the dense sources) form segments; block b owns a contiguous
-//    tile range whose cost (bytes x position passes) is 1/grid of the total,
-//    so the blocks finish together.  Within a range the 8 waves take every
-//    8th tile.  The number of union members stays in device memory.
-//  * A wave tile is NS weight rows streamed by all four 16-lane groups of the
-//    wave (GR = 4 groups per row): each wave load reads 1 KB of one row, and
-//    a lane issues the loads of MI 16-byte iterations before using them.
-//  * Activations are staged in LDS per block in a bank-conflict-free order
-//    (gate/up: the whole block of positions once; down: the segment's input
-//    rows), so only weights come from HBM.
-//  * bf16 -> fp32 by a shift or mask, fp32 accumulation; per-row sums use
-//    four DPP steps inside a 16-lane row and two cross-group shuffles, and are
-//    identical in every lane.  No float atomics: results are bitwise
-//    reproducible.
+//  * Persistent 512-thread blocks over a tile list: the union members' row
+//    tiles, then each dense source's.  Wave w of block b takes the tiles
+//    b*8 + w, then every (grid*8)-th one, so at any moment the whole grid
+//    streams a narrow window of consecutive rows.  The union size stays in
+//    device memory; the member table (weight block, first pair, positions)
+//    and the token / gate lists are copied to LDS at the start.
+//  * A tile is 4 weight rows (gate/up: two (G, U) row pairs) and expands into
+//    passes of up to 4 positions.  All 64 lanes of a wave stream the same
+//    rows: lane l owns the 16-byte units it*64 + l, so one load instruction
+//    reads 1 KB of a row (128-bit non-temporal loads).
+//  * The wave's passes form one flat sequence of 16-byte iterations.  A ring
+//    of kRing iterations (x 4 rows) of weights lives in registers: the loader
+//    runs kRing iterations ahead of the consumer across pass and tile
+//    boundaries, so the next tile's first loads are in flight while the
+//    current one finishes and its sums are reduced.
+//  * Activations come from LDS (the block of positions staged once, in a
+//    bank-conflict-free order) or, for the grouped down, from the small
+//    L2-resident A rows.
+//  * bf16 -> fp32 by a shift or mask, fp32 accumulation; a row sum is four DPP
+//    steps inside 16 lanes and two cross-row shuffles, identical in every
+//    lane.  No float atomics: results are bitwise reproducible.
 #include "de_common.h"
 
 // Build-time tuning knobs (kept at the measured best by default).
 #ifndef DE_NT_LOADS
 #define DE_NT_LOADS 1
 #endif
-#ifndef DE_GU_STRIDED
-#define DE_GU_STRIDED 1
+#ifndef DE_RING
+#define DE_RING 4
 #endif
-#ifndef DE_DN_STRIDED
-#define DE_DN_STRIDED 1
-#endif
-#ifndef DE_GU_PAIRS
-#define DE_GU_PAIRS 2
-#endif
-#ifndef DE_DN_ROWS
-#define DE_DN_ROWS 4
-#endif
-#ifndef DE_RD_ROWS
-#define DE_RD_ROWS 4
+#ifndef DE_DENSE_RING
+#define DE_DENSE_RING 2
 #endif
 #ifndef DE_DENSE_NT
-#define DE_DENSE_NT 4
-#endif
-#ifndef DE_TOK_GROUP
-#define DE_TOK_GROUP 4
-#endif
-#ifndef DE_REG_BUDGET
-#define DE_REG_BUDGET 96
+#define DE_DENSE_NT 9
 #endif
 
 namespace de {
@@ -58,30 +49,18 @@ namespace {
 
 constexpr int kBlock = 512;                 // 8 waves share the staged activations
 constexpr int kWavesPB = kBlock / kWave;
-constexpr int kTokGroup = DE_TOK_GROUP;               // positions whose activation loads may be hoisted together
-constexpr int kLdsBudget = 144 * 1024;      // staged activations per block (gate/up)
-constexpr int kDownLds = 72 * 1024;         // staged input rows per block (down): two blocks/CU
-
-// Wave tiles: every lane of a wave streams the same NS rows, 1 KB of one row
-// per load instruction.
-constexpr int kGuPairs = DE_GU_PAIRS;       // gate/up: (G row, U row) pairs
-constexpr int kDnRows = DE_DN_ROWS;         // grouped down: D rows
-constexpr int kRdRows = DE_RD_ROWS;         // row-dot (LM head, dense down): rows
+constexpr int kNS = 4;                      // weight rows per tile
 constexpr int kRoutedNT = 4;                // positions per pass of a union member
-constexpr int kDenseNT = DE_DENSE_NT;       // positions per pass of a dense source (cap)
+constexpr int kDenseNT = DE_DENSE_NT;       // positions per pass of a dense source
+constexpr int kMaxStaged = 32;              // union members with input rows staged per block (down)
+constexpr int kGuPairs = kNS / 2;           // gate/up: (G, U) row pairs per tile
+constexpr int kRing = DE_RING;              // 16-byte iterations in flight per lane (x kNS), members
+constexpr int kDenseRing = DE_DENSE_RING;   // the same, dense sources
+constexpr int kLdsBudget = 144 * 1024;      // staged activations + tables per block (gate/up)
+constexpr int kDownLds = 76 * 1024;         // staged inputs + tables per block (down): two blocks/CU
 
-// 16-byte iterations whose weight loads are issued together (NS*MI loads in
-// flight per lane): what the register budget leaves after the NS*NT
-// accumulators and one group of activations.
-template <int NS, int NT, int EPU>
-struct InFlight {
-  static constexpr int TG = NT < kTokGroup ? NT : kTokGroup;
-  static constexpr int free_regs = DE_REG_BUDGET - NS * NT - TG * EPU - EPU;
-  static constexpr int MI = free_regs / (4 * NS) > 4 ? 4 : (free_regs / (4 * NS) < 1 ? 1 : free_regs / (4 * NS));
-};
-
-// Dynamic LDS: the block's staged activation rows.
-extern __shared__ __align__(16) float s_act[];
+// Dynamic LDS: staged activation rows, then the member table and the lists.
+extern __shared__ __align__(16) float s_dyn[];
 
 template <typename WT>
 struct WTr;
@@ -121,9 +100,10 @@ __device__ __forceinline__ void unpack(const u32x4& r, float (&f)[4]) {
 
 // Staged layout of one activation row for bf16 weights: the 8 floats that
 // meet weight unit u (16 bytes = 8 bf16) are split into two float4 halves
-// stored at ((u/16)*2 + half)*16 + u%16, so the 16 lanes of a group read 256
-// contiguous bytes per ds_read_b128 (no bank conflicts).  Rows are padded to a
-// multiple of 128 floats.  fp32 weights (4 per unit) keep the natural order.
+// stored at ((u/16)*2 + half)*16 + u%16, so the 16 lanes of a row group read
+// 256 contiguous bytes per ds_read_b128 (no bank conflicts).  Rows are padded
+// to a multiple of 128 floats.  fp32 weights (4 per unit) keep the natural
+// order.
 __device__ __forceinline__ int perm_index(int u, int half) {
   return (((u >> 4) * 2 + half) * 16 + (u & 15)) * 4;
 }
@@ -133,18 +113,19 @@ __host__ __device__ __forceinline__ int staged_stride(int len) {
   return EPU == 8 ? ((len + 127) / 128) * 128 : len;
 }
 
-// The EPU activations that meet weight unit u of one row, from LDS (staged
-// layout, row at float offset `off`) or from global memory (natural layout).
-template <int EPU, bool LDSX>
+// The EPU activations that meet weight unit u of one row: from LDS (staged
+// layout, row at float offset `off`) when g is null, else from global memory
+// (natural layout).
+template <int EPU>
 __device__ __forceinline__ void act_frag(const float* g, int off, int u, float (&v)[EPU]) {
-  if constexpr (LDSX) {
+  if (g == nullptr) {
     if constexpr (EPU == 8) {
-      const float4 a = *reinterpret_cast<const float4*>(&s_act[off + perm_index(u, 0)]);
-      const float4 b = *reinterpret_cast<const float4*>(&s_act[off + perm_index(u, 1)]);
+      const float4 a = *reinterpret_cast<const float4*>(&s_dyn[off + perm_index(u, 0)]);
+      const float4 b = *reinterpret_cast<const float4*>(&s_dyn[off + perm_index(u, 1)]);
       v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
       v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
     } else {
-      const float4 a = *reinterpret_cast<const float4*>(&s_act[off + u * 4]);
+      const float4 a = *reinterpret_cast<const float4*>(&s_dyn[off + u * 4]);
       v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
     }
   } else {
@@ -171,72 +152,21 @@ __device__ __forceinline__ void stage_rows(const float* g, int gstride, int rows
     const int t = i / l4, h4 = i - t * l4;
     const f32x4 v = gptr<f32x4>(g + (size_t)t * gstride)[h4];
     const int dst = t * sst + (EPU == 8 ? perm_index(h4 >> 1, h4 & 1) : h4 * 4);
-    *reinterpret_cast<f32x4*>(&s_act[dst]) = v;
+    *reinterpret_cast<f32x4*>(&s_dyn[dst]) = v;
   }
 }
 
-// Dot products of NS weight rows (L 16-byte units each) with up to NT
-// activation rows.  Lane l owns the units it*64 + l; loads of MI iterations are
-// issued together, then consumed.  Past the row end a lane re-reads the last
-// unit (always in bounds) and zeroes it.  Activation row m starts at float
-// offset voff[m] (LDS or global).  The sums are partial per lane; row_total()
-// finishes them.
-template <typename WT, int NS, int NT, bool LDSX>
-__device__ __forceinline__ void rows_dot(const char* const (&rowp)[NS], int L, int lane,
-                                         const float* gact, const int (&voff)[NT], int nt,
-                                         float (&acc)[NS][NT]) {
-  constexpr int EPU = WTr<WT>::EPU;
-  constexpr int MI = InFlight<NS, NT, EPU>::MI;
-  constexpr int TG = InFlight<NS, NT, EPU>::TG;
-  const int nit = (L + kWave - 1) / kWave;
-  for (int i0 = 0; i0 < nit; i0 += MI) {
-    u32x4 raw[MI][NS];
-#pragma unroll
-    for (int q = 0; q < MI; ++q) {
-      if (i0 + q < nit) {
-        const uint32_t uc = (uint32_t)min((i0 + q) * kWave + lane, L - 1) * 16u;
-#pragma unroll
-        for (int s = 0; s < NS; ++s) raw[q][s] = load_w16(rowp[s] + uc);
-      }
-    }
-#pragma unroll
-    for (int q = 0; q < MI; ++q) {
-      if (i0 + q < nit) {
-        const int u = (i0 + q) * kWave + lane;
-        const bool ok = u < L;
-        const int uc = ok ? u : L - 1;
-        // Positions in groups of TG: the group's activations are loaded once
-        // and meet every row; a row's weights are unpacked when used.
-#pragma unroll
-        for (int mg = 0; mg < NT; mg += TG) {
-          if (mg < nt) {
-            float xv[TG][EPU];
-#pragma unroll
-            for (int m = 0; m < TG; ++m) {
-              if (mg + m < nt) {
-                act_frag<EPU, LDSX>(gact, voff[mg + m], uc, xv[m]);
-              } else {
-#pragma unroll
-                for (int v = 0; v < EPU; ++v) xv[m][v] = 0.f;
-              }
-            }
-#pragma unroll
-            for (int s = 0; s < NS; ++s) {
-              const u32x4 r = ok ? raw[q][s] : u32x4{0u, 0u, 0u, 0u};
-              float w[EPU];
-              unpack(r, w);
-#pragma unroll
-              for (int m = 0; m < TG; ++m)
-#pragma unroll
-                for (int v = 0; v < EPU; ++v) acc[s][mg + m] = fmaf(w[v], xv[m][v], acc[s][mg + m]);
-            }
-          }
-          // Keeps the next group's (or iteration's) activation loads from
-          // being hoisted above this one's arithmetic.
-          __builtin_amdgcn_sched_barrier(0);
-        }
-      }
-    }
+// The same, into LDS at dst.
+template <int EPU>
+__device__ __forceinline__ void stage_rows_at(float* dst, const float* g, int gstride, int rows,
+                                              int len) {
+  const int l4 = len >> 2;
+  const int sst = staged_stride<EPU>(len);
+  for (int i = threadIdx.x; i < rows * l4; i += kBlock) {
+    const int t = i / l4, h4 = i - t * l4;
+    const f32x4 v = gptr<f32x4>(g + (size_t)t * gstride)[h4];
+    const int o = t * sst + (EPU == 8 ? perm_index(h4 >> 1, h4 & 1) : h4 * 4);
+    *reinterpret_cast<f32x4*>(dst + o) = v;
   }
 }
 
@@ -249,11 +179,12 @@ __device__ __forceinline__ float row_total(float v) {
   return v;
 }
 
-__device__ __forceinline__ int cdiv(int a, int b) { return (a + b - 1) / b; }
+__host__ __device__ __forceinline__ int cdiv(int a, int b) { return (a + b - 1) / b; }
 
-// Values that are the same in every lane (tile and segment metadata, read from
-// memory) are moved to scalar registers; the compiler cannot prove it itself
-// for loaded values, and keeping them in vector registers causes spills.
+// Values that are the same in every lane (tile and pass metadata, read from
+// memory or produced by integer division, which has no scalar instruction)
+// are moved to scalar registers; the compiler cannot prove it itself, and
+// keeping them in vector registers causes spills.
 __device__ __forceinline__ int uni(int v) { return __builtin_amdgcn_readfirstlane(v); }
 template <typename P>
 __device__ __forceinline__ P* uni(P* p) {
@@ -263,448 +194,548 @@ __device__ __forceinline__ P* uni(P* p) {
   return reinterpret_cast<P*>(((uint64_t)hi << 32) | lo);
 }
 
+// The dense sources are read from an LDS copy (Tables::dense): a run-time
+// index into the kernel argument (a.dense[s]) makes the compiler copy the
+// whole argument to per-lane scratch memory.
+
+// ------------------------------------------------------------------ block tables
+
+// A union member as a block sees it: its weight block (null when the expert
+// is not resident or the lists are malformed), first pair, positions, and the
+// LDS float offset of its staged input rows (down only; -1: global memory).
+struct Member {
+  const char* blk;
+  int off;
+  int ntok;
+  int act;
+  int pad;
+};
+
+// LDS layout: [staged activations: act_floats][dense: 3][members: max_union]
+//             [tok: pairs_max][gate: pairs_max]
+struct Tables {
+  DenseSrc* dense;
+  Member* mem;
+  int32_t* tok;
+  float* gate;
+};
+
+size_t tables_bytes(const GroupedArgs& a) {
+  size_t b = 3 * sizeof(DenseSrc);
+  if (a.has_routed) b += (size_t)a.r.max_union * sizeof(Member) + (size_t)a.r.pairs_max * 8;
+  return b;
+}
+
+__device__ __forceinline__ Tables tables_at(const GroupedArgs& a, int act_floats) {
+  Tables tb;
+  char* p = reinterpret_cast<char*>(s_dyn + act_floats);
+  tb.dense = reinterpret_cast<DenseSrc*>(p);
+  p += 3 * sizeof(DenseSrc);
+  tb.mem = reinterpret_cast<Member*>(p);
+  const int nm = a.has_routed ? a.r.max_union : 0;
+  tb.tok = reinterpret_cast<int32_t*>(p + (size_t)nm * sizeof(Member));
+  tb.gate = reinterpret_cast<float*>(tb.tok + (a.has_routed ? a.r.pairs_max : 0));
+  return tb;
+}
+
+// Dense source s from the LDS copy, in scalar registers.
+__device__ __forceinline__ DenseSrc dense_at(const Tables& tb, int s) {
+  const DenseSrc& g = tb.dense[s];
+  DenseSrc d;
+  d.w = uni(g.w);
+  d.inter = uni(g.inter);
+  d.ld = uni(g.ld);
+  d.rows = uni(g.rows);
+  d.gate = __int_as_float(uni(__float_as_int(g.gate)));
+  d.vin = uni(g.vin);
+  d.vin_stride = uni(g.vin_stride);
+  d.out = uni(g.out);
+  d.out_stride = uni(g.out_stride);
+  return d;
+}
+
+// Copies the dense-source descriptors to LDS (static indices only).  The
+// caller synchronises.
+__device__ __forceinline__ void fill_dense(const GroupedArgs& a, const Tables& tb) {
+  if (threadIdx.x == 0 && a.n_dense > 0) tb.dense[0] = a.dense[0];
+  if (threadIdx.x == 1 && a.n_dense > 1) tb.dense[1] = a.dense[1];
+  if (threadIdx.x == 2 && a.n_dense > 2) tb.dense[2] = a.dense[2];
+}
+
+// Resolves the union members into LDS.  Lists built by the union kernel always
+// pass; caller-supplied ones are checked so that a bad list can only drop
+// work, never read or write out of bounds.  All threads; the caller
+// synchronises.
+__device__ __forceinline__ void fill_tables(const GroupedArgs& a, const Tables& tb, int nu) {
+  const RoutedSrc& r = a.r;
+  for (int j = threadIdx.x; j < nu; j += kBlock) {
+    Member m{nullptr, 0, 0, -1, 0};
+    const int e = r.union_ids[j];
+    const int slot =
+        (e >= 0 && e < r.max_union) ? (r.slot_of_expert ? r.slot_of_expert[e] : e) : -1;
+    const int off = r.offsets[j], end = r.offsets[j + 1];
+    if (slot >= 0 && slot < r.n_slots && off >= 0 && end >= off && end <= r.pairs_max) {
+      m.blk = r.base + (size_t)slot * r.stride;
+      m.off = off;
+      m.ntok = end - off;
+    }
+    tb.mem[j] = m;
+  }
+  for (int i = threadIdx.x; i < r.pairs_max; i += kBlock) {
+    const int t = r.tok_list[i];
+    tb.tok[i] = t < 0 ? 0 : (t >= a.T ? a.T - 1 : t);  // a position outside the block never indexes x
+    tb.gate[i] = r.gate_list[i];
+  }
+}
+
 __device__ __forceinline__ int routed_count(const GroupedArgs& a) {
   if (!a.has_routed) return 0;
   const int nu = uni(*a.r.n_union);
   return nu < 0 ? 0 : min(nu, a.r.max_union);
 }
 
-// Resolves union member j to its weight block and token-list span; nullptr
-// when the expert is not resident or the lists are malformed (lists built by
-// the union kernel always pass; caller-supplied ones are checked so that a
-// bad list can only drop work, never read or write out of bounds).
-__device__ __forceinline__ const char* member_block(const RoutedSrc& r, int j, int& off,
-                                                    int& ntok) {
-  const int e = uni(r.union_ids[j]);
-  if (e < 0 || e >= r.max_union) return nullptr;
-  const int slot = uni(r.slot_of_expert ? r.slot_of_expert[e] : e);
-  if (slot < 0 || slot >= r.n_slots) return nullptr;
-  off = uni(r.offsets[j]);
-  const int end = uni(r.offsets[j + 1]);
-  if (off < 0 || end < off || end > r.pairs_max) return nullptr;
-  ntok = end - off;
-  return uni(r.base + (size_t)slot * r.stride);
-}
+// ------------------------------------------------------------------ the pass stream
 
-// a.dense[s] with a run-time s would copy the kernel-argument array to scratch
-// memory; an explicit select keeps everything in scalar registers.
-__device__ __forceinline__ DenseSrc pick_dense(const GroupedArgs& a, int s) {
-  return s == 0 ? a.dense[0] : (s == 1 ? a.dense[1] : a.dense[2]);
-}
-
-// Tiles are laid out as consecutive segments (the union members, then each
-// dense source); every tile of a segment has the same cost.  Block b owns the
-// contiguous tile range whose cost covers [b, b+1) * total / grid.
-struct Segments {
-  int n;
-  int tiles[4];
-  long long cost[4];  // per tile
+// One pass: kNS weight rows against up to NT activation rows.
+template <int NT>
+struct Pass {
+  const char* row[kNS];
+  int L;               // 16-byte units per row
+  int nit;             // wave iterations: ceil(L / 64)
+  int nt;              // positions
+  const float* act;    // activation base; null: LDS
+  int vo[NT];          // activation offsets (floats)
+  int r0;              // gate/up: first (G, U) pair; down: first row
+  int rows;            // rows (pairs) of the source
+  float* out;
+  int ostride;
+  int orow0;           // output row of the pass's first position
+  int goff;            // routed down: gate-list index of the first position; -1: gscalar
+  float gscalar;
 };
 
-__device__ __forceinline__ int tile_at_cost(const Segments& sg, long long c) {
-  int t0 = 0;
-  long long c0 = 0;
-  for (int i = 0; i < sg.n; ++i) {
-    const long long seg = (long long)sg.tiles[i] * sg.cost[i];
-    if (c < c0 + seg) return t0 + (int)((c - c0 + sg.cost[i] - 1) / sg.cost[i]);
-    t0 += sg.tiles[i];
-    c0 += seg;
+// Tile list of a launch: the dense sources' tiles first (source s from ds[s]),
+// then the union members' tiles from ndt (member j: tr tiles).  Named fields:
+// an array indexed at run time would live in per-lane scratch memory.
+struct Layout {
+  int ndt, tr, nr, total, nd;
+  int ds1, ds2;
+  int act0, act1, act2;  // down: LDS offsets of the dense sources' staged inputs (-1: global)
+
+  __device__ __forceinline__ int source(int t, int& start, int& act) const {
+    if (nd > 2 && t >= ds2) {
+      start = ds2;
+      act = act2;
+      return 2;
+    }
+    if (nd > 1 && t >= ds1) {
+      start = ds1;
+      act = act1;
+      return 1;
+    }
+    start = 0;
+    act = act0;
+    return 0;
   }
-  return t0;
+};
+
+__device__ __forceinline__ Layout make_layout(const GroupedArgs& a, int nu, bool gateup) {
+  Layout ly;
+  const int per = gateup ? kGuPairs : kNS;
+  const int n0 = a.n_dense > 0 ? uni(cdiv(gateup ? a.dense[0].inter : a.dense[0].rows, per)) : 0;
+  const int n1 = a.n_dense > 1 ? uni(cdiv(gateup ? a.dense[1].inter : a.dense[1].rows, per)) : 0;
+  const int n2 = a.n_dense > 2 ? uni(cdiv(gateup ? a.dense[2].inter : a.dense[2].rows, per)) : 0;
+  ly.nd = a.n_dense;
+  ly.ds1 = n0;
+  ly.ds2 = n0 + n1;
+  ly.ndt = n0 + n1 + n2;
+  ly.tr = a.has_routed ? uni(cdiv(gateup ? a.r.inter : a.H, per)) : 0;
+  ly.nr = nu * ly.tr;
+  ly.total = ly.ndt + ly.nr;
+  ly.act0 = ly.act1 = ly.act2 = -1;
+  return ly;
 }
 
-// Integer division has no scalar instruction, so its results land in vector
-// registers; lo and hi are moved back to scalar ones.
-__device__ __forceinline__ void block_range(const Segments& sg, int& lo, int& hi) {
-  long long total = 0;
-  for (int i = 0; i < sg.n; ++i) total += (long long)sg.tiles[i] * sg.cost[i];
-  lo = uni(tile_at_cost(sg, total * blockIdx.x / gridDim.x));
-  hi = uni(tile_at_cost(sg, total * (blockIdx.x + 1) / gridDim.x));
+// A wave's position in its sequence of passes: tile, first position of the
+// pass, positions of the tile.
+struct Cursor {
+  int tile, m0, ntok;
+};
+
+// The passes of a wave's tiles in [lo, hi) (tiles b*8 + w + k * step).
+template <typename WT, bool GATEUP, int NT>
+struct Walker {
+  Layout ly;      // by value: a reference to a local would live in per-lane scratch
+  Tables tb;
+  int step;       // grid * waves
+  int lo, hi;
+  int xstride;    // gate/up: row stride of the staged (or global) x
+  bool xlds;      // gate/up: x is staged in LDS
+
+  // Fills p for tile c.tile at position c.m0; c.ntok receives the tile's
+  // position count.  False when the tile's member is not resident.
+  __device__ __forceinline__ bool make(const GroupedArgs& a, Cursor& c, Pass<NT>& p) const {
+    constexpr size_t esz = sizeof(WT);
+    constexpr int EPU = WTr<WT>::EPU;
+    const int H = a.H;
+    if (c.tile >= ly.ndt) {
+      const int j = uni((c.tile - ly.ndt) / ly.tr);
+      const int rg = c.tile - ly.ndt - j * ly.tr;
+      const Member mb = tb.mem[j];
+      const char* blk = uni(mb.blk);
+      if (blk == nullptr) return false;
+      const int off = uni(mb.off);
+      c.ntok = uni(mb.ntok);
+      const int I = a.r.inter;
+      p.nt = min(NT, c.ntok - c.m0);
+      p.orow0 = off + c.m0;
+      if constexpr (GATEUP) {
+        const size_t rb = (size_t)H * esz;
+        const char* U = blk + (size_t)I * rb;
+        p.r0 = rg * kGuPairs;
+        p.rows = I;
+#pragma unroll
+        for (int q = 0; q < kGuPairs; ++q) {
+          const size_t rc = (size_t)min(p.r0 + q, I - 1);
+          p.row[2 * q] = blk + rc * rb;
+          p.row[2 * q + 1] = U + rc * rb;
+        }
+        p.L = (int)(rb / 16);
+        p.act = xlds ? nullptr : a.x;
+#pragma unroll
+        for (int m = 0; m < NT; ++m) p.vo[m] = uni(tb.tok[p.orow0 + min(m, p.nt - 1)]) * xstride;
+        p.out = a.r.a;
+        p.ostride = I;
+        p.goff = -1;
+      } else {
+        const size_t rb = (size_t)I * esz;
+        const char* D = blk + 2 * (size_t)I * H * esz;
+        p.r0 = rg * kNS;
+        p.rows = H;
+#pragma unroll
+        for (int k = 0; k < kNS; ++k) p.row[k] = D + (size_t)min(p.r0 + k, H - 1) * rb;
+        p.L = (int)(rb / 16);
+        const int act = uni(mb.act);
+        if (act >= 0) {
+          const int sst = staged_stride<EPU>(I);
+          p.act = nullptr;
+#pragma unroll
+          for (int m = 0; m < NT; ++m) p.vo[m] = act + (c.m0 + min(m, p.nt - 1)) * sst;
+        } else {
+          p.act = a.r.a;
+#pragma unroll
+          for (int m = 0; m < NT; ++m) p.vo[m] = (p.orow0 + min(m, p.nt - 1)) * I;
+        }
+        p.out = a.r.p;
+        p.ostride = H;
+        p.goff = p.orow0;
+      }
+      p.gscalar = 0.f;
+    } else {
+      int start = 0, dact = -1;
+      const int s = ly.source(c.tile, start, dact);
+      const DenseSrc d = dense_at(tb, s);
+      const int rg = c.tile - start;
+      c.ntok = a.T;
+      p.nt = min(NT, a.T - c.m0);
+      p.orow0 = c.m0;
+      const char* W = static_cast<const char*>(d.w);
+      if constexpr (GATEUP) {
+        const size_t rb = (size_t)H * esz;
+        const char* U = W + (size_t)d.inter * rb;
+        p.r0 = rg * kGuPairs;
+        p.rows = d.inter;
+#pragma unroll
+        for (int q = 0; q < kGuPairs; ++q) {
+          const size_t rc = (size_t)min(p.r0 + q, d.inter - 1);
+          p.row[2 * q] = W + rc * rb;
+          p.row[2 * q + 1] = U + rc * rb;
+        }
+        p.L = (int)(rb / 16);
+        p.act = xlds ? nullptr : a.x;
+#pragma unroll
+        for (int m = 0; m < NT; ++m) p.vo[m] = (c.m0 + min(m, p.nt - 1)) * xstride;
+        p.out = d.out;
+        p.ostride = d.inter;
+      } else {
+        const size_t rb = (size_t)(d.ld > 0 ? d.ld : d.inter) * esz;
+        p.r0 = rg * kNS;
+        p.rows = d.rows;
+#pragma unroll
+        for (int k = 0; k < kNS; ++k) p.row[k] = W + (size_t)min(p.r0 + k, d.rows - 1) * rb;
+        p.L = (int)((size_t)d.inter * esz / 16);
+        const int act = dact;
+        if (act >= 0) {
+          const int sst = staged_stride<EPU>(d.inter);
+          p.act = nullptr;
+#pragma unroll
+          for (int m = 0; m < NT; ++m) p.vo[m] = act + (c.m0 + min(m, p.nt - 1)) * sst;
+        } else {
+          p.act = d.vin;
+#pragma unroll
+          for (int m = 0; m < NT; ++m) p.vo[m] = (c.m0 + min(m, p.nt - 1)) * d.vin_stride;
+        }
+        p.out = d.out;
+        p.ostride = d.out_stride;
+      }
+      p.goff = -1;
+      p.gscalar = d.gate;
+    }
+    p.nit = (p.L + kWave - 1) / kWave;
+    return true;
+  }
+
+  // The first pass at or after tile c.tile; false at the end of the range.
+  __device__ __forceinline__ bool seek(const GroupedArgs& a, Cursor& c, Pass<NT>& p) const {
+    c.m0 = 0;
+    while (c.tile < hi) {
+      if (make(a, c, p) && c.ntok > 0) return true;
+      c.tile += step;
+    }
+    return false;
+  }
+
+  // The pass after c; false at the end of the range.
+  __device__ __forceinline__ bool next(const GroupedArgs& a, Cursor& c, Pass<NT>& p) const {
+    c.m0 += NT;
+    if (c.m0 < c.ntok) return make(a, c, p);
+    c.tile += step;
+    return seek(a, c, p);
+  }
+};
+
+// Loads iteration `it` of pass p (kNS rows) into r.  Past a row's end the lane
+// re-reads the last unit (always in bounds); consume() zeroes it.
+template <int NT>
+__device__ __forceinline__ void issue(const Pass<NT>& p, int it, u32x4 (&r)[kNS], int lane) {
+  const uint32_t uc = (uint32_t)min(it * kWave + lane, p.L - 1) * 16u;
+#pragma unroll
+  for (int k = 0; k < kNS; ++k) r[k] = load_w16(p.row[k] + uc);
 }
 
-// ------------------------------------------------------------------ gate/up
-
-constexpr int kGuRows = kGuPairs;  // (G, U) row pairs per wave tile
-
-// One pass (up to NT positions) over the (G, U) row pairs r0 .. r0+kGuPairs-1:
-// A[arow0 + m][r] = silu(G_r . x_m) * (U_r . x_m).
-template <typename WT, int NT, bool LDSX>
-__device__ __forceinline__ void gateup_pass(const char* G, const char* U, int inter, int H, int r0,
-                                            int lane, const float* gx, const int (&voff)[NT],
-                                            int nt, float* A, int arow0) {
-  constexpr int NS = 2 * kGuPairs;
-  const size_t rb = (size_t)H * sizeof(WT);
-  const char* rowp[NS];
-#pragma unroll
-  for (int p = 0; p < kGuPairs; ++p) {
-    const size_t rc = (size_t)min(r0 + p, inter - 1);
-    rowp[2 * p] = G + rc * rb;
-    rowp[2 * p + 1] = U + rc * rb;
-  }
-  float acc[NS][NT];
-#pragma unroll
-  for (int k = 0; k < NS; ++k)
-#pragma unroll
-    for (int m = 0; m < NT; ++m) acc[k][m] = 0.f;
-  rows_dot<WT, NS, NT, LDSX>(rowp, (int)(rb / 16), lane, gx, voff, nt, acc);
+// Accumulates iteration `it` of pass p.
+template <typename WT, int NT>
+__device__ __forceinline__ void consume(const Pass<NT>& p, int it, const u32x4 (&r)[kNS], int lane,
+                                        float (&acc)[kNS][NT]) {
+  constexpr int EPU = WTr<WT>::EPU;
+  const int u = it * kWave + lane;
+  const bool ok = u < p.L;
+  const int uc = ok ? u : p.L - 1;
 #pragma unroll
   for (int m = 0; m < NT; ++m) {
-    if (m < nt) {
+    if (m < p.nt) {
+      float xv[EPU];
+      act_frag<EPU>(p.act, p.vo[m], uc, xv);
 #pragma unroll
-      for (int p = 0; p < kGuPairs; ++p) {
-        const float g = row_total(acc[2 * p][m]);
-        const float u = row_total(acc[2 * p + 1][m]);
-        if (lane == m && r0 + p < inter) A[(size_t)(arow0 + m) * inter + r0 + p] = silu_f(g) * u;
+      for (int k = 0; k < kNS; ++k) {
+        const u32x4 rr = ok ? r[k] : u32x4{0u, 0u, 0u, 0u};
+        float w[EPU];
+        unpack(rr, w);
+#pragma unroll
+        for (int v = 0; v < EPU; ++v) acc[k][m] = fmaf(w[v], xv[v], acc[k][m]);
+      }
+    }
+    // Keeps the next position's activation loads from being hoisted above
+    // this one's arithmetic.
+    __builtin_amdgcn_sched_barrier(0);
+  }
+}
+
+// Reduces the pass's sums and writes them; clears acc.
+template <bool GATEUP, int NT>
+__device__ __forceinline__ void finish(const Pass<NT>& p, const Tables& tb, int lane,
+                                       float (&acc)[kNS][NT]) {
+#pragma unroll
+  for (int m = 0; m < NT; ++m) {
+    if (m < p.nt) {
+      if constexpr (GATEUP) {
+#pragma unroll
+        for (int q = 0; q < kGuPairs; ++q) {
+          const float g = row_total(acc[2 * q][m]);
+          const float u = row_total(acc[2 * q + 1][m]);
+          if (lane == m && p.r0 + q < p.rows)
+            p.out[(size_t)(p.orow0 + m) * p.ostride + p.r0 + q] = silu_f(g) * u;
+        }
+      } else {
+        const float gm = p.goff >= 0 ? tb.gate[p.goff + m] : p.gscalar;
+#pragma unroll
+        for (int k = 0; k < kNS; ++k) {
+          const float v = row_total(acc[k][m]);
+          if (lane == m && p.r0 + k < p.rows)
+            p.out[(size_t)(p.orow0 + m) * p.ostride + p.r0 + k] = gm * v;
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int k = 0; k < kNS; ++k)
+#pragma unroll
+    for (int m = 0; m < NT; ++m) acc[k][m] = 0.f;
+}
+
+// Streams the wave's pass sequence: the loader runs RING iterations ahead of
+// the consumer, across pass and tile boundaries.
+template <typename WT, bool GATEUP, int NT, int RING>
+__device__ __forceinline__ void run_stream(const GroupedArgs& a, const Walker<WT, GATEUP, NT> wk,
+                                           int first_tile, int lane) {
+  Cursor lc{first_tile, 0, 0}, cc{first_tile, 0, 0};
+  Pass<NT> lp, cp;
+  bool l_ok = wk.seek(a, lc, lp);
+  bool c_ok = wk.seek(a, cc, cp);
+  int l_it = 0, c_it = 0;
+  u32x4 raw[RING][kNS];
+#pragma unroll
+  for (int q = 0; q < RING; ++q) {
+    if (l_ok) {
+      issue(lp, l_it, raw[q], lane);
+      if (++l_it == lp.nit) {
+        l_ok = wk.next(a, lc, lp);
+        l_it = 0;
+      }
+    }
+  }
+  float acc[kNS][NT];
+#pragma unroll
+  for (int k = 0; k < kNS; ++k)
+#pragma unroll
+    for (int m = 0; m < NT; ++m) acc[k][m] = 0.f;
+  while (c_ok) {
+#pragma unroll
+    for (int q = 0; q < RING; ++q) {
+      if (c_ok) {
+        consume<WT, NT>(cp, c_it, raw[q], lane, acc);
+        if (++c_it == cp.nit) {
+          finish<GATEUP, NT>(cp, wk.tb, lane, acc);
+          c_ok = wk.next(a, cc, cp);
+          c_it = 0;
+        }
+        if (l_ok) {
+          issue(lp, l_it, raw[q], lane);
+          if (++l_it == lp.nit) {
+            l_ok = wk.next(a, lc, lp);
+            l_it = 0;
+          }
+        }
       }
     }
   }
 }
 
-// Activation offsets of one pass (token list or consecutive positions).
-template <int NT>
-__device__ __forceinline__ void pass_offsets(int (&voff)[NT], const int32_t* tok, int tok_base,
-                                             int nt, int T, int stride) {
-#pragma unroll
-  for (int m = 0; m < NT; ++m) {
-    int t = uni(m < nt ? (tok ? tok[m] : tok_base + m) : tok_base);
-    t = t < 0 ? 0 : (t >= T ? T - 1 : t);  // a position outside the block never indexes x
-    voff[m] = t * stride;
+// A wave's tiles: first, first + step, ...  The dense tiles [0, ndt) run with
+// passes of kDenseNT positions, the members' tiles with kRoutedNT.
+template <typename WT, bool GATEUP>
+__device__ __forceinline__ void run_tiles(const GroupedArgs& a, const Layout ly, const Tables& tb,
+                                          int xstride, bool xlds, int lane, int wave) {
+  const int step = (int)gridDim.x * kWavesPB;
+  const int first = (int)blockIdx.x * kWavesPB + wave;
+  if (first < ly.ndt) {
+    const Walker<WT, GATEUP, kDenseNT> wd{ly, tb, step, 0, ly.ndt, xstride, xlds};
+    run_stream<WT, GATEUP, kDenseNT, kDenseRing>(a, wd, first, lane);
+  }
+  if (ly.nr > 0) {
+    const int f2 = first >= ly.ndt ? first : first + cdiv(ly.ndt - first, step) * step;
+    const Walker<WT, GATEUP, kRoutedNT> wr{ly, tb, step, ly.ndt, ly.total, xstride, xlds};
+    run_stream<WT, GATEUP, kRoutedNT, kRing>(a, wr, f2, lane);
   }
 }
 
-// Every pass over one wave tile of a source: its ntok positions (token list
-// tok, or 0..ntok-1) in passes of NTP, a single remaining position by the
-// one-position variant.  The passes run back to back, so the later ones find
-// the rows in cache.
-template <typename WT, int NTP, bool LDSX>
-__device__ __forceinline__ void gateup_tile(const char* G, const char* U, int inter, int H, int r0,
-                                            int lane, const float* gx, int xstride, int T,
-                                            const int32_t* tok, int ntok, float* A, int arow0) {
-  for (int m0 = 0; m0 < ntok; m0 += NTP) {
-    const int nt = min(NTP, ntok - m0);
-    const int32_t* tk = tok ? tok + m0 : nullptr;
-    if (nt == 1) {
-      int voff[1];
-      pass_offsets<1>(voff, tk, m0, 1, T, xstride);
-      gateup_pass<WT, 1, LDSX>(G, U, inter, H, r0, lane, gx, voff, 1, A, arow0 + m0);
-    } else {
-      int voff[NTP];
-      pass_offsets<NTP>(voff, tk, m0, nt, T, xstride);
-      gateup_pass<WT, NTP, LDSX>(G, U, inter, H, r0, lane, gx, voff, nt, A, arow0 + m0);
-    }
-  }
-}
+// ------------------------------------------------------------------ kernels
 
-// Persistent gate/up kernel over the union members and the dense sources.
-// Tiles: union member j covers tiles [j*tr, (j+1)*tr), then each dense source.
+// Gate/up: A = silu(G x) * (U x) for the dense sources and the union members'
+// pairs.  LDSX: the block of positions is staged in LDS.
 template <typename WT, bool LDSX>
 __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) void gateup_kernel(
     GroupedArgs a) {
   constexpr int EPU = WTr<WT>::EPU;
   const int lane = threadIdx.x & 63, wave = uni((int)(threadIdx.x >> 6));
-  int xstride = a.H;
-  if constexpr (LDSX) {
-    stage_rows<EPU>(a.x, a.H, a.T, a.H);
-    __syncthreads();
-    xstride = staged_stride<EPU>(a.H);
-  }
+  const int act_floats = LDSX ? a.T * staged_stride<EPU>(a.H) : 0;
   const int nu = routed_count(a);
-  const int tr = uni(a.has_routed ? cdiv(a.r.inter, kGuRows) : 0);
-  const int nr = nu * tr;
-  const size_t esz = sizeof(WT);
-  int dstart[4];
-  int total = nr;
-  for (int s = 0; s < a.n_dense; ++s) {
-    dstart[s] = total;
-    total += uni(cdiv(a.dense[s].inter, kGuRows));
-  }
-  dstart[a.n_dense] = total;
-#if DE_GU_STRIDED
-  // Grid-strided tile order: at any moment the whole grid streams a narrow
-  // window of consecutive rows.
-  int cur_j = -1, off = 0, ntok = 0;
-  const char* blk = nullptr;
-  for (int tile = blockIdx.x * kWavesPB + wave; tile < total; tile += gridDim.x * kWavesPB) {
-    if (tile < nr) {
-      const int j = uni(tile / tr);
-      if (j != cur_j) {
-        blk = member_block(a.r, j, off, ntok);
-        cur_j = j;
-      }
-      if (blk == nullptr) continue;
-      gateup_tile<WT, kRoutedNT, LDSX>(blk, blk + (size_t)a.r.inter * a.H * esz, a.r.inter, a.H,
-                                       (tile - j * tr) * kGuRows, lane, a.x, xstride, a.T,
-                                       a.r.tok_list + off, ntok, a.r.a, off);
-    } else {
-      int s = 0;
-      while (s + 1 < a.n_dense && tile >= dstart[s + 1]) ++s;
-      const DenseSrc d = pick_dense(a, s);
-      const char* G = static_cast<const char*>(d.w);
-      gateup_tile<WT, kDenseNT, LDSX>(G, G + (size_t)d.inter * a.H * esz, d.inter, a.H,
-                                      (tile - dstart[s]) * kGuRows, lane, a.x, xstride, a.T,
-                                      nullptr, a.T, d.out, 0);
-    }
-  }
-#else
-  // Contiguous order: block b owns the tile range whose cost (bytes x passes)
-  // is 1/grid of the total; its waves take every 8th tile of the range.
-  Segments sg;
-  const long long row_cost = (long long)a.H * sizeof(WT) * 2 * kGuRows;
-  sg.n = 0;
-  sg.tiles[sg.n] = nr;
-  sg.cost[sg.n++] = row_cost;  // one pass for a member in the common case
-  for (int s = 0; s < a.n_dense; ++s) {
-    sg.tiles[sg.n] = dstart[s + 1] - dstart[s];
-    sg.cost[sg.n++] = row_cost * ((a.T + kDenseNT - 1) / kDenseNT);
-  }
-  int lo, hi;
-  block_range(sg, lo, hi);
-  int t = lo;
-  while (t < hi) {
-    if (t < nr) {
-      const int j = uni(t / tr), seg0 = j * tr, t1 = min(hi, seg0 + tr);
-      int off = 0, ntok = 0;
-      const char* blk = member_block(a.r, j, off, ntok);
-      if (blk != nullptr)
-        for (int tile = t + wave; tile < t1; tile += kWavesPB)
-          gateup_tile<WT, kRoutedNT, LDSX>(blk, blk + (size_t)a.r.inter * a.H * esz, a.r.inter,
-                                           a.H, (tile - seg0) * kGuRows, lane, a.x, xstride, a.T,
-                                           a.r.tok_list + off, ntok, a.r.a, off);
-      t = t1;
-    } else {
-      int s = 0;
-      while (s + 1 < a.n_dense && t >= dstart[s + 1]) ++s;
-      const DenseSrc d = pick_dense(a, s);
-      const int seg0 = dstart[s], t1 = min(hi, dstart[s + 1]);
-      const char* G = static_cast<const char*>(d.w);
-      for (int tile = t + wave; tile < t1; tile += kWavesPB)
-        gateup_tile<WT, kDenseNT, LDSX>(G, G + (size_t)d.inter * a.H * esz, d.inter, a.H,
-                                        (tile - seg0) * kGuRows, lane, a.x, xstride, a.T, nullptr,
-                                        a.T, d.out, 0);
-      t = t1;
-    }
-  }
-#endif
+  const Tables tb = tables_at(a, act_floats);
+  if constexpr (LDSX) stage_rows<EPU>(a.x, a.H, a.T, a.H);
+  fill_dense(a, tb);
+  if (a.has_routed) fill_tables(a, tb, nu);
+  __syncthreads();
+  const Layout ly = make_layout(a, nu, true);
+  run_tiles<WT, true>(a, ly, tb, LDSX ? staged_stride<EPU>(a.H) : a.H, LDSX, lane, wave);
 }
 
-// ------------------------------------------------------------------ down / row-dot
-
-// One pass over the NS rows r0.. of a [rows, len] matrix for up to NT inputs:
-// out[orow0 + m][r] = gate_m * (M_r . v_m).
-template <typename WT, int NS, int NT, bool LDSX>
-__device__ __forceinline__ void down_pass(const char* M, int rows, int len, int r0, int lane,
-                                          const float* gv, const int (&voff)[NT], int nt,
-                                          const float* gates, float gscalar, float* out,
-                                          int ostride, int orow0) {
-  const size_t rb = (size_t)len * sizeof(WT);
-  const char* rowp[NS];
-#pragma unroll
-  for (int k = 0; k < NS; ++k) rowp[k] = M + (size_t)min(r0 + k, rows - 1) * rb;
-  float acc[NS][NT];
-#pragma unroll
-  for (int k = 0; k < NS; ++k)
-#pragma unroll
-    for (int m = 0; m < NT; ++m) acc[k][m] = 0.f;
-  rows_dot<WT, NS, NT, LDSX>(rowp, (int)(rb / 16), lane, gv, voff, nt, acc);
-#pragma unroll
-  for (int m = 0; m < NT; ++m) {
-    if (m < nt) {
-      const float gm = gates ? gates[m] : gscalar;
-#pragma unroll
-      for (int k = 0; k < NS; ++k) {
-        const float v = row_total(acc[k][m]);
-        if (lane == m && r0 + k < rows) out[(size_t)(orow0 + m) * ostride + r0 + k] = gm * v;
-      }
-    }
-  }
-}
-
-// Every pass over one wave tile for the inputs vrow0 .. vrow0+n-1 (rows of
-// length len at stride vstride, LDS or global), NTP per pass, a single
-// remaining input by the one-input variant.
-template <typename WT, int NS, int NTP, bool LDSX>
-__device__ __forceinline__ void down_tile(const char* M, int rows, int len, int r0, int lane,
-                                          const float* gv, int vstride, int vrow0, int n,
-                                          const float* gates, float gscalar, float* out,
-                                          int ostride, int orow0) {
-  for (int m0 = 0; m0 < n; m0 += NTP) {
-    const int nt = min(NTP, n - m0);
-    const float* gt = gates ? gates + m0 : nullptr;
-    if (nt == 1) {
-      const int voff[1] = {(vrow0 + m0) * vstride};
-      down_pass<WT, NS, 1, LDSX>(M, rows, len, r0, lane, gv, voff, 1, gt, gscalar, out, ostride,
-                                 orow0 + m0);
-    } else {
-      int voff[NTP];
-#pragma unroll
-      for (int m = 0; m < NTP; ++m) voff[m] = (vrow0 + m0 + (m < nt ? m : 0)) * vstride;
-      down_pass<WT, NS, NTP, LDSX>(M, rows, len, r0, lane, gv, voff, nt, gt, gscalar, out,
-                                   ostride, orow0 + m0);
-    }
-  }
-}
-
-// One source of the down kernel, resolved for tile t.
-struct DownSeg {
-  const char* M;
-  const float* vin;
-  const float* gates;
-  float* out;
-  float gscalar;
-  int rows, len, vstride, vrow0, ntok, ostride, orow0, seg0, seg1;
-  bool routed, valid;
-};
-
+// Down projection / row-dot: out = gate * (M v) for the dense sources and the
+// union members' D rows.  A block stages in LDS the input rows of the members
+// its tiles visit (one or two per sweep of the grid) and of the dense sources
+// it meets, as far as they fit; the rest are read from global memory.
 template <typename WT>
-__device__ __forceinline__ DownSeg down_seg(const GroupedArgs& a, int t, int nr, int tr,
-                                            const int (&dstart)[4]) {
-  DownSeg g;
-  const size_t esz = sizeof(WT);
-  if (t < nr) {
-    const int j = uni(t / tr);
-    int off = 0, ntok = 0;
-    const char* blk = member_block(a.r, j, off, ntok);
-    g.valid = blk != nullptr;
-    g.routed = true;
-    g.seg0 = j * tr;
-    g.seg1 = g.seg0 + tr;
-    g.M = blk + 2 * (size_t)a.r.inter * a.H * esz;
-    g.rows = a.H;
-    g.len = a.r.inter;
-    g.vin = a.r.a;
-    g.vstride = a.r.inter;
-    g.vrow0 = off;
-    g.ntok = ntok;
-    g.gates = a.r.gate_list + off;
-    g.gscalar = 0.f;
-    g.out = a.r.p;
-    g.ostride = a.H;
-    g.orow0 = off;
-  } else {
-    int s = 0;
-    while (s + 1 < a.n_dense && t >= dstart[s + 1]) ++s;
-    const DenseSrc d = pick_dense(a, s);
-    g.valid = true;
-    g.routed = false;
-    g.seg0 = dstart[s];
-    g.seg1 = dstart[s + 1];
-    g.M = static_cast<const char*>(d.w);
-    g.rows = d.rows;
-    g.len = d.inter;
-    g.vin = d.vin;
-    g.vstride = d.vin_stride;
-    g.vrow0 = 0;
-    g.ntok = a.T;
-    g.gates = nullptr;
-    g.gscalar = d.gate;
-    g.out = d.out;
-    g.ostride = d.out_stride;
-    g.orow0 = 0;
-  }
-  return g;
-}
-
-// Persistent down-projection / row-dot kernel (NS rows per wave tile).
-template <typename WT, bool LDSX, int NS>
 __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) void down_kernel(
     GroupedArgs a) {
   constexpr int EPU = WTr<WT>::EPU;
   const int lane = threadIdx.x & 63, wave = uni((int)(threadIdx.x >> 6));
   const int nu = routed_count(a);
-  const int tr = uni(a.has_routed ? cdiv(a.H, NS) : 0);
-  const int nr = nu * tr;
-  int dstart[4];
-  int total = nr;
-  for (int s = 0; s < a.n_dense; ++s) {
-    dstart[s] = total;
-    total += uni(cdiv(a.dense[s].rows, NS));
-  }
-  dstart[a.n_dense] = total;
-#if DE_DN_STRIDED
-  // Grid-strided tile order.  Inputs: a single dense source (the row-dot)
-  // stages all T input rows in LDS at the start when LDSX; otherwise they are
-  // read from global memory (they are small and stay in cache).
-  int sstride = 0;
-  if constexpr (LDSX) {
-    const DenseSrc d0 = a.dense[0];
-    stage_rows<EPU>(d0.vin, d0.vin_stride, a.T, d0.inter);
-    __syncthreads();
-    sstride = staged_stride<EPU>(d0.inter);
-  }
-  int cur = -1;
-  DownSeg g;
-  for (int tile = blockIdx.x * kWavesPB + wave; tile < total; tile += gridDim.x * kWavesPB) {
-    if (tile >= cur) {  // tiles only increase: a new segment starts at or after seg1
-      g = down_seg<WT>(a, tile, nr, tr, dstart);
-      cur = g.seg1;
-    }
-    if (!g.valid) continue;
-    const int r0 = (tile - g.seg0) * NS;
-    if (LDSX && !g.routed)
-      down_tile<WT, NS, kDenseNT, LDSX>(g.M, g.rows, g.len, r0, lane, nullptr, sstride, 0, g.ntok,
-                                        nullptr, g.gscalar, g.out, g.ostride, 0);
-    else if (g.routed)
-      down_tile<WT, NS, kRoutedNT, false>(g.M, g.rows, g.len, r0, lane, g.vin, g.vstride, g.vrow0,
-                                          g.ntok, g.gates, 0.f, g.out, g.ostride, g.orow0);
-    else
-      down_tile<WT, NS, kDenseNT, false>(g.M, g.rows, g.len, r0, lane, g.vin, g.vstride, 0, g.ntok,
-                                         nullptr, g.gscalar, g.out, g.ostride, 0);
-  }
-#else
-  // Contiguous order: block b owns the tile range whose cost is 1/grid of the
-  // total and walks it segment by segment; with LDSX each segment's input
-  // rows are staged in LDS (as many as fit at once, all of them normally).
-  Segments sg;
-  sg.n = 0;
-  sg.tiles[sg.n] = nr;
-  sg.cost[sg.n++] = (long long)(a.has_routed ? a.r.inter : 0) * sizeof(WT) * NS + 1;
-  for (int s = 0; s < a.n_dense; ++s) {
-    sg.tiles[sg.n] = dstart[s + 1] - dstart[s];
-    sg.cost[sg.n++] =
-        (long long)a.dense[s].inter * sizeof(WT) * NS * ((a.T + kDenseNT - 1) / kDenseNT);
-  }
-  int lo, hi;
-  block_range(sg, lo, hi);
-  int t = lo;
-  while (t < hi) {
-    const DownSeg g = down_seg<WT>(a, t, nr, tr, dstart);
-    const int t1 = min(hi, g.seg1);
-    if (g.valid) {
-      if constexpr (LDSX) {
-        const int sst = staged_stride<EPU>(g.len);
-        const int cap = uni(max(1, a.lds_floats / sst));
-        for (int c0 = 0; c0 < g.ntok; c0 += cap) {
-          const int nc = min(cap, g.ntok - c0);
-          __syncthreads();  // the previous rows are no longer read
-          stage_rows<EPU>(g.vin + (size_t)(g.vrow0 + c0) * g.vstride, g.vstride, nc, g.len);
-          __syncthreads();
-          for (int tile = t + wave; tile < t1; tile += kWavesPB) {
-            const int r0 = (tile - g.seg0) * NS;
-            if (g.routed)
-              down_tile<WT, NS, kRoutedNT, true>(g.M, g.rows, g.len, r0, lane, nullptr, sst, 0, nc,
-                                                 g.gates + c0, 0.f, g.out, g.ostride,
-                                                 g.orow0 + c0);
-            else
-              down_tile<WT, NS, kDenseNT, true>(g.M, g.rows, g.len, r0, lane, nullptr, sst, 0, nc,
-                                                nullptr, g.gscalar, g.out, g.ostride, c0);
-          }
-        }
-      } else {
-        for (int tile = t + wave; tile < t1; tile += kWavesPB) {
-          const int r0 = (tile - g.seg0) * NS;
-          if (g.routed)
-            down_tile<WT, NS, kRoutedNT, false>(g.M, g.rows, g.len, r0, lane, g.vin, g.vstride,
-                                                g.vrow0, g.ntok, g.gates, 0.f, g.out, g.ostride,
-                                                g.orow0);
-          else
-            down_tile<WT, NS, kDenseNT, false>(g.M, g.rows, g.len, r0, lane, g.vin, g.vstride, 0,
-                                               g.ntok, nullptr, g.gscalar, g.out, g.ostride, 0);
+  const Tables tb = tables_at(a, a.lds_floats);
+  fill_dense(a, tb);
+  if (a.has_routed) fill_tables(a, tb, nu);
+  __syncthreads();
+  Layout ly = make_layout(a, nu, false);
+  __shared__ int s_dact[3];
+  __shared__ int s_list[kMaxStaged + 1];
+  __shared__ int s_nlist;
+  if (threadIdx.x == 0) {
+    const int step = (int)gridDim.x * kWavesPB;
+    int used = 0, n = 0;
+    // Dense sources whose tiles this block visits.
+    for (int s = 0; s < 3; ++s) s_dact[s] = -1;
+    for (int t = blockIdx.x * kWavesPB; t < ly.ndt; t += step) {
+      for (int w = 0; w < kWavesPB && t + w < ly.ndt; w += kWavesPB - 1) {
+        int start = 0, unused = 0;
+        const int s = ly.source(t + w, start, unused);
+        const int len = s == 0 ? a.dense[0].inter : (s == 1 ? a.dense[1].inter : a.dense[2].inter);
+        const int need = a.T * staged_stride<EPU>(len);
+        if (s_dact[s] < 0 && used + need <= a.lds_floats) {
+          s_dact[s] = used;
+          used += need;
         }
       }
     }
-    t = t1;
+    // Members whose tiles this block visits, in visiting order.
+    int last = -1;
+    for (int t = blockIdx.x * kWavesPB + (ly.ndt > 0 ? cdiv(ly.ndt - (int)blockIdx.x * kWavesPB, step) * step : 0);
+         t < ly.total; t += step) {
+      const int t0 = max(t, ly.ndt), t1 = min(t + kWavesPB - 1, ly.total - 1);
+      if (t0 > t1) continue;
+      for (int j = (t0 - ly.ndt) / ly.tr; j <= (t1 - ly.ndt) / ly.tr; ++j) {
+        if (j == last || n >= kMaxStaged) continue;
+        last = j;
+        Member& m = tb.mem[j];
+        const int need = m.ntok * staged_stride<EPU>(a.r.inter);
+        if (m.blk != nullptr && m.ntok > 0 && used + need <= a.lds_floats) {
+          m.act = used;
+          used += need;
+          s_list[n++] = j;
+        }
+      }
+    }
+    s_nlist = n;
   }
-#endif
+  __syncthreads();
+  for (int i = 0; i < s_nlist; ++i) {
+    const Member m = tb.mem[s_list[i]];
+    stage_rows_at<EPU>(s_dyn + m.act, a.r.a + (size_t)m.off * a.r.inter, a.r.inter, m.ntok,
+                       a.r.inter);
+  }
+  // Static indices only: a run-time index into the kernel argument would make
+  // the compiler copy the whole argument to scratch memory.
+  if (a.n_dense > 0 && s_dact[0] >= 0)
+    stage_rows_at<EPU>(s_dyn + s_dact[0], a.dense[0].vin, a.dense[0].vin_stride, a.T,
+                       a.dense[0].inter);
+  if (a.n_dense > 1 && s_dact[1] >= 0)
+    stage_rows_at<EPU>(s_dyn + s_dact[1], a.dense[1].vin, a.dense[1].vin_stride, a.T,
+                       a.dense[1].inter);
+  if (a.n_dense > 2 && s_dact[2] >= 0)
+    stage_rows_at<EPU>(s_dyn + s_dact[2], a.dense[2].vin, a.dense[2].vin_stride, a.T,
+                       a.dense[2].inter);
+  __syncthreads();
+  ly.act0 = uni(s_dact[0]);
+  ly.act1 = uni(s_dact[1]);
+  ly.act2 = uni(s_dact[2]);
+  run_tiles<WT, false>(a, ly, tb, 0, false, lane, wave);
 }
 
 // ------------------------------------------------------------------ combine
@@ -775,9 +806,9 @@ int occupancy_blocks(K kernel, size_t lds) {
 }
 
 // Grid: enough blocks to fill the device at the kernel's occupancy, never more
-// than max_blocks (a block has work for up to 8 tiles at a time).
+// than one wave per tile.
 template <typename K>
-hipError_t launch_persistent(K kernel, int max_blocks, size_t lds, const GroupedArgs& a,
+hipError_t launch_persistent(K kernel, int max_tiles, size_t lds, const GroupedArgs& a,
                              hipStream_t s) {
   static bool attr_set = false;
   if (!attr_set) {
@@ -787,21 +818,16 @@ hipError_t launch_persistent(K kernel, int max_blocks, size_t lds, const Grouped
   }
   const int occ = occupancy_blocks(kernel, lds);
   const int cap = dev_info().num_cus * occ;
-  int g = max_blocks < cap ? max_blocks : cap;
-  if (g < 1) g = 1;
+  const int want = cdiv(max_tiles, kWavesPB);
+  const int g = want < 1 ? 1 : (want < cap ? want : cap);
   hipLaunchKernelGGL(kernel, dim3(g), dim3(kBlock), lds, s, a);
   return hipGetLastError();
 }
 
-int gateup_max_tiles(const GroupedArgs& a) {
-  int t = a.has_routed ? a.r.max_union * ((a.r.inter + kGuRows - 1) / kGuRows) : 0;
-  for (int s = 0; s < a.n_dense; ++s) t += (a.dense[s].inter + kGuRows - 1) / kGuRows;
-  return t;
-}
-
-int down_max_tiles(const GroupedArgs& a, int rows_per_tile) {
-  int t = a.has_routed ? a.r.max_union * ((a.H + rows_per_tile - 1) / rows_per_tile) : 0;
-  for (int s = 0; s < a.n_dense; ++s) t += (a.dense[s].rows + rows_per_tile - 1) / rows_per_tile;
+int max_tiles(const GroupedArgs& a, bool gateup) {
+  const int per = gateup ? kGuPairs : kNS;
+  int t = a.has_routed ? a.r.max_union * cdiv(gateup ? a.r.inter : a.H, per) : 0;
+  for (int s = 0; s < a.n_dense; ++s) t += cdiv(gateup ? a.dense[s].inter : a.dense[s].rows, per);
   return t;
 }
 
@@ -813,62 +839,27 @@ size_t staged_bytes(int rows, int len) {
 // The whole block of positions is staged in LDS when it fits the budget.
 template <typename WT>
 hipError_t gateup_typed(const GroupedArgs& a, hipStream_t s) {
-  const int tiles = gateup_max_tiles(a);
+  const int tiles = max_tiles(a, true);
   if (tiles == 0) return hipSuccess;
+  const size_t tabs = tables_bytes(a);
   const size_t lds = staged_bytes<WT>(a.T, a.H);
-  if (lds <= (size_t)kLdsBudget)
-    return launch_persistent(gateup_kernel<WT, true>, (tiles + kWavesPB - 1) / kWavesPB, lds, a, s);
-  return launch_persistent(gateup_kernel<WT, false>, (tiles + kWavesPB - 1) / kWavesPB, 0, a, s);
+  if (lds + tabs <= (size_t)kLdsBudget)
+    return launch_persistent(gateup_kernel<WT, true>, tiles, lds + tabs, a, s);
+  return launch_persistent(gateup_kernel<WT, false>, tiles, tabs, a, s);
 }
 
-#if DE_DN_STRIDED
-// Strided order: a single dense source (the row-dot) stages all T input rows
-// once when they fit; the grouped down reads its inputs directly.
-template <typename WT, int NS>
-hipError_t down_launch(GroupedArgs a, hipStream_t s) {
-  const int tiles = (down_max_tiles(a, NS) + kWavesPB - 1) / kWavesPB;
-  if (tiles == 0) return hipSuccess;
-  if (!a.has_routed && a.n_dense == 1) {
-    const size_t lds = staged_bytes<WT>(a.T, a.dense[0].inter);
-    if (lds <= (size_t)kLdsBudget) {
-      a.lds_floats = (int)(lds / sizeof(float));
-      return launch_persistent(down_kernel<WT, true, NS>, tiles, lds, a, s);
-    }
-  }
-  a.lds_floats = 0;
-  return launch_persistent(down_kernel<WT, false, NS>, tiles, 0, a, s);
-}
-#else
-// Inputs are staged in LDS when at least min(T, 4) rows of the longest input
-// fit the per-block budget (two blocks per CU); otherwise (rows as long as a
-// 10944-wide dense layer) they are read from global memory.
-template <typename WT, int NS>
-hipError_t down_launch(GroupedArgs a, hipStream_t s) {
-  constexpr int EPU = WTr<WT>::EPU;
-  const int tiles = (down_max_tiles(a, NS) + kWavesPB - 1) / kWavesPB;
-  if (tiles == 0) return hipSuccess;
-  int maxlen = a.has_routed ? a.r.inter : 0;
-  for (int i = 0; i < a.n_dense; ++i) maxlen = maxlen > a.dense[i].inter ? maxlen : a.dense[i].inter;
-  const int want = a.T < 4 ? a.T : 4;
-  const size_t row_bytes = (size_t)staged_stride<EPU>(maxlen) * sizeof(float);
-  if ((size_t)want * row_bytes <= (size_t)kDownLds) {
-    size_t lds = (size_t)kDownLds;
-    const size_t all = (size_t)a.T * row_bytes;
-    if (all < lds) lds = all;
-    a.lds_floats = (int)(lds / sizeof(float));
-    return launch_persistent(down_kernel<WT, true, NS>, tiles, lds, a, s);
-  }
-  a.lds_floats = 0;
-  return launch_persistent(down_kernel<WT, false, NS>, tiles, 0, a, s);
-}
-#endif
-
+// The down kernel stages the inputs of the sources a block visits: a fixed
+// budget per block (two blocks per CU), which holds a row-dot's T input rows
+// and the few members' rows of the grouped down in the common case.
 template <typename WT>
-hipError_t down_typed(const GroupedArgs& a, hipStream_t s) {
-  // One dense source and no routed part is a plain row-dot (the LM head, the
-  // down projection of a dense layer).
-  if (!a.has_routed && a.n_dense == 1) return down_launch<WT, kRdRows>(a, s);
-  return down_launch<WT, kDnRows>(a, s);
+hipError_t down_typed(GroupedArgs a, hipStream_t s) {
+  const int tiles = max_tiles(a, false);
+  if (tiles == 0) return hipSuccess;
+  const size_t tabs = tables_bytes(a);
+  const size_t budget = (size_t)kDownLds > tabs + 4096 ? (size_t)kDownLds - tabs : 4096;
+  a.lds_floats = (int)(budget / sizeof(float)) & ~3;
+  return launch_persistent(down_kernel<WT>, tiles, (size_t)a.lds_floats * sizeof(float) + tabs, a,
+                           s);
 }
 
 }  // namespace

@@ -1,17 +1,21 @@
 // Router scoring (Eq. 1), top-k with gates (Eq. 4) and the block union with
-// per-expert token lists (Eq. 2, Eq. 3), in one launch.
+// per-expert token lists (Eq. 2, Eq. 3).
 //
-// route_kernel: ceil(N/16) blocks of 16 waves, one wave per expert.  A block
-//   stages the block's activations in LDS, each wave streams its expert's
-//   fp32 router row once (all of its float4 loads issued together) and dots
-//   it with every position.  The last block to finish (device-scope counter,
-//   release/acquire fences so logits written on other XCDs are visible) then
-//   selects the top-k of every position, one wave per position, by repeated
-//   wave-wide (key, id) argmax with ties to the lower id, and builds the union
-//   with integer work only: a 64-bit position mask per expert, a wave prefix
-//   scan over the experts for the list offsets, rank = popcount of the mask
-//   below the position.  No floating-point arithmetic touches the union, so
-//   it is bit-exact and deterministic.
+// scores_kernel: a 2-D grid of (4 experts) x (up to 8 positions) blocks.  A
+//   block issues its experts' router-row loads, stages its positions'
+//   activations in LDS with all loads in flight at once, and each wave dots
+//   one expert's row with every staged position.  Logits go to z [T, N].
+// select_kernel: one block.  Each wave takes one position: lane l holds the
+//   candidates l, l+64, ...; a candidate's rank is the number of candidates
+//   with a larger key (ties to the lower id), counted against every key
+//   broadcast with readlane, so no chain of cross-lane shuffles is needed.
+//   Rank < k places the candidate in the ordered top-k list.  The gates are
+//   then normalised in list order and the union is built with integer work
+//   only: a 64-bit position mask per expert, a wave prefix scan over the
+//   experts for the list offsets, rank of a position = popcount of the mask
+//   below it.  No floating-point arithmetic touches the union, so it is
+//   bit-exact and deterministic.  The kernel boundary between the two
+//   launches orders the logits before the selection.
 // union_kernel: the same union build from caller-supplied top-k lists.
 #include "de_common.h"
 
@@ -20,26 +24,21 @@
 namespace de {
 namespace {
 
-constexpr int kRouteThreads = 1024;
-constexpr int kRouteWaves = kRouteThreads / kWave;  // experts per block
-constexpr int kRouteLds = 136 * 1024;  // + ~20 KB of static selection state <= 160 KB
-constexpr int kRouterTok = 16;                      // positions per accumulator pass
+constexpr int kSelThreads = 1024;                 // select / union: one wave per position
+constexpr int kScoreWaves = 4;                    // experts per scores block
+constexpr int kScoreThreads = kScoreWaves * kWave;
+constexpr int kScoreTok = 8;                      // positions per scores block (max)
+constexpr int kScoreLds = 64 * 1024;              // staged activations per scores block
+constexpr int kStageBatch = 16;                   // float4 loads in flight per thread
 constexpr int kMaxT = 64;
 constexpr int kMaxK = 32;
 constexpr int kMaxN = 256;
 
 extern __shared__ __align__(16) float s_x[];
 
-// (key, id) candidate ordering: larger key first, equal keys to the lower id.
-// id == INT_MAX marks "no candidate".
-__device__ __forceinline__ bool better(float ka, int ea, float kb, int eb) {
-  if (ea == INT_MAX) return false;
-  if (eb == INT_MAX) return true;
-  return ka > kb || (ka == kb && ea < eb);
-}
-
 struct SelShared {
   int32_t idx[kMaxT * kMaxK];
+  float sc[kMaxT * kMaxK];    // score of each list entry
   float gate[kMaxT * kMaxK];
   unsigned long long mask[kMaxN];
   int32_t off[kMaxN];
@@ -48,20 +47,20 @@ struct SelShared {
 };
 
 // Top-k of every position from the logits z [T, N] (one wave per position),
-// into s.idx / s.gate and the optional global outputs.
+// into s.idx / s.gate and the optional global outputs.  All threads.
 __device__ void select_topk(const TopkUnionArgs& a, SelShared& s) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int nwaves = blockDim.x >> 6;
   const int T = a.T, N = a.N, k = a.k;
   for (int t = wave; t < T; t += nwaves) {
     float key[4], sc[4];
-    bool taken[4];
+    bool valid[4];
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const int e = lane + q * kWave;
-      const bool valid = e < N;
-      const float zz = valid ? a.z[(size_t)t * N + e] : 0.f;
-      const float b = (valid && a.bias != nullptr) ? a.bias[e] : 0.f;
+      valid[q] = e < N;
+      const float zz = valid[q] ? a.z[(size_t)t * N + e] : 0.f;
+      const float b = (valid[q] && a.bias != nullptr) ? a.bias[e] : 0.f;
       float kk, sv;
       if (a.score_func == 0) {  // softmax(z + b): key z + b
         kk = zz + b;
@@ -71,69 +70,63 @@ __device__ void select_topk(const TopkUnionArgs& a, SelShared& s) {
         kk = sv + b;
       }
       if (!(kk == kk)) kk = -INFINITY;  // a NaN never wins
-      key[q] = valid ? kk : -INFINITY;
+      key[q] = valid[q] ? kk : -INFINITY;
       sc[q] = sv;
-      taken[q] = !valid;
     }
     if (a.score_func == 0) {
       float m = -INFINITY;
 #pragma unroll
       for (int q = 0; q < 4; ++q)
-        if (!taken[q]) m = fmaxf(m, key[q]);
+        if (valid[q]) m = fmaxf(m, key[q]);
       m = wave_max(m);
       float ex[4], sum = 0.f;
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        ex[q] = taken[q] ? 0.f : expf(key[q] - m);
+        ex[q] = valid[q] ? expf(key[q] - m) : 0.f;
         sum += ex[q];
       }
       sum = wave_sum(sum);
 #pragma unroll
       for (int q = 0; q < 4; ++q) sc[q] = ex[q] / sum;
     }
-    int my_e = 0;
-    float my_s = 0.f, gsum = 0.f;
-    for (int j = 0; j < k; ++j) {
-      float bk = -INFINITY, bs = 0.f;
-      int be = INT_MAX;
+    // rank[q] = number of candidates that beat candidate (key[q], id).
+    int rank[4] = {0, 0, 0, 0};
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int e = lane + q * kWave;
-        if (!taken[q] && better(key[q], e, bk, be)) {
-          bk = key[q];
-          be = e;
-          bs = sc[q];
+    for (int q2 = 0; q2 < 4; ++q2) {
+      if (q2 * kWave >= N) break;
+      const int n2 = min(kWave, N - q2 * kWave);
+      for (int l = 0; l < n2; ++l) {
+        const float kb = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(key[q2]), l));
+        const int eb = q2 * kWave + l;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int e = lane + q * kWave;
+          rank[q] += (kb > key[q] || (kb == key[q] && eb < e)) ? 1 : 0;
         }
       }
-#pragma unroll
-      for (int o = 32; o > 0; o >>= 1) {
-        const float ok = __shfl_xor(bk, o, kWave);
-        const int oe = __shfl_xor(be, o, kWave);
-        const float os = __shfl_xor(bs, o, kWave);
-        if (better(ok, oe, bk, be)) {
-          bk = ok;
-          be = oe;
-          bs = os;
-        }
-      }
-#pragma unroll
-      for (int q = 0; q < 4; ++q)
-        if (lane + q * kWave == be) taken[q] = true;
-      if (lane == j) {
-        my_e = be;
-        my_s = bs;
-      }
-      gsum += bs;
     }
-    if (lane < k) {
-      float g = my_s;
-      if (a.norm_topk) g = g / gsum;
-      g *= a.routed_scale;
-      s.idx[t * k + lane] = my_e;
-      s.gate[t * k + lane] = g;
-      if (a.idx_out) a.idx_out[(size_t)t * k + lane] = my_e;
-      if (a.gate_out) a.gate_out[(size_t)t * k + lane] = g;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      if (valid[q] && rank[q] < k) {
+        s.idx[t * k + rank[q]] = lane + q * kWave;
+        s.sc[t * k + rank[q]] = sc[q];
+      }
     }
+  }
+  __syncthreads();
+  // Gates in list order: g_j = score_j (/ sum of the k scores) * routed_scale.
+  for (int i = threadIdx.x; i < T * k; i += blockDim.x) {
+    const int t = i / k;
+    float g = s.sc[i];
+    if (a.norm_topk) {
+      float gsum = 0.f;
+      for (int j = 0; j < k; ++j) gsum += s.sc[t * k + j];
+      g = g / gsum;
+    }
+    g *= a.routed_scale;
+    s.gate[i] = g;
+    if (a.idx_out) a.idx_out[i] = s.idx[i];
+    if (a.gate_out) a.gate_out[i] = g;
   }
 }
 
@@ -229,91 +222,86 @@ __device__ void build_union(const TopkUnionArgs& a, SelShared& s) {
   }
 }
 
+// z[t0 + m, e] = W_r[e] . x[t0 + m] for the block's experts (one per wave) and
+// positions.  With XLDS the positions are staged in LDS (all loads of a batch
+// in flight before any store); otherwise they are read from global memory.
 template <bool XLDS>
-__global__ __launch_bounds__(kRouteThreads) void route_kernel(RouteArgs r) {
-  __shared__ SelShared sel;
-  __shared__ int s_last;
-  const TopkUnionArgs& a = r.sel;
+__global__ __launch_bounds__(kScoreThreads) void scores_kernel(RouteArgs r) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int T = a.T, H = r.H, N = a.N, H4 = H >> 2;
+  const int T = r.sel.T, H = r.H, N = r.sel.N, H4 = H >> 2;
+  const int t0 = blockIdx.y * r.tok_per_block;
+  const int nt = min(r.tok_per_block, T - t0);
+  const float4* xg = reinterpret_cast<const float4*>(r.x) + (size_t)t0 * H4;
   if constexpr (XLDS) {
-    for (int i = threadIdx.x; i < T * H4; i += kRouteThreads)
-      reinterpret_cast<float4*>(s_x)[i] = reinterpret_cast<const float4*>(r.x)[i];
+    float4* sx = reinterpret_cast<float4*>(s_x);
+    const int n4 = nt * H4;
+    for (int i0 = 0; i0 < n4; i0 += kScoreThreads * kStageBatch) {
+      float4 v[kStageBatch];
+#pragma unroll
+      for (int j = 0; j < kStageBatch; ++j)  // clamped: every load is in bounds, none is skipped
+        v[j] = xg[min(i0 + j * kScoreThreads + (int)threadIdx.x, n4 - 1)];
+#pragma unroll
+      for (int j = 0; j < kStageBatch; ++j) {
+        const int i = i0 + j * kScoreThreads + threadIdx.x;
+        if (i < n4) sx[i] = v[j];
+      }
+    }
     __syncthreads();
   }
-  const int e = blockIdx.x * kRouteWaves + wave;
-  if (e < N) {
-    const float4* wr = reinterpret_cast<const float4*>(r.w + (size_t)e * H);
-    for (int h0 = 0; h0 < H4; h0 += kWave * 8) {
-      float4 wv[8];
+  const int e = blockIdx.x * kScoreWaves + wave;
+  if (e >= N) return;
+  const float4* wr = reinterpret_cast<const float4*>(r.w + (size_t)e * H);
+  float acc[kScoreTok];
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const int h = h0 + lane + i * kWave;
-        wv[i] = h < H4 ? wr[h] : make_float4(0.f, 0.f, 0.f, 0.f);
-      }
-      for (int t0 = 0; t0 < T; t0 += kRouterTok) {
-        float acc[kRouterTok];
+  for (int m = 0; m < kScoreTok; ++m) acc[m] = 0.f;
+  for (int h0 = 0; h0 < H4; h0 += kWave * 8) {
+    float4 wv[8];
 #pragma unroll
-        for (int m = 0; m < kRouterTok; ++m) acc[m] = 0.f;
+    for (int i = 0; i < 8; ++i) {
+      const int h = h0 + lane + i * kWave;
+      wv[i] = h < H4 ? wr[h] : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+#pragma unroll
+    for (int m = 0; m < kScoreTok; ++m) {
+      if (m < nt) {
+        float v = acc[m];
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
           const int h = h0 + lane + i * kWave;
           if (h < H4) {
-#pragma unroll
-            for (int m = 0; m < kRouterTok; ++m) {
-              if (t0 + m < T) {
-                const float4 xv = XLDS ? reinterpret_cast<const float4*>(s_x)[(t0 + m) * H4 + h]
-                                       : reinterpret_cast<const float4*>(r.x)[(size_t)(t0 + m) * H4 + h];
-                float v = acc[m];
-                v = fmaf(wv[i].x, xv.x, v);
-                v = fmaf(wv[i].y, xv.y, v);
-                v = fmaf(wv[i].z, xv.z, v);
-                v = fmaf(wv[i].w, xv.w, v);
-                acc[m] = v;
-              }
-            }
+            const float4 xv = XLDS ? reinterpret_cast<const float4*>(s_x)[m * H4 + h]
+                                   : xg[(size_t)m * H4 + h];
+            v = fmaf(wv[i].x, xv.x, v);
+            v = fmaf(wv[i].y, xv.y, v);
+            v = fmaf(wv[i].z, xv.z, v);
+            v = fmaf(wv[i].w, xv.w, v);
           }
         }
-#pragma unroll
-        for (int m = 0; m < kRouterTok; ++m) {
-          if (t0 + m < T) {
-            const float sm = wave_sum(acc[m]);
-            // Partial sums over h0 chunks accumulate in z (H > 2048 only).
-            if (lane == 0) {
-              float* zp = r.z + (size_t)(t0 + m) * N + e;
-              *zp = h0 == 0 ? sm : *zp + sm;
-            }
-          }
-        }
+        acc[m] = v;
       }
     }
   }
-  // ---- the last block to finish selects and builds the union.  The barrier
-  // orders the block's logit stores before thread 0's device-scope release;
-  // one fence per block (each is an L2 write-back on this part).
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    __threadfence();
-    const unsigned prev = __hip_atomic_fetch_add(r.counter, 1u, __ATOMIC_ACQ_REL,
-                                                 __HIP_MEMORY_SCOPE_AGENT);
-    s_last = prev == gridDim.x - 1;
-    if (s_last) {
-      __threadfence();
-      __hip_atomic_store(r.counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+#pragma unroll
+  for (int m = 0; m < kScoreTok; ++m) {
+    if (m < nt) {
+      const float sm = wave_sum(acc[m]);
+      if (lane == 0) r.z[(size_t)(t0 + m) * N + e] = sm;
     }
   }
-  __syncthreads();
-  if (!s_last) return;
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");  // every wave reads other blocks' logits
+}
+
+// Top-k of every position, then (when asked) the union.  One block.
+__global__ __launch_bounds__(kSelThreads) void select_kernel(TopkUnionArgs a) {
+  __shared__ SelShared sel;
   select_topk(a, sel);
   if (a.n_union == nullptr) return;
   __syncthreads();
   build_union(a, sel);
 }
 
-__global__ __launch_bounds__(kRouteThreads) void union_kernel(TopkUnionArgs a) {
+__global__ __launch_bounds__(kSelThreads) void union_kernel(TopkUnionArgs a) {
   __shared__ SelShared sel;
-  for (int i = threadIdx.x; i < a.T * a.k; i += kRouteThreads) {
+  for (int i = threadIdx.x; i < a.T * a.k; i += kSelThreads) {
     sel.idx[i] = a.idx_in[i];
     sel.gate[i] = a.gate_in[i];
   }
@@ -323,25 +311,30 @@ __global__ __launch_bounds__(kRouteThreads) void union_kernel(TopkUnionArgs a) {
 
 }  // namespace
 
-hipError_t launch_route(const RouteArgs& r, hipStream_t s) {
-  const int grid = (r.sel.N + kRouteWaves - 1) / kRouteWaves;
-  const size_t lds = (size_t)r.sel.T * r.H * sizeof(float);
-  if (lds <= (size_t)kRouteLds) {
-    static bool attr = false;
-    if (!attr) {
-      hipFuncSetAttribute(reinterpret_cast<const void*>(route_kernel<true>),
-                          hipFuncAttributeMaxDynamicSharedMemorySize, kRouteLds);
-      attr = true;
-    }
-    hipLaunchKernelGGL(route_kernel<true>, dim3(grid), dim3(kRouteThreads), lds, s, r);
+hipError_t launch_route(const RouteArgs& r0, hipStream_t s) {
+  RouteArgs r = r0;
+  const int T = r.sel.T;
+  // Positions per scores block: at most kScoreTok, fewer when a row is long,
+  // spread evenly over the position chunks.
+  const int fit = (int)(kScoreLds / ((size_t)r.H * sizeof(float)));
+  const int cap = fit < 1 ? kScoreTok : (fit < kScoreTok ? fit : kScoreTok);
+  const int chunks = (T + cap - 1) / cap;
+  r.tok_per_block = (T + chunks - 1) / chunks;
+  const dim3 grid((r.sel.N + kScoreWaves - 1) / kScoreWaves, chunks);
+  if (fit >= 1) {
+    const size_t lds = (size_t)r.tok_per_block * r.H * sizeof(float);
+    hipLaunchKernelGGL(scores_kernel<true>, grid, dim3(kScoreThreads), lds, s, r);
   } else {
-    hipLaunchKernelGGL(route_kernel<false>, dim3(grid), dim3(kRouteThreads), 0, s, r);
+    hipLaunchKernelGGL(scores_kernel<false>, grid, dim3(kScoreThreads), 0, s, r);
   }
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(select_kernel, dim3(1), dim3(kSelThreads), 0, s, r.sel);
   return hipGetLastError();
 }
 
 hipError_t launch_union(const TopkUnionArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL(union_kernel, dim3(1), dim3(kRouteThreads), 0, s, a);
+  hipLaunchKernelGGL(union_kernel, dim3(1), dim3(kSelThreads), 0, s, a);
   return hipGetLastError();
 }
 
