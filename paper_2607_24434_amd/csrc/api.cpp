@@ -115,6 +115,8 @@ int check_epi(const de_epilogue* epi) {
 
 int hip_status(hipError_t e) { return e == hipSuccess ? DE_OK : DE_ERR_HIP; }
 
+// Router logits (into the workspace) and the ordered top-k lists of every
+// position; the layer calls build the union in their gate/up kernel.
 hipError_t route(const de_moe_desc& d, int T, const float* x, const float* w_router,
                  const Layout& L, void* ws, const de::TopkUnionArgs& sel, hipStream_t s) {
   de::RouteArgs r{};
@@ -124,6 +126,7 @@ hipError_t route(const de_moe_desc& d, int T, const float* x, const float* w_rou
   r.H = d.hidden;
   r.z = reinterpret_cast<float*>(static_cast<char*>(ws) + L.z);
   r.sel.z = r.z;
+  r.counter = reinterpret_cast<unsigned*>(static_cast<char*>(ws) + L.ctl);
   return de::launch_route(r, s);
 }
 
@@ -174,9 +177,13 @@ de::RoutedSrc routed_src(const de_moe_desc& d, int T, const de_expert_table* tab
 int run_grouped(const de_moe_desc& d, int T, const float* x, const de::RoutedSrc& r,
                 const int32_t* pair_pos, int kk, const void* shared_w, const void* draft_w,
                 float gamma, float* y, const de_epilogue* epi, const Layout& L, void* ws,
-                hipStream_t s) {
+                const de::TopkUnionArgs* fused_sel, hipStream_t s) {
   const size_t esz = elem_bytes(d.wdtype);
   de::GroupedArgs g{};
+  if (fused_sel != nullptr) {
+    g.fuse_route = 1;
+    g.sel = *fused_sel;
+  }
   g.T = T;
   g.H = d.hidden;
   g.x = x;
@@ -241,6 +248,7 @@ int run_grouped(const de_moe_desc& d, int T, const float* x, const de::RoutedSrc
     c.dense_p[c.n_dense++] = ds.out;
   }
   g.n_dense = nd;
+  g.fuse_route = 0;
   e = timed_phase(DE_PHASE_DOWN, s, [&] { return de::launch_down(g, d.wdtype, s); });
   if (e != hipSuccess) return DE_ERR_HIP;
   c.p_r = r.p;
@@ -368,7 +376,7 @@ int de_grouped_swiglu(const de_moe_desc* d, int T, const float* x, const de_expe
   const de::RoutedSrc r = routed_src(*d, T, routed, n_union, union_ids, offsets, tok_list, gate_list,
                                      at<float>(ws, L.a_r), at<float>(ws, L.p_r));
   return run_grouped(*d, T, x, r, pair_pos, d->top_k, shared_w, nullptr, 0.f, y, epi, L, ws,
-                     stream);
+                     nullptr, stream);
 }
 
 int de_draft_layer(const de_moe_desc* d, int T, const float* x, const float* w_router,
@@ -405,10 +413,12 @@ int de_draft_layer(const de_moe_desc* d, int T, const float* x, const float* w_r
   a.tok_list = at<int32_t>(ws, L.tok);
   a.gate_list = at<float>(ws, L.glist);
   a.pair_pos = at<int32_t>(ws, L.ppos);
+  a.z = at<float>(ws, L.z);
   if (route(*d, T, x, w_router, L, ws, a, stream) != hipSuccess) return DE_ERR_HIP;
   const de::RoutedSrc r = routed_src(*d, T, routed, a.n_union, a.union_ids, a.offsets, a.tok_list,
                                      a.gate_list, at<float>(ws, L.a_r), at<float>(ws, L.p_r));
-  return run_grouped(*d, T, x, r, a.pair_pos, 1, shared_w, draft_w, gamma, y, epi, L, ws, stream);
+  return run_grouped(*d, T, x, r, a.pair_pos, 1, shared_w, draft_w, gamma, y, epi, L, ws, &a,
+                     stream);
 }
 
 int de_verify_layer(const de_moe_desc* d, int T, const float* x, const float* w_router,
@@ -444,10 +454,11 @@ int de_verify_layer(const de_moe_desc* d, int T, const float* x, const float* w_
   a.tok_list = tok_list ? tok_list : at<int32_t>(ws, L.tok);
   a.gate_list = gate_list ? gate_list : at<float>(ws, L.glist);
   a.pair_pos = pair_pos ? pair_pos : at<int32_t>(ws, L.ppos);
+  a.z = at<float>(ws, L.z);
   if (route(*d, T, x, w_router, L, ws, a, stream) != hipSuccess) return DE_ERR_HIP;
   const de::RoutedSrc r = routed_src(*d, T, routed, a.n_union, a.union_ids, a.offsets, a.tok_list,
                                      a.gate_list, at<float>(ws, L.a_r), at<float>(ws, L.p_r));
-  return run_grouped(*d, T, x, r, a.pair_pos, d->top_k, shared_w, nullptr, 0.f, y, epi, L, ws,
+  return run_grouped(*d, T, x, r, a.pair_pos, d->top_k, shared_w, nullptr, 0.f, y, epi, L, ws, &a,
                      stream);
 }
 

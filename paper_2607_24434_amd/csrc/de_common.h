@@ -26,15 +26,22 @@ __device__ __forceinline__ float row16_sum(float v) {
   return v;
 }
 
+// Sum / max over the 64 lanes: four DPP steps inside each 16-lane row, then two
+// cross-row shuffles; every lane receives the same bits.
 __device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
+  v = row16_sum(v);
+  v += __shfl_xor(v, 16, kWave);
+  v += __shfl_xor(v, 32, kWave);
   return v;
 }
 
 __device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, kWave));
+  v = fmaxf(v, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0xB1, 0xF, 0xF, false)));
+  v = fmaxf(v, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x4E, 0xF, 0xF, false)));
+  v = fmaxf(v, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x141, 0xF, 0xF, false)));
+  v = fmaxf(v, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x140, 0xF, 0xF, false)));
+  v = fmaxf(v, __shfl_xor(v, 16, kWave));
+  v = fmaxf(v, __shfl_xor(v, 32, kWave));
   return v;
 }
 
@@ -94,25 +101,6 @@ struct RoutedSrc {
   float* p;                    // P_r [pairs, H]
 };
 
-struct GroupedArgs {
-  int T;
-  int H;
-  const float* x;      // [T, H]
-  int has_routed;
-  RoutedSrc r;
-  int n_dense;
-  DenseSrc dense[3];
-  int lds_floats;      // set by the launcher: staged-input capacity of a block
-};
-
-// ---------------------------------------------------------------- launchers (HIP side)
-
-struct DevInfo {
-  int device;
-  int num_cus;
-};
-const DevInfo& dev_info();
-
 struct TopkUnionArgs {
   int T, N, k;
   const float* z;          // [T, N] logits; NULL: read idx_in/gate_in instead
@@ -131,14 +119,40 @@ struct TopkUnionArgs {
   float* gate_list;
   int32_t* pair_pos;       // [T, ucols]
 };
-// Router scoring, then top-k (+ union when sel.n_union is set): two launches.
+
+struct GroupedArgs {
+  int T;
+  int H;
+  const float* x;      // [T, H]
+  int has_routed;
+  RoutedSrc r;
+  int n_dense;
+  DenseSrc dense[3];
+  int lds_floats;      // set by the launcher: staged-input capacity of a block
+  // Gate/up only: recompute the top-k and the union from sel.z in every block
+  // (block 0 also writes sel's outputs); r.n_union ... r.gate_list are then
+  // not read.
+  int fuse_route;
+  TopkUnionArgs sel;
+};
+
+// ---------------------------------------------------------------- launchers (HIP side)
+
+struct DevInfo {
+  int device;
+  int num_cus;
+};
+const DevInfo& dev_info();
+
+
+// Router logits and top-k of every position (one block per position).
 struct RouteArgs {
-  TopkUnionArgs sel;       // sel.z is the logits scratch [T, N]
+  TopkUnionArgs sel;       // top-k options and the idx_out / gate_out lists
   const float* x;          // [T, H]
   const float* w;          // [N, H] fp32 router
   int H;
-  float* z;                // == sel.z
-  int tok_per_block;       // set by the launcher
+  float* z;                // [T, N] logits out, or NULL
+  unsigned* counter;       // [T] arrival counters, zero between calls (split launch)
 };
 hipError_t launch_route(const RouteArgs& r, hipStream_t s);
 // Union only, from caller-supplied lists (sel.idx_in / sel.gate_in).

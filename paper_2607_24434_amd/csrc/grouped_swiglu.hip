@@ -29,6 +29,7 @@
 //    steps inside 16 lanes and two cross-row shuffles, identical in every
 //    lane.  No float atomics: results are bitwise reproducible.
 #include "de_common.h"
+#include "topk_union.h"
 
 // Build-time tuning knobs (kept at the measured best by default).
 #ifndef DE_NT_LOADS
@@ -223,7 +224,29 @@ struct Tables {
 size_t tables_bytes(const GroupedArgs& a) {
   size_t b = 3 * sizeof(DenseSrc);
   if (a.has_routed) b += (size_t)a.r.max_union * sizeof(Member) + (size_t)a.r.pairs_max * 8;
+  if (a.fuse_route) b += sel_view_bytes(a.T, a.sel.k, a.sel.N);
   return b;
+}
+
+// The selection state after the tables (fused routing only).
+__device__ __forceinline__ SelView sel_at(const GroupedArgs& a, const Tables& tb) {
+  char* p = reinterpret_cast<char*>(tb.gate + (a.has_routed ? a.r.pairs_max : 0));
+  return sel_view_at(p, a.T, a.sel.k, a.sel.N);
+}
+
+// The member table from a union built in LDS: member j = the expert with
+// union index j.  All threads; the caller synchronises.
+__device__ __forceinline__ void members_from_union(const GroupedArgs& a, const Tables& tb,
+                                                   const SelView& v) {
+  const RoutedSrc& r = a.r;
+  for (int e = threadIdx.x; e < a.sel.N; e += kBlock) {
+    const unsigned long long m = v.mask[e];
+    if (m == 0ull) continue;
+    const int slot = e < r.max_union ? (r.slot_of_expert ? r.slot_of_expert[e] : e) : -1;
+    Member mb{nullptr, v.off[e], (int)__popcll(m), -1, 0};
+    if (slot >= 0 && slot < r.n_slots) mb.blk = r.base + (size_t)slot * r.stride;
+    tb.mem[v.upos[e]] = mb;
+  }
 }
 
 __device__ __forceinline__ Tables tables_at(const GroupedArgs& a, int act_floats) {
@@ -649,11 +672,27 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
   constexpr int EPU = WTr<WT>::EPU;
   const int lane = threadIdx.x & 63, wave = uni((int)(threadIdx.x >> 6));
   const int act_floats = LDSX ? a.T * staged_stride<EPU>(a.H) : 0;
-  const int nu = routed_count(a);
   const Tables tb = tables_at(a, act_floats);
   if constexpr (LDSX) stage_rows<EPU>(a.x, a.H, a.T, a.H);
   fill_dense(a, tb);
-  if (a.has_routed) fill_tables(a, tb, nu);
+  int nu;
+  if (a.fuse_route) {
+    // The union of the top-k lists, in every block; block 0 also publishes it
+    // for the down and combine launches.
+    const SelView v = sel_at(a, tb);
+    for (int i = threadIdx.x; i < a.T * a.sel.k; i += kBlock) {
+      v.idx[i] = a.sel.idx_out[i];
+      v.gate[i] = a.sel.gate_out[i];
+    }
+    __syncthreads();
+    build_union(a.sel, v, blockIdx.x == 0, tb.tok, tb.gate);
+    nu = uni(v.misc[1]);
+    nu = nu < 0 ? 0 : min(nu, a.r.max_union);
+    if (nu > 0) members_from_union(a, tb, v);
+  } else {
+    nu = routed_count(a);
+    if (a.has_routed) fill_tables(a, tb, nu);
+  }
   __syncthreads();
   const Layout ly = make_layout(a, nu, true);
   run_tiles<WT, true>(a, ly, tb, LDSX ? staged_stride<EPU>(a.H) : a.H, LDSX, lane, wave);
@@ -745,7 +784,9 @@ constexpr int kCombPer = 4;
 
 // y[t] = sum of the dense partials + sum_j P_r[pair_pos[t, j]] (+ residual),
 // in that fixed order; optionally also RMSNorm(y).  One block per position;
-// each thread's kCombPer elements are loaded independently.
+// each thread's kCombPer elements are loaded independently, and for a row of
+// at most kCombThreads * kCombPer elements they stay in registers for the
+// normalisation.
 __global__ __launch_bounds__(kCombThreads) void combine_kernel(CombineArgs a) {
   __shared__ float red[kCombThreads / 64];
   const int t = blockIdx.x;
@@ -757,8 +798,8 @@ __global__ __launch_bounds__(kCombThreads) void combine_kernel(CombineArgs a) {
     pp[j] = (p >= 0 && p < a.pairs_max) ? p : -1;
   }
   float ss = 0.f;
+  float v[kCombPer];
   for (int h0 = threadIdx.x; h0 < a.H; h0 += kCombThreads * kCombPer) {
-    float v[kCombPer];
 #pragma unroll
     for (int i = 0; i < kCombPer; ++i) {
       const int h = h0 + i * kCombThreads;
@@ -791,7 +832,16 @@ __global__ __launch_bounds__(kCombThreads) void combine_kernel(CombineArgs a) {
     float tot = 0.f;
     for (int w = 0; w < kCombThreads / 64; ++w) tot += red[w];
     const float r = 1.0f / sqrtf(tot / (float)a.H + a.eps);
-    for (int h = threadIdx.x; h < a.H; h += kCombThreads) a.normed[rowoff + h] = a.y[rowoff + h] * r;
+    if (a.H <= kCombThreads * kCombPer) {
+#pragma unroll
+      for (int i = 0; i < kCombPer; ++i) {
+        const int h = threadIdx.x + i * kCombThreads;
+        if (h < a.H) a.normed[rowoff + h] = v[i] * r;
+      }
+    } else {
+      for (int h = threadIdx.x; h < a.H; h += kCombThreads)
+        a.normed[rowoff + h] = a.y[rowoff + h] * r;
+    }
   }
 }
 

@@ -1,0 +1,259 @@
+// Top-k selection with gates (Eq. 1, Eq. 4) and the block union with
+// per-expert position lists (Eq. 2, Eq. 3), as block-level device functions
+// over LDS arrays.  Used by the standalone selection kernel and by the
+// prologue of the grouped gate/up kernel, which recomputes them in every block
+// from the router logits instead of waiting for a separate launch.
+//
+// Selection: one wave per position.  Lane l holds the candidates l, l+64, ...
+// (N <= 256); a candidate's rank is the number of candidates with a larger key
+// (ties to the lower id), counted against every key broadcast with readlane,
+// so no chain of cross-lane shuffles is needed.  Rank < k places it in the
+// ordered list.  Gates are normalised in list order.
+//
+// Union: integer work only.  Every (position, slot) entry sets its position
+// bit in the expert's 64-bit mask with an LDS atomic OR (a bit already set
+// means the id repeats within a position); a wave scan over the experts in
+// ascending id gives each member's list offset and union index; the rank of
+// a position in its expert's list is the popcount of the mask below it.
+#pragma once
+
+#include "de_common.h"
+
+namespace de {
+
+// LDS arrays of the selection and union (sizes: T*k, T*k, T*k, N, N, N, 4).
+struct SelView {
+  int32_t* idx;              // ordered top-k ids [T, k]
+  float* sc;                 // their scores
+  float* gate;               // their gates
+  unsigned long long* mask;  // position mask per expert [N]
+  int32_t* off;              // list offset per expert
+  int32_t* upos;             // union index per expert
+  int32_t* misc;             // [0] bad, [1] n_union, [2] pairs
+};
+
+__host__ __device__ inline size_t sel_view_bytes(int T, int k, int N) {
+  const size_t tk = (size_t)T * k;
+  return ((tk * 12 + 7) & ~(size_t)7) + (size_t)N * 16 + 16;
+}
+
+__device__ inline SelView sel_view_at(char* p, int T, int k, int N) {
+  SelView v;
+  const size_t tk = (size_t)T * k;
+  v.idx = reinterpret_cast<int32_t*>(p);
+  v.sc = reinterpret_cast<float*>(v.idx + tk);
+  v.gate = v.sc + tk;
+  p += (tk * 12 + 7) & ~(size_t)7;
+  v.mask = reinterpret_cast<unsigned long long*>(p);
+  v.off = reinterpret_cast<int32_t*>(v.mask + N);
+  v.upos = v.off + N;
+  v.misc = v.upos + N;
+  return v;
+}
+
+// Ordered top-k of position t from its N logits zrow (one wave; zrow may be
+// in LDS or global memory): ids into idx[0..k), scores into sc[0..k).
+__device__ inline void topk_row(const TopkUnionArgs& a, const float* zrow, int32_t* idx,
+                                float* sc_out) {
+  const int lane = threadIdx.x & 63;
+  const int N = a.N, k = a.k;
+  const int nq = (N + kWave - 1) / kWave;  // candidates per lane (<= 4)
+  float key[4], sc[4];
+  bool valid[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int e = lane + q * kWave;
+    valid[q] = q < nq && e < N;
+    const float zz = valid[q] ? zrow[e] : 0.f;
+    const float b = (valid[q] && a.bias != nullptr) ? a.bias[e] : 0.f;
+    float kk, sv;
+    if (a.score_func == 0) {  // softmax(z + b): key z + b
+      kk = zz + b;
+      sv = 0.f;
+    } else {                  // sigmoid(z): key sigmoid(z) + b
+      sv = 1.0f / (1.0f + expf(-zz));
+      kk = sv + b;
+    }
+    if (!(kk == kk)) kk = -INFINITY;  // a NaN never wins
+    key[q] = valid[q] ? kk : -INFINITY;
+    sc[q] = sv;
+  }
+  if (a.score_func == 0) {
+    float m = -INFINITY;
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      if (valid[q]) m = fmaxf(m, key[q]);
+    m = wave_max(m);
+    float ex[4], sum = 0.f;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      ex[q] = valid[q] ? expf(key[q] - m) : 0.f;
+      sum += ex[q];
+    }
+    sum = wave_sum(sum);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) sc[q] = ex[q] / sum;
+  }
+  // rank[q] = number of candidates that beat candidate (key[q], id).
+  int rank[4] = {0, 0, 0, 0};
+#pragma unroll
+  for (int q2 = 0; q2 < 4; ++q2) {
+    if (q2 >= nq) break;
+    const int n2 = min(kWave, N - q2 * kWave);
+    for (int l = 0; l < n2; ++l) {
+      const float kb = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(key[q2]), l));
+      const int eb = q2 * kWave + l;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        if (q >= nq) break;
+        const int e = lane + q * kWave;
+        rank[q] += (kb > key[q] || (kb == key[q] && eb < e)) ? 1 : 0;
+      }
+    }
+  }
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    if (valid[q] && rank[q] < k) {
+      idx[rank[q]] = lane + q * kWave;
+      sc_out[rank[q]] = sc[q];
+    }
+  }
+}
+
+// Gate of list entry j of a position from the list's scores: score_j
+// (/ sum of the k scores in list order) * routed_scale.
+__device__ inline float topk_gate(const TopkUnionArgs& a, const float* sc, int j) {
+  float g = sc[j];
+  if (a.norm_topk) {
+    float gsum = 0.f;
+    for (int i = 0; i < a.k; ++i) gsum += sc[i];
+    g = g / gsum;
+  }
+  return g * a.routed_scale;
+}
+
+// Top-k of every position from the logits a.z [T, N] into s.idx / s.gate;
+// with write_out also into a.idx_out / a.gate_out.  All threads of the block;
+// ends with a barrier.
+__device__ inline void select_topk(const TopkUnionArgs& a, const SelView& s, bool write_out) {
+  const int wave = threadIdx.x >> 6;
+  const int nwaves = blockDim.x >> 6;
+  const int T = a.T, N = a.N, k = a.k;
+  for (int t = wave; t < T; t += nwaves) topk_row(a, a.z + (size_t)t * N, s.idx + t * k, s.sc + t * k);
+  __syncthreads();
+  for (int i = threadIdx.x; i < T * k; i += blockDim.x) {
+    const int t = i / k;
+    const float g = topk_gate(a, s.sc + t * k, i - t * k);
+    s.gate[i] = g;
+    if (write_out && a.idx_out) a.idx_out[i] = s.idx[i];
+    if (write_out && a.gate_out) a.gate_out[i] = g;
+  }
+  __syncthreads();
+}
+
+// Union of the first a.ucols entries of every position's list in s.idx /
+// s.gate.  s.misc[1] receives n_union (-1 for an id outside [0, N) or an id
+// that repeats within a position) and s.misc[2] the number of pairs.  With
+// write_out the lists go to a.n_union / union_ids / offsets / tok_list /
+// gate_list / pair_pos; with ptok / pgate the per-pair positions and gates
+// also go to LDS.  All threads of the block; ends with a barrier.
+__device__ inline void build_union(const TopkUnionArgs& a, const SelView& s, bool write_out,
+                                   int32_t* ptok, float* pgate) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int nthreads = blockDim.x;
+  const int T = a.T, N = a.N, k = a.k, uc = a.ucols;
+  for (int e = tid; e < N; e += nthreads) s.mask[e] = 0ull;
+  if (tid == 0) s.misc[0] = 0;
+  __syncthreads();
+  for (int i = tid; i < T * uc; i += nthreads) {
+    const int t = i / uc, j = i - t * uc;
+    const int e = s.idx[t * k + j];
+    if (e < 0 || e >= N) {
+      s.misc[0] = 1;
+    } else {
+      const unsigned long long bit = 1ull << t;
+      const unsigned long long old = atomicOr(&s.mask[e], bit);
+      if (old & bit) s.misc[0] = 1;
+    }
+  }
+  __syncthreads();
+  if (s.misc[0]) {
+    if (tid == 0) {
+      s.misc[1] = -1;
+      s.misc[2] = 0;
+      if (write_out) *a.n_union = -1;
+    }
+    __syncthreads();
+    return;
+  }
+  // Exclusive scans over the experts in ascending id (wave 0, four per lane).
+  if (wave == 0) {
+    int cnt[4], flg[4], csum = 0, fsum = 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int e = lane * 4 + q;
+      const unsigned long long m = e < N ? s.mask[e] : 0ull;
+      cnt[q] = __popcll(m);
+      flg[q] = m != 0ull;
+      csum += cnt[q];
+      fsum += flg[q];
+    }
+    int ci = csum, fi = fsum;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+      const int cu = __shfl_up(ci, o, kWave);
+      const int fu = __shfl_up(fi, o, kWave);
+      if (lane >= o) {
+        ci += cu;
+        fi += fu;
+      }
+    }
+    int cbase = ci - csum, fbase = fi - fsum;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int e = lane * 4 + q;
+      if (e < N) {
+        s.off[e] = cbase;
+        s.upos[e] = fbase;
+      }
+      cbase += cnt[q];
+      fbase += flg[q];
+    }
+    if (lane == kWave - 1) {
+      s.misc[1] = fi;
+      s.misc[2] = ci;
+    }
+  }
+  __syncthreads();
+  const int nu = s.misc[1], total = s.misc[2];
+  if (write_out) {
+    for (int e = tid; e < N; e += nthreads) {
+      if (s.mask[e] != 0ull) {
+        a.union_ids[s.upos[e]] = e;
+        a.offsets[s.upos[e]] = s.off[e];
+      }
+    }
+    for (int u = nu + tid; u < N; u += nthreads) a.union_ids[u] = -1;
+    for (int u = nu + tid; u <= N; u += nthreads) a.offsets[u] = total;
+    if (tid == 0) *a.n_union = nu;
+  }
+  for (int i = tid; i < T * uc; i += nthreads) {
+    const int t = i / uc, j = i - t * uc;
+    const int e = s.idx[t * k + j];
+    const unsigned long long below = t == 0 ? 0ull : (s.mask[e] & (~0ull >> (64 - t)));
+    const int p = s.off[e] + __popcll(below);
+    const float g = s.gate[t * k + j];
+    if (write_out) {
+      a.tok_list[p] = t;
+      a.gate_list[p] = g;
+      a.pair_pos[i] = p;
+    }
+    if (ptok != nullptr) {
+      ptok[p] = t;
+      pgate[p] = g;
+    }
+  }
+  __syncthreads();
+}
+
+}  // namespace de
