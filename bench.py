@@ -35,6 +35,34 @@ import time
 METRIC = "verify-layer µs + achieved HBM GB/s over union expert weights (K=8, V2-Lite shape)"
 PEAK_HBM_GBS = 8000.0
 
+# HBM bytes per launch of the verify-layer gate/up kernel, from two rocprofv3
+# --pmc runs of this benchmark (FETCH_SIZE, then WRITE_SIZE; summary and scale
+# factors in profiles/verify_layer_v2lite_T9.md).  Valid only for the kernel
+# sources they were measured on: reported as null once those change.
+PMC_TRAFFIC = {
+    "bytes_per_launch": 463.25e6,
+    "vs_algorithmic": 1.003,
+    "union_mean": 38.0,
+    "sources": ["paper_2607_24434_amd/csrc/grouped_swiglu.hip",
+                "paper_2607_24434_amd/csrc/topk_union.h",
+                "paper_2607_24434_amd/csrc/de_common.h"],
+    "sha256": "e440ed9d9c1737cd49a4f59aa316b0e94c5df05a10334e47ad4390397c52b418",
+}
+
+
+def pmc_traffic():
+    """The measured per-launch traffic when the kernel sources are unchanged, else None."""
+    import hashlib
+    root = os.path.dirname(os.path.abspath(__file__))
+    h = hashlib.sha256()
+    try:
+        for f in PMC_TRAFFIC["sources"]:
+            with open(os.path.join(root, f), "rb") as fh:
+                h.update(fh.read())
+    except OSError:
+        return None
+    return PMC_TRAFFIC["bytes_per_launch"] if h.hexdigest() == PMC_TRAFFIC["sha256"] else None
+
 
 def parse():
     p = argparse.ArgumentParser()
@@ -245,7 +273,8 @@ def main():
             "peak": PEAK_HBM_GBS,
             "unit": "GB/s",
             "frac": round(gu_gbs / PEAK_HBM_GBS, 4),
-            "traffic": None,
+            "traffic": pmc_traffic(),
+            "traffic_vs_algorithmic": PMC_TRAFFIC["vs_algorithmic"] if pmc_traffic() else None,
             "algorithmic_bytes_per_launch": int(round(float(gu_bytes.mean()))),
         },
         "cpu_baseline": cpu,
