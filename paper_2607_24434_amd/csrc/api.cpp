@@ -249,8 +249,6 @@ int run_grouped(const de_moe_desc& d, int T, const float* x, const de::RoutedSrc
   }
   g.n_dense = nd;
   g.fuse_route = 0;
-  e = timed_phase(DE_PHASE_DOWN, s, [&] { return de::launch_down(g, d.wdtype, s); });
-  if (e != hipSuccess) return DE_ERR_HIP;
   c.p_r = r.p;
   c.pair_pos = pair_pos;
   c.kk = kk;
@@ -259,6 +257,8 @@ int run_grouped(const de_moe_desc& d, int T, const float* x, const de::RoutedSrc
   c.residual = epi ? epi->residual : nullptr;
   c.normed = epi ? epi->normed : nullptr;
   c.eps = epi ? epi->eps : 0.f;
+  e = timed_phase(DE_PHASE_DOWN, s, [&] { return de::launch_down(g, d.wdtype, s); });
+  if (e != hipSuccess) return DE_ERR_HIP;
   return hip_status(de::launch_combine(c, s));
 }
 

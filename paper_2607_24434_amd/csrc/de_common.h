@@ -120,6 +120,20 @@ struct TopkUnionArgs {
   int32_t* pair_pos;       // [T, ucols]
 };
 
+struct CombineArgs {
+  int T, H;
+  int n_dense;
+  const float* dense_p[3];     // [T, H] partials with their gates applied
+  const float* p_r;            // [pairs, H] routed partials or NULL
+  const int32_t* pair_pos;     // [T, kk]
+  int kk;
+  int pairs_max;               // rows of p_r
+  const float* residual;       // [T, H] or NULL
+  float* y;                    // [T, H]
+  float* normed;               // [T, H] or NULL
+  float eps;
+};
+
 struct GroupedArgs {
   int T;
   int H;
@@ -161,19 +175,7 @@ hipError_t launch_union(const TopkUnionArgs& a, hipStream_t s);
 hipError_t launch_gateup(const GroupedArgs& a, int wdtype, hipStream_t s);
 hipError_t launch_down(const GroupedArgs& a, int wdtype, hipStream_t s);
 
-struct CombineArgs {
-  int T, H;
-  int n_dense;
-  const float* dense_p[3];     // [T, H] partials with their gates applied
-  const float* p_r;            // [pairs, H] routed partials or NULL
-  const int32_t* pair_pos;     // [T, kk]
-  int kk;
-  int pairs_max;               // rows of p_r
-  const float* residual;       // [T, H] or NULL
-  float* y;                    // [T, H]
-  float* normed;               // [T, H] or NULL
-  float eps;
-};
+
 hipError_t launch_combine(const CombineArgs& a, hipStream_t s);
 
 struct AcceptArgs {

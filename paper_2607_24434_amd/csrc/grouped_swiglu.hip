@@ -577,15 +577,19 @@ __device__ __forceinline__ void finish(const Pass<NT>& p, const Tables& tb, int 
           const float g = row_total(acc[2 * q][m]);
           const float u = row_total(acc[2 * q + 1][m]);
           if (lane == m && p.r0 + q < p.rows)
-            p.out[(size_t)(p.orow0 + m) * p.ostride + p.r0 + q] = silu_f(g) * u;
+            *(DE_GLOBAL float*)(p.out + (size_t)(p.orow0 + m) * p.ostride + p.r0 + q) =
+                silu_f(g) * u;
         }
       } else {
         const float gm = p.goff >= 0 ? tb.gate[p.goff + m] : p.gscalar;
 #pragma unroll
         for (int k = 0; k < kNS; ++k) {
           const float v = row_total(acc[k][m]);
-          if (lane == m && p.r0 + k < p.rows)
-            p.out[(size_t)(p.orow0 + m) * p.ostride + p.r0 + k] = gm * v;
+          if (lane == m && p.r0 + k < p.rows) {
+            // A global (not flat) store: a flat store also counts against the
+            // LDS wait counter and would hold up the activation reads behind it.
+            *(DE_GLOBAL float*)(p.out + (size_t)(p.orow0 + m) * p.ostride + p.r0 + k) = gm * v;
+          }
         }
       }
     }
@@ -663,6 +667,7 @@ __device__ __forceinline__ void run_tiles(const GroupedArgs& a, const Layout ly,
 }
 
 // ------------------------------------------------------------------ kernels
+
 
 // Gate/up: A = silu(G x) * (U x) for the dense sources and the union members'
 // pairs.  LDSX: the block of positions is staged in LDS.
@@ -783,13 +788,12 @@ constexpr int kCombThreads = 1024;
 constexpr int kCombPer = 4;
 
 // y[t] = sum of the dense partials + sum_j P_r[pair_pos[t, j]] (+ residual),
-// in that fixed order; optionally also RMSNorm(y).  One block per position;
-// each thread's kCombPer elements are loaded independently, and for a row of
-// at most kCombThreads * kCombPer elements they stay in registers for the
+// in that fixed order; optionally also RMSNorm(y).  One block of NTH threads
+// per position; each thread's kCombPer elements are loaded independently and,
+// for a row of at most NTH * kCombPer elements, stay in registers for the
 // normalisation.
-__global__ __launch_bounds__(kCombThreads) void combine_kernel(CombineArgs a) {
-  __shared__ float red[kCombThreads / 64];
-  const int t = blockIdx.x;
+template <int NTH>
+__device__ __forceinline__ void combine_row(const CombineArgs& a, int t, float* red) {
   const size_t rowoff = (size_t)t * a.H;
   int pp[8];
   const int kk = a.p_r ? min(a.kk, 8) : 0;
@@ -799,26 +803,42 @@ __global__ __launch_bounds__(kCombThreads) void combine_kernel(CombineArgs a) {
   }
   float ss = 0.f;
   float v[kCombPer];
-  for (int h0 = threadIdx.x; h0 < a.H; h0 += kCombThreads * kCombPer) {
+  for (int h0 = threadIdx.x; h0 < a.H; h0 += NTH * kCombPer) {
+    // All of an element's partials are loaded before any is added (fixed
+    // maxima, predicated), so the loads overlap; the sum keeps the fixed order.
+    float dv[kCombPer][3], rv[kCombPer][8], res[kCombPer];
 #pragma unroll
     for (int i = 0; i < kCombPer; ++i) {
-      const int h = h0 + i * kCombThreads;
+      const int h = min(h0 + i * NTH, a.H - 1);
+#pragma unroll
+      for (int s = 0; s < 3; ++s) dv[i][s] = s < a.n_dense ? a.dense_p[s][rowoff + h] : 0.f;
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        rv[i][j] = (j < kk && pp[j] >= 0) ? a.p_r[(size_t)pp[j] * a.H + h] : 0.f;
+      res[i] = a.residual ? a.residual[rowoff + h] : 0.f;
+    }
+#pragma unroll
+    for (int i = 0; i < kCombPer; ++i) {
+      const int h = h0 + i * NTH;
       float x = 0.f;
       if (h < a.H) {
-        for (int s = 0; s < a.n_dense; ++s) x += a.dense_p[s][rowoff + h];
-        for (int j = 0; j < kk; ++j)
-          if (pp[j] >= 0) x += a.p_r[(size_t)pp[j] * a.H + h];
+#pragma unroll
+        for (int s = 0; s < 3; ++s)
+          if (s < a.n_dense) x += dv[i][s];
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+          if (j < kk && pp[j] >= 0) x += rv[i][j];
         for (int j = kk; j < (a.p_r ? a.kk : 0); ++j) {
           const int p = a.pair_pos[(size_t)t * a.kk + j];
           if (p >= 0 && p < a.pairs_max) x += a.p_r[(size_t)p * a.H + h];
         }
-        if (a.residual) x = a.residual[rowoff + h] + x;
+        if (a.residual) x = res[i] + x;
       }
       v[i] = x;
     }
 #pragma unroll
     for (int i = 0; i < kCombPer; ++i) {
-      const int h = h0 + i * kCombThreads;
+      const int h = h0 + i * NTH;
       if (h < a.H) {
         a.y[rowoff + h] = v[i];
         ss = fmaf(v[i], v[i], ss);
@@ -830,19 +850,24 @@ __global__ __launch_bounds__(kCombThreads) void combine_kernel(CombineArgs a) {
     if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
     __syncthreads();
     float tot = 0.f;
-    for (int w = 0; w < kCombThreads / 64; ++w) tot += red[w];
+    for (int w = 0; w < NTH / 64; ++w) tot += red[w];
     const float r = 1.0f / sqrtf(tot / (float)a.H + a.eps);
-    if (a.H <= kCombThreads * kCombPer) {
+    if (a.H <= NTH * kCombPer) {
 #pragma unroll
       for (int i = 0; i < kCombPer; ++i) {
-        const int h = threadIdx.x + i * kCombThreads;
+        const int h = threadIdx.x + i * NTH;
         if (h < a.H) a.normed[rowoff + h] = v[i] * r;
       }
     } else {
-      for (int h = threadIdx.x; h < a.H; h += kCombThreads)
-        a.normed[rowoff + h] = a.y[rowoff + h] * r;
+      for (int h = threadIdx.x; h < a.H; h += NTH) a.normed[rowoff + h] = a.y[rowoff + h] * r;
     }
+    __syncthreads();  // red is reused by the next row
   }
+}
+
+__global__ __launch_bounds__(kCombThreads) void combine_kernel(CombineArgs a) {
+  __shared__ float red[kCombThreads / 64];
+  combine_row<kCombThreads>(a, blockIdx.x, red);
 }
 
 // ------------------------------------------------------------------ launch
