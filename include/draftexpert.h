@@ -202,6 +202,82 @@ size_t de_dense_workspace_bytes(int T, int H, int I);
 int de_dense_swiglu(int T, int H, int I, int wdtype, const float* x, const void* w, float* y,
                     const de_epilogue* epi, void* ws, size_t ws_bytes, hipStream_t stream);
 
+/* ---- The stacked model and one draft-then-verify step (Algorithm 1) ---- */
+
+/* Weights of one MoE layer of the stack. */
+typedef struct de_layer_weights {
+  const float* w_router;  /* fp32 [N, H] */
+  const float* bias;      /* fp32 [N] or NULL */
+  de_expert_table routed; /* routed experts (resident, or the slots of a cache) */
+  const void* shared_w;   /* shared-path block; NULL when moe.shared_inter is 0 */
+  const void* draft_w;    /* draft-expert block or NULL (drops the gamma term) */
+  float gamma;            /* scale of the draft-expert term of Eq. (5) */
+} de_layer_weights;
+
+/* A pre-norm residual stack without attention (attention and its KV cache
+ * stay resident and are outside this path):
+ *   h = Emb[token];  h += Dense(RMSNorm(h))          (layer 0, if dense_inter > 0)
+ *   h += MoE_l(RMSNorm(h)),  l = 1..n_layers          (Eq. 4 target / Eq. 5 draft)
+ *   logits = W_lm RMSNorm(h).
+ * All RMSNorms have unit gain and epsilon eps.  Without attention a block
+ * position depends only on its own token. */
+typedef struct de_model {
+  de_moe_desc moe;                /* shape of every MoE layer */
+  int32_t n_layers;               /* MoE layers (0..4096) */
+  int32_t vocab;                  /* V */
+  int32_t dense_inter;            /* I of the dense layer 0 (0: no dense layer) */
+  int32_t dense_wdtype;           /* DE_F32 or DE_BF16 */
+  float eps;                      /* RMSNorm epsilon (>= 0) */
+  const void* emb;                /* bf16 [V, H] */
+  const void* dense_w;            /* dense block [G|U|D]; NULL when dense_inter is 0 */
+  const void* lm_head;            /* bf16 [V, H] */
+  const de_layer_weights* layers; /* HOST array [n_layers]; read during the call only */
+} de_model;
+
+/* Forward modes: the MoE layers as the target (Eq. 4) or the drafter (Eq. 5). */
+#define DE_TARGET 0
+#define DE_DRAFT 1
+
+/* Scratch bytes of the model calls for blocks of up to T positions (0 on an
+ * invalid model).  A fresh allocation is zero-filled once with
+ * de_workspace_init; every model call leaves its control words zero again.
+ * Calls that share one workspace must not run concurrently. */
+size_t de_model_workspace_bytes(const de_model* m, int T);
+
+/* Host-only validation of a model (DE_OK or an error code).  Checks the MoE
+ * shape, every layer's pointers and table, and the glue's sizes. */
+int de_check_model(const de_model* m);
+
+/* Logits of T independent positions (each a token id, device int32 [T]):
+ * logits [T, V] fp32; argmax [T] (may be NULL) the row argmax, ties to the
+ * lowest id; n_union [n_layers] (may be NULL; DE_TARGET only) the union size
+ * of every MoE layer over the T positions (Eq. 3). */
+int de_model_forward(const de_model* m, int T, const int32_t* tokens, int mode, float* logits,
+                     int32_t* argmax, int32_t* n_union, void* ws, size_t ws_bytes,
+                     hipStream_t stream);
+
+/* One exact draft-then-verify step with K drafts (Algorithm 1, fixed K):
+ *   block [K+1] int32: block[0] = the last committed token (input);
+ *     block[i+1] = argmax of the drafter's logits at block[i], i = 0..K-1
+ *     (output: the drafts);
+ *   the target then scores the K+1 positions of block in one pass:
+ *   target_argmax [K+1] its row argmax; out [2] = (n, bonus) as
+ *   de_accept_len, so the step emits block[1..n] followed by the bonus token;
+ *   n_union [n_layers] (may be NULL) the verify union size per MoE layer;
+ *   pred_idx [K, n_layers, k] (may be NULL) the drafter's router top-k at
+ *   draft position i in layer l: the experts predicted for verify position i.
+ * Every launch is enqueued on `stream`; nothing synchronises the host.
+ * Scratch: de_model_workspace_bytes(m, K + 1). */
+int de_spec_step(const de_model* m, int K, int32_t* block, int32_t* target_argmax, int32_t* out,
+                 int32_t* n_union, int32_t* pred_idx, void* ws, size_t ws_bytes,
+                 hipStream_t stream);
+
+/* Plain greedy decoding with the target, one position per pass:
+ * tokens [n_steps + 1], tokens[0] the input, tokens[i+1] = argmax of the
+ * target logits at tokens[i].  Scratch: de_model_workspace_bytes(m, 1). */
+int de_greedy_decode(const de_model* m, int n_steps, int32_t* tokens, void* ws, size_t ws_bytes,
+                     hipStream_t stream);
+
 /* Pure streaming read of `bytes` (multiple of 16) from buf: the measured HBM
  * read ceiling.  sink [1] receives a value that depends on every byte. */
 int de_stream_probe(const void* buf, size_t bytes, float* sink, hipStream_t stream);

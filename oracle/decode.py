@@ -55,6 +55,7 @@ class Trace:
     gate: list = field(default_factory=list)
     moe_out: list = field(default_factory=list)
     final_h: np.ndarray | None = None
+    logits: np.ndarray | None = None
 
 
 def forward(model: ModelWeights, tokens, mode: str = "target", trace: Trace | None = None):
@@ -80,25 +81,34 @@ def forward(model: ModelWeights, tokens, mode: str = "target", trace: Trace | No
             trace.moe_out.append(y)
         h = h + y
     hn = moe.rmsnorm(h, model.eps)
+    logits = hn @ model.lm_head.T
     if trace is not None:
         trace.final_h = hn
-    return hn @ model.lm_head.T
+        trace.logits = logits
+    return logits
 
 
-def spec_step(model: ModelWeights, last_token: int, k_draft: int):
+def spec_step(model: ModelWeights, last_token: int, k_draft: int, traces: list | None = None):
     """One exact draft-then-verify step (Algorithm 1 with a fixed draft length K).
 
     Drafts d_1..d_K with the fixed-footprint drafter, verifies the block
     [c, d_1..d_K] with the target in one pass and accepts the target-consistent
     prefix.  Returns (drafts, n, bonus, target_argmax); the emitted tokens are
-    drafts[:n] followed by the bonus token.
+    drafts[:n] followed by the bonus token.  With ``traces`` (a list), the
+    Trace of each of the K draft passes and then of the verify pass is appended.
     """
+    def traced():
+        if traces is None:
+            return None
+        traces.append(Trace())
+        return traces[-1]
+
     drafts = []
     cur = int(last_token)
     for _ in range(k_draft):
-        cur = int(moe.argmax_first(forward(model, [cur], "draft"))[0])
+        cur = int(moe.argmax_first(forward(model, [cur], "draft", traced()))[0])
         drafts.append(cur)
-    logits = forward(model, [int(last_token)] + drafts, "target")
+    logits = forward(model, [int(last_token)] + drafts, "target", traced())
     n, bonus, t = moe.accept_len(logits, drafts)
     return drafts, n, bonus, t
 

@@ -30,9 +30,13 @@ C_FUNCS = [
     "de_expert_union", "de_grouped_swiglu", "de_draft_layer", "de_verify_layer", "de_accept_workspace_bytes", "de_accept_len",
     "de_lm_head", "de_rmsnorm", "de_embed_gather", "de_dense_workspace_bytes", "de_dense_swiglu",
     "de_stream_probe", "de_time_next_phase",
+    "de_check_model", "de_model_workspace_bytes", "de_model_forward", "de_spec_step",
+    "de_greedy_decode",
 ]
 DE_PHASE_GATEUP = 0
 DE_PHASE_DOWN = 1
+DE_TARGET = 0
+DE_DRAFT = 1
 
 
 class DEError(RuntimeError):
@@ -62,6 +66,22 @@ class Epilogue(ctypes.Structure):
     _fields_ = [("residual", ctypes.c_void_p), ("normed", ctypes.c_void_p), ("eps", ctypes.c_float)]
 
 
+class LayerWeights(ctypes.Structure):
+    _fields_ = [
+        ("w_router", ctypes.c_void_p), ("bias", ctypes.c_void_p), ("routed", ExpertTable),
+        ("shared_w", ctypes.c_void_p), ("draft_w", ctypes.c_void_p), ("gamma", ctypes.c_float),
+    ]
+
+
+class Model(ctypes.Structure):
+    _fields_ = [
+        ("moe", MoEDesc), ("n_layers", ctypes.c_int32), ("vocab", ctypes.c_int32),
+        ("dense_inter", ctypes.c_int32), ("dense_wdtype", ctypes.c_int32), ("eps", ctypes.c_float),
+        ("emb", ctypes.c_void_p), ("dense_w", ctypes.c_void_p), ("lm_head", ctypes.c_void_p),
+        ("layers", ctypes.POINTER(LayerWeights)),
+    ]
+
+
 def _load(path: str = LIB_PATH):
     if not os.path.exists(path):
         raise ImportError(f"{path} is missing: build it with `python paper_2607_24434_amd/build.py`")
@@ -73,6 +93,7 @@ def _load(path: str = LIB_PATH):
     DP = ctypes.POINTER(MoEDesc)
     TP = ctypes.POINTER(ExpertTable)
     EP = ctypes.POINTER(Epilogue)
+    MP = ctypes.POINTER(Model)
     sig = {
         "de_abi_version": (I, []),
         "de_error_string": (ctypes.c_char_p, [I]),
@@ -93,6 +114,11 @@ def _load(path: str = LIB_PATH):
         "de_dense_swiglu": (I, [I, I, I, I, P, P, P, EP, P, SZ, P]),
         "de_stream_probe": (I, [P, SZ, P, P]),
         "de_time_next_phase": (I, [I, P, P]),
+        "de_check_model": (I, [MP]),
+        "de_model_workspace_bytes": (SZ, [MP, I]),
+        "de_model_forward": (I, [MP, I, P, I, P, P, P, P, SZ, P]),
+        "de_spec_step": (I, [MP, I, P, P, P, P, P, P, SZ, P]),
+        "de_greedy_decode": (I, [MP, I, P, P, SZ, P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -263,3 +289,57 @@ def de_time_next_phase(phase, start_event, stop_event):
     _check("de_time_next_phase", LIB.de_time_next_phase(
         int(phase), None if start_event is None else start_event.cuda_event,
         None if stop_event is None else stop_event.cuda_event))
+
+
+def make_model(desc, layers, vocab, emb, lm_head, dense_w=None, dense_inter=0,
+               dense_wdtype=DE_BF16, eps=1e-6):
+    """A ``Model`` struct; ``layers`` is a list of dicts with the keys w_router,
+    bias, table (an ExpertTable), shared_w, draft_w, gamma.  The returned
+    struct keeps the layer array alive."""
+    arr = (LayerWeights * max(1, len(layers)))()
+    for i, l in enumerate(layers):
+        arr[i] = LayerWeights(_ptr(l["w_router"]), _ptr(l.get("bias")), l["table"],
+                              _ptr(l.get("shared_w")), _ptr(l.get("draft_w")),
+                              float(l.get("gamma", 1.0)))
+    m = Model(desc, len(layers), int(vocab), int(dense_inter), int(dense_wdtype), float(eps),
+              _ptr(emb), _ptr(dense_w), _ptr(lm_head), arr)
+    m._layers = arr
+    return m
+
+
+def de_check_model(model) -> int:
+    return LIB.de_check_model(ctypes.byref(model))
+
+
+def de_model_workspace_bytes(model, T) -> int:
+    return LIB.de_model_workspace_bytes(ctypes.byref(model), int(T))
+
+
+def model_workspace(model, T, device="cuda"):
+    """A zero-initialised scratch tensor for the model calls with up to T positions."""
+    n = de_model_workspace_bytes(model, T)
+    if n == 0:
+        _check("de_model_workspace_bytes", de_check_model(model) or -1)
+    ws = torch.empty(n, dtype=torch.uint8, device=device)
+    de_workspace_init(ws)
+    return ws
+
+
+def de_model_forward(model, T, tokens, mode, logits, argmax=None, n_union=None, ws=None,
+                     stream=None):
+    _check("de_model_forward", LIB.de_model_forward(
+        ctypes.byref(model), int(T), _ptr(tokens), int(mode), _ptr(logits), _ptr(argmax),
+        _ptr(n_union), _ptr(ws), ws.numel() if ws is not None else 0, _stream(stream)))
+
+
+def de_spec_step(model, K, block, target_argmax, out, n_union=None, pred_idx=None, ws=None,
+                 stream=None):
+    _check("de_spec_step", LIB.de_spec_step(
+        ctypes.byref(model), int(K), _ptr(block), _ptr(target_argmax), _ptr(out), _ptr(n_union),
+        _ptr(pred_idx), _ptr(ws), ws.numel() if ws is not None else 0, _stream(stream)))
+
+
+def de_greedy_decode(model, n_steps, tokens, ws=None, stream=None):
+    _check("de_greedy_decode", LIB.de_greedy_decode(
+        ctypes.byref(model), int(n_steps), _ptr(tokens), _ptr(ws),
+        ws.numel() if ws is not None else 0, _stream(stream)))

@@ -25,6 +25,18 @@ const DevInfo& dev_info() {
   return info[dev];
 }
 
+// Host checks of an expert table against a layer shape (also used by the
+// model calls before they enqueue anything).
+int check_table(const de_moe_desc& d, const de_expert_table* t) {
+  if (t == nullptr || t->base == nullptr || (reinterpret_cast<uintptr_t>(t->base) & 15u) != 0)
+    return DE_ERR_INVALID;
+  const int64_t need = 3ll * d.inter * d.hidden * (d.wdtype == DE_BF16 ? 2 : 4);
+  if (t->slot_stride_bytes < need || (t->slot_stride_bytes & 15) != 0) return DE_ERR_INVALID;
+  if (t->n_slots < 1) return DE_ERR_INVALID;
+  if (t->slot_of_expert == nullptr && t->n_slots < d.n_experts) return DE_ERR_INVALID;
+  return DE_OK;
+}
+
 }  // namespace de
 
 namespace {
@@ -95,15 +107,6 @@ int check_T(int T) { return (T >= 1 && T <= kMaxT) ? DE_OK : DE_ERR_INVALID; }
 int check_ws(const de_moe_desc& d, int T, const void* ws, size_t ws_bytes) {
   if (ws == nullptr || (reinterpret_cast<uintptr_t>(ws) & 255u) != 0) return DE_ERR_WORKSPACE;
   if (ws_bytes < layout(d, T).total) return DE_ERR_WORKSPACE;
-  return DE_OK;
-}
-
-int check_table(const de_moe_desc& d, const de_expert_table* t) {
-  if (t == nullptr || t->base == nullptr || !aligned16(t->base)) return DE_ERR_INVALID;
-  const int64_t need = 3ll * d.inter * d.hidden * elem_bytes(d.wdtype);
-  if (t->slot_stride_bytes < need || (t->slot_stride_bytes & 15) != 0) return DE_ERR_INVALID;
-  if (t->n_slots < 1) return DE_ERR_INVALID;
-  if (t->slot_of_expert == nullptr && t->n_slots < d.n_experts) return DE_ERR_INVALID;
   return DE_OK;
 }
 
@@ -369,7 +372,7 @@ int de_grouped_swiglu(const de_moe_desc* d, int T, const float* x, const de_expe
     return DE_ERR_INVALID;
   if (!aligned16(x)) return DE_ERR_INVALID;
   if (d->shared_inter > 0 && (shared_w == nullptr || !aligned16(shared_w))) return DE_ERR_INVALID;
-  if ((rc = check_table(*d, routed)) != DE_OK) return rc;
+  if ((rc = de::check_table(*d, routed)) != DE_OK) return rc;
   if ((rc = check_epi(epi)) != DE_OK) return rc;
   if ((rc = check_ws(*d, T, ws, ws_bytes)) != DE_OK) return rc;
   const Layout L = layout(*d, T);
@@ -392,7 +395,7 @@ int de_draft_layer(const de_moe_desc* d, int T, const float* x, const float* w_r
   if (d->shared_inter > 0 && (shared_w == nullptr || !aligned16(shared_w))) return DE_ERR_INVALID;
   if (draft_w != nullptr && !aligned16(draft_w)) return DE_ERR_INVALID;
   if (!std::isfinite(gamma)) return DE_ERR_INVALID;
-  if ((rc = check_table(*d, routed)) != DE_OK) return rc;
+  if ((rc = de::check_table(*d, routed)) != DE_OK) return rc;
   if ((rc = check_epi(epi)) != DE_OK) return rc;
   if ((rc = check_ws(*d, T, ws, ws_bytes)) != DE_OK) return rc;
   const Layout L = layout(*d, T);
@@ -433,7 +436,7 @@ int de_verify_layer(const de_moe_desc* d, int T, const float* x, const float* w_
   if (!x || !w_router || !y || !aligned16(x) || !aligned16(w_router) || d->hidden % 4)
     return DE_ERR_INVALID;
   if (d->shared_inter > 0 && (shared_w == nullptr || !aligned16(shared_w))) return DE_ERR_INVALID;
-  if ((rc = check_table(*d, routed)) != DE_OK) return rc;
+  if ((rc = de::check_table(*d, routed)) != DE_OK) return rc;
   if ((rc = check_epi(epi)) != DE_OK) return rc;
   if ((rc = check_ws(*d, T, ws, ws_bytes)) != DE_OK) return rc;
   const Layout L = layout(*d, T);

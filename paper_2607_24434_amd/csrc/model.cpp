@@ -1,0 +1,218 @@
+// The stacked model of the decoding step and Algorithm 1 on top of it: the
+// drafter generates K tokens one position at a time (Eq. 5 in every MoE
+// layer), the target scores the K+1-position block in one pass (Eq. 4), and
+// the greedy rule accepts the target-consistent prefix.  Every stage is one
+// of the layer calls, enqueued on the caller's stream; the tokens never leave
+// device memory, so a whole step runs without a host synchronisation.
+#include "../../include/draftexpert.h"
+
+#include <cmath>
+#include <cstdint>
+#include <utility>
+
+namespace de {
+int check_table(const de_moe_desc& d, const de_expert_table* t);
+}
+
+namespace {
+
+constexpr int kMaxLayers = 4096;
+
+size_t up256(size_t v) { return (v + 255) & ~size_t(255); }
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// Scratch of the model calls for blocks of up to T positions.  The two
+// regions holding control words come first, at offsets that do not depend on
+// T: the acceptance scratch, sized for the largest block (its counters sit at
+// its start for every row count), then the layer scratch (its counters sit at
+// its start for every block length).  One zero fill of a fresh allocation
+// therefore serves calls with any block length.
+constexpr int kMaxBlock = 64;
+
+struct ModelLayout {
+  size_t accept_ws, accept_bytes;
+  size_t layer_ws, layer_bytes;
+  size_t dense_ws, dense_bytes;
+  size_t misc;                // int32 [2]: acceptance output of the argmax-only calls
+  size_t h, n0, n1, logits;   // residual stream, two normed buffers, logits
+  size_t total;
+};
+
+ModelLayout model_layout(const de_model& m, int T) {
+  ModelLayout L{};
+  size_t o = 0;
+  auto take = [&](size_t bytes) {
+    const size_t r = o;
+    o += up256(bytes);
+    return r;
+  };
+  const size_t H = (size_t)m.moe.hidden;
+  L.accept_bytes = de_accept_workspace_bytes(kMaxBlock - 1, m.vocab);
+  L.layer_bytes = m.n_layers > 0 ? de_workspace_bytes(&m.moe, T) : 0;
+  L.dense_bytes = m.dense_inter > 0 ? de_dense_workspace_bytes(T, (int)H, m.dense_inter) : 0;
+  L.accept_ws = take(L.accept_bytes);
+  L.layer_ws = take(L.layer_bytes);
+  L.dense_ws = take(L.dense_bytes);
+  L.misc = take(8);
+  L.h = take((size_t)T * H * 4);
+  L.n0 = take((size_t)T * H * 4);
+  L.n1 = take((size_t)T * H * 4);
+  L.logits = take((size_t)T * m.vocab * 4);
+  L.total = o;
+  return L;
+}
+
+template <typename T>
+T* at(void* ws, size_t off) {
+  return reinterpret_cast<T*>(static_cast<char*>(ws) + off);
+}
+
+int check_block(const de_model& m, int T, const void* ws, size_t ws_bytes) {
+  if (T < 1 || T > kMaxBlock) return DE_ERR_INVALID;
+  if (ws == nullptr || (reinterpret_cast<uintptr_t>(ws) & 255u) != 0) return DE_ERR_WORKSPACE;
+  if (ws_bytes < model_layout(m, T).total) return DE_ERR_WORKSPACE;
+  return DE_OK;
+}
+
+// Where the argmax of a forward goes.  amax NULL skips the acceptance launch.
+struct ArgmaxOut {
+  int32_t* amax;          // [T]
+  int32_t* out;           // [2]: (n, bonus) against `drafts`
+  const int32_t* drafts;  // [T-1] (NULL when T is 1)
+};
+
+// Logits of T positions through the whole stack; the last MoE layer's fused
+// epilogue leaves RMSNorm(h) in the normed buffer, which the LM head reads.
+int forward(const de_model& m, int T, const int32_t* tokens, int mode, float* logits,
+            const ArgmaxOut& am, int32_t* n_union, int32_t* pred_idx, size_t pred_stride,
+            void* ws, const ModelLayout& L, hipStream_t s) {
+  const int H = m.moe.hidden;
+  float* h = at<float>(ws, L.h);
+  float* ncur = at<float>(ws, L.n0);
+  float* nnext = at<float>(ws, L.n1);
+  int rc = de_embed_gather(T, H, m.vocab, tokens, m.emb, h, ncur, m.eps, s);
+  if (rc != DE_OK) return rc;
+  if (m.dense_inter > 0) {
+    const de_epilogue epi{h, nnext, m.eps};
+    rc = de_dense_swiglu(T, H, m.dense_inter, m.dense_wdtype, ncur, m.dense_w, h, &epi,
+                         at<void>(ws, L.dense_ws), L.dense_bytes, s);
+    if (rc != DE_OK) return rc;
+    std::swap(ncur, nnext);
+  }
+  void* lws = at<void>(ws, L.layer_ws);
+  for (int l = 0; l < m.n_layers; ++l) {
+    const de_layer_weights& w = m.layers[l];
+    const de_epilogue epi{h, nnext, m.eps};
+    if (mode == DE_TARGET) {
+      rc = de_verify_layer(&m.moe, T, ncur, w.w_router, w.bias, &w.routed, w.shared_w, h, nullptr,
+                           nullptr, n_union ? n_union + l : nullptr, nullptr, nullptr, nullptr,
+                           nullptr, nullptr, &epi, lws, L.layer_bytes, s);
+    } else {
+      rc = de_draft_layer(&m.moe, T, ncur, w.w_router, w.bias, &w.routed, w.shared_w, w.draft_w,
+                          w.gamma, h, pred_idx ? pred_idx + l * pred_stride : nullptr, nullptr,
+                          &epi, lws, L.layer_bytes, s);
+    }
+    if (rc != DE_OK) return rc;
+    std::swap(ncur, nnext);
+  }
+  rc = de_lm_head(T, H, m.vocab, ncur, m.lm_head, logits, s);
+  if (rc != DE_OK || am.amax == nullptr) return rc;
+  return de_accept_len(T - 1, m.vocab, logits, am.drafts, am.amax, am.out,
+                       at<void>(ws, L.accept_ws), L.accept_bytes, s);
+}
+
+}  // namespace
+
+extern "C" {
+
+int de_check_model(const de_model* m) {
+  if (m == nullptr) return DE_ERR_INVALID;
+  int rc = de_check_desc(&m->moe);
+  if (rc != DE_OK) return rc;
+  const de_moe_desc& d = m->moe;
+  if (m->n_layers < 0 || m->n_layers > kMaxLayers) return DE_ERR_INVALID;
+  if (m->vocab < 1 || m->vocab > (1 << 24)) return DE_ERR_INVALID;
+  if (!(m->eps >= 0.f) || !std::isfinite(m->eps)) return DE_ERR_INVALID;
+  if (d.hidden % 8) return DE_ERR_INVALID;  // bf16 embedding and LM head rows
+  if (m->emb == nullptr || m->lm_head == nullptr || !aligned16(m->lm_head)) return DE_ERR_INVALID;
+  if (m->dense_inter < 0) return DE_ERR_INVALID;
+  if (m->dense_inter > 0) {
+    if (m->dense_wdtype != DE_F32 && m->dense_wdtype != DE_BF16) return DE_ERR_UNSUPPORTED;
+    const int al = m->dense_wdtype == DE_BF16 ? 8 : 4;
+    if (m->dense_inter % al || m->dense_inter > (1 << 17)) return DE_ERR_INVALID;
+    if (m->dense_w == nullptr || !aligned16(m->dense_w)) return DE_ERR_INVALID;
+  }
+  if (m->n_layers > 0 && m->layers == nullptr) return DE_ERR_INVALID;
+  for (int l = 0; l < m->n_layers; ++l) {
+    const de_layer_weights& w = m->layers[l];
+    if (w.w_router == nullptr || !aligned16(w.w_router) || d.hidden % 4) return DE_ERR_INVALID;
+    if (d.shared_inter > 0 && (w.shared_w == nullptr || !aligned16(w.shared_w)))
+      return DE_ERR_INVALID;
+    if (w.draft_w != nullptr && !aligned16(w.draft_w)) return DE_ERR_INVALID;
+    if (!std::isfinite(w.gamma)) return DE_ERR_INVALID;
+    if ((rc = de::check_table(d, &w.routed)) != DE_OK) return rc;
+  }
+  return DE_OK;
+}
+
+size_t de_model_workspace_bytes(const de_model* m, int T) {
+  if (de_check_model(m) != DE_OK || T < 1 || T > kMaxBlock) return 0;
+  return model_layout(*m, T).total;
+}
+
+int de_model_forward(const de_model* m, int T, const int32_t* tokens, int mode, float* logits,
+                     int32_t* argmax, int32_t* n_union, void* ws, size_t ws_bytes,
+                     hipStream_t stream) {
+  int rc = de_check_model(m);
+  if (rc != DE_OK) return rc;
+  if (mode != DE_TARGET && mode != DE_DRAFT) return DE_ERR_INVALID;
+  if (tokens == nullptr || logits == nullptr) return DE_ERR_INVALID;
+  if (n_union != nullptr && mode != DE_TARGET) return DE_ERR_INVALID;
+  if ((rc = check_block(*m, T, ws, ws_bytes)) != DE_OK) return rc;
+  const ModelLayout L = model_layout(*m, T);
+  // The acceptance launch also yields (n, bonus) against tokens[1..T-1]; the
+  // pair goes to scratch.
+  const ArgmaxOut am{argmax, at<int32_t>(ws, L.misc), T > 1 ? tokens + 1 : nullptr};
+  return forward(*m, T, tokens, mode, logits, am, n_union, nullptr, 0, ws, L, stream);
+}
+
+int de_spec_step(const de_model* m, int K, int32_t* block, int32_t* target_argmax, int32_t* out,
+                 int32_t* n_union, int32_t* pred_idx, void* ws, size_t ws_bytes,
+                 hipStream_t stream) {
+  int rc = de_check_model(m);
+  if (rc != DE_OK) return rc;
+  if (K < 0 || K > 63 || block == nullptr || target_argmax == nullptr || out == nullptr)
+    return DE_ERR_INVALID;
+  if ((rc = check_block(*m, K + 1, ws, ws_bytes)) != DE_OK) return rc;
+  const ModelLayout L = model_layout(*m, K + 1);
+  float* logits = at<float>(ws, L.logits);
+  const size_t k = (size_t)m->moe.top_k;
+  // Draft loop: position i's token is block[i]; its drafter argmax is block[i+1].
+  for (int i = 0; i < K; ++i) {
+    const ArgmaxOut am{block + i + 1, at<int32_t>(ws, L.misc), nullptr};
+    rc = forward(*m, 1, block + i, DE_DRAFT, logits, am, nullptr,
+                 pred_idx ? pred_idx + (size_t)i * m->n_layers * k : nullptr, k, ws, L, stream);
+    if (rc != DE_OK) return rc;
+  }
+  // Verify the block [c, d_1..d_K] and accept.
+  const ArgmaxOut am{target_argmax, out, K > 0 ? block + 1 : nullptr};
+  return forward(*m, K + 1, block, DE_TARGET, logits, am, n_union, nullptr, 0, ws, L, stream);
+}
+
+int de_greedy_decode(const de_model* m, int n_steps, int32_t* tokens, void* ws, size_t ws_bytes,
+                     hipStream_t stream) {
+  int rc = de_check_model(m);
+  if (rc != DE_OK) return rc;
+  if (n_steps < 0 || tokens == nullptr) return DE_ERR_INVALID;
+  if ((rc = check_block(*m, 1, ws, ws_bytes)) != DE_OK) return rc;
+  const ModelLayout L = model_layout(*m, 1);
+  float* logits = at<float>(ws, L.logits);
+  for (int i = 0; i < n_steps; ++i) {
+    const ArgmaxOut am{tokens + i + 1, at<int32_t>(ws, L.misc), nullptr};
+    rc = forward(*m, 1, tokens + i, DE_TARGET, logits, am, nullptr, nullptr, 0, ws, L, stream);
+    if (rc != DE_OK) return rc;
+  }
+  return DE_OK;
+}
+
+}  // extern "C"

@@ -108,3 +108,40 @@ def gapped_x(layer: OracleLayer, T: int, block: int = 0, max_redraw: int = 200):
                 raise RuntimeError("could not draw a gapped activation row")
             x[t] = gen.x_rows(c, t + 1, block, redraws)[t]
     return x, redraws
+
+
+class OracleModel:
+    """fp64 weights of a generated stacked model (MoE layer l uses the layer-l streams)."""
+
+    def __init__(self, model: configs.ModelCfg):
+        m = model.moe
+        self.cfg = model
+        self.layers = [OracleLayer(m, l) for l in range(1, model.n_moe_layers + 1)]
+        emb = gen.embedding(model)
+        dense = moe.split_expert(gen.dense_block(model), model.dense_inter, m.hidden)
+        lm = moe.to_f64(gen.lm_head(model.cfg_id, model.vocab, m.hidden, model.lm_std))
+        self.weights = decode.ModelWeights(
+            emb=lambda t: moe.to_f64(emb[t]), dense=dense,
+            layers=[ol.layer_weights() for ol in self.layers], lm_head=lm, eps=model.eps)
+
+    def trace_gaps_ok(self, tr: decode.Trace, gap: float = GAP) -> bool:
+        """Every routing decision and every row argmax of one pass has a margin > gap."""
+        k = self.cfg.moe.top_k
+        for ol, x in zip(self.layers, tr.moe_inputs):
+            _, _, (_, _, keys) = ol.route(x)
+            if not all(topk_gaps_ok(row, k, gap) for row in keys):
+                return False
+        lg = np.asarray(tr.logits, dtype=np.float32).astype(np.float64)
+        return all(topk_gaps_ok(row, 1, gap) for row in lg)
+
+    def gapped_step(self, K: int, tries: int = 6, redraw0: int = 0):
+        """An oracle step from the first generated start token whose decisions are all gapped.
+
+        Returns (start_token, drafts, n, bonus, target_argmax, traces)."""
+        for r in range(redraw0, redraw0 + tries):
+            c = gen.start_token(self.cfg, redraw=r)
+            traces: list = []
+            drafts, n, bonus, t = decode.spec_step(self.weights, c, K, traces)
+            if all(self.trace_gaps_ok(tr) for tr in traces):
+                return c, drafts, n, bonus, t, traces
+        raise RuntimeError("no gapped start token found")

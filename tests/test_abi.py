@@ -141,3 +141,58 @@ def test_binding_raises_on_error_codes():
     with pytest.raises(de.DEError) as ei:
         de._lib._check("de_verify_layer", raw_verify(d, 9))
     assert ei.value.code == -1
+
+
+def fake_model(n_layers=3, layer_kw=None, **kw):
+    tab = de.make_table(FAKE, 3 * 1408 * 2048 * 2, None, 64)
+    lay = dict(w_router=FAKE, bias=None, table=tab, shared_w=FAKE, draft_w=FAKE, gamma=1.0)
+    lay.update(layer_kw or {})
+    args = dict(vocab=102400, emb=FAKE, lm_head=FAKE, dense_w=FAKE, dense_inter=10944)
+    args.update(kw)
+    return de.make_model(cfg2_desc(), [dict(lay) for _ in range(n_layers)], **args)
+
+
+@pytest.mark.parametrize("kw,layer_kw,code", [
+    ({}, None, 0),
+    ({"vocab": 0}, None, -1),
+    ({"lm_head": None}, None, -1),
+    ({"lm_head": FAKE + 8}, None, -1),
+    ({"emb": None}, None, -1),
+    ({"dense_w": None}, None, -1),
+    ({"dense_w": None, "dense_inter": 0}, None, 0),
+    ({"dense_inter": 10940}, None, -1),          # not a multiple of 8 for bf16
+    ({"dense_wdtype": 5}, None, -2),
+    ({"eps": float("nan")}, None, -1),
+    ({}, {"w_router": None}, -1),
+    ({}, {"shared_w": None}, -1),
+    ({}, {"draft_w": None}, 0),                   # no draft expert: shared + top-1 only
+    ({}, {"draft_w": FAKE + 4}, -1),
+    ({}, {"gamma": float("inf")}, -1),
+    ({}, {"table": de.make_table(FAKE, 1024, None, 64)}, -1),
+])
+def test_check_model(kw, layer_kw, code):
+    assert de.de_check_model(fake_model(layer_kw=layer_kw, **kw)) == code
+
+
+def test_model_workspace_and_step_reject_bad_arguments_on_host():
+    m = fake_model()
+    L = de.LIB
+    sizes = [de.de_model_workspace_bytes(m, T) for T in (1, 5, 9, 17, 64)]
+    assert all(s > 0 for s in sizes) and sizes == sorted(sizes)
+    assert de.de_model_workspace_bytes(m, 0) == 0 and de.de_model_workspace_bytes(m, 65) == 0
+    # logits [T, V] and the layer scratch are both inside the model scratch
+    assert sizes[2] >= 9 * 102400 * 4 + de.de_workspace_bytes(cfg2_desc(), 9)
+    assert de.de_model_workspace_bytes(fake_model(vocab=0), 9) == 0
+    big = 1 << 34
+    mp = ctypes.byref(m)
+    assert L.de_spec_step(mp, -1, FAKE, FAKE, FAKE, None, None, FAKE, big, None) == -1
+    assert L.de_spec_step(mp, 64, FAKE, FAKE, FAKE, None, None, FAKE, big, None) == -1
+    assert L.de_spec_step(mp, 8, None, FAKE, FAKE, None, None, FAKE, big, None) == -1
+    assert L.de_spec_step(mp, 8, FAKE, FAKE, FAKE, None, None, FAKE, sizes[2] - 256, None) == -4
+    assert L.de_spec_step(mp, 8, FAKE, FAKE, FAKE, None, None, FAKE + 16, big, None) == -4
+    assert L.de_model_forward(mp, 9, FAKE, 2, FAKE, None, None, FAKE, big, None) == -1
+    assert L.de_model_forward(mp, 9, FAKE, de.DE_DRAFT, FAKE, None, FAKE, FAKE, big, None) == -1
+    assert L.de_model_forward(mp, 0, FAKE, de.DE_TARGET, FAKE, None, None, FAKE, big, None) == -1
+    assert L.de_greedy_decode(mp, -1, FAKE, FAKE, big, None) == -1
+    assert L.de_greedy_decode(mp, 4, FAKE, FAKE, 64, None) == -4
+    assert L.de_check_model(None) == -1

@@ -1,0 +1,143 @@
+"""The stacked model's draft-then-verify step on the GPU against the oracle.
+
+Small stacks (3 tiny fp32 layers; 2 V2-Lite-shaped layers) are compared with
+the fp64 oracle step: drafts, target argmax, accept length, bonus, the verify
+union size of every layer and the drafter's predicted experts bit-exact, the
+verify logits within 1e-4 relative.  The full 26-layer V2-Lite stack
+(102400-vocab head, K = 8) is checked through properties that hold at any
+size: the emitted tokens equal greedy target decoding, and a step is
+deterministic.
+"""
+from dataclasses import replace
+
+import numpy as np
+import pytest
+import torch
+
+from support import OracleModel, rel_err
+from workloads import configs
+from workloads import gpu as wgpu
+
+pytestmark = pytest.mark.gpu
+
+# A tiny fp32 stack whose drafter (gamma 6) often disagrees with the target,
+# so the start tokens below give accept lengths 4, 1 and 2 of K = 4.
+TINY = configs.scaled_model(configs.CFG4, n_moe_layers=3, vocab=1000, dense_inter=256, k_draft=4,
+                            moe=replace(configs.CFG1, cfg_id=41, gamma=6.0), name="tiny-stack")
+V2_SMALL = configs.scaled_model(configs.CFG4, n_moe_layers=2, vocab=8192, dense_inter=1408,
+                                k_draft=2, name="v2lite-stack-small")
+SMALL = [("tiny-3layer-K4-a", TINY, 0), ("tiny-3layer-K4-b", TINY, 3),
+         ("tiny-3layer-K4-c", TINY, 6), ("v2lite-2layer-K2", V2_SMALL, 0)]
+
+
+def device_model(model: configs.ModelCfg, max_block: int):
+    import paper_2607_24434_amd as de
+    m = model.moe
+    t = wgpu.model_tensors(model)
+    desc = de.make_desc(m.hidden, m.n_experts, m.top_k, m.inter, m.shared_inter, m.draft_inter,
+                        m.score_func, m.norm_topk, m.routed_scale, m.wdtype)
+    return de.DeviceModel(desc, t["layers"], model.vocab, t["emb"], t["lm"], t["dense"],
+                          model.dense_inter, de.DE_BF16, model.eps, m.gamma, max_block)
+
+
+_ORACLES: dict = {}
+_DEVICE: dict = {}
+
+
+@pytest.mark.parametrize("name,model,redraw0", SMALL, ids=[s[0] for s in SMALL])
+def test_spec_step_matches_oracle(name, model, redraw0):
+    import paper_2607_24434_amd as de
+    K = model.k_draft
+    L = model.n_moe_layers
+    k = model.moe.top_k
+    if model.name not in _ORACLES:
+        _ORACLES[model.name] = OracleModel(model)
+    om = _ORACLES[model.name]
+    c, drafts, n, bonus, t, traces = om.gapped_step(K, redraw0=redraw0)
+    print(f"{name}: start {c} drafts {drafts} n {n} bonus {bonus}", flush=True)
+    if model.name not in _DEVICE:
+        _DEVICE.clear()
+        _DEVICE[model.name] = device_model(model, K + 1)
+    dm = _DEVICE[model.name]
+    block = dm.new_block(K, c)
+    amax = torch.empty(K + 1, dtype=torch.int32, device="cuda")
+    out = torch.empty(2, dtype=torch.int32, device="cuda")
+    nu = torch.empty(L, dtype=torch.int32, device="cuda")
+    pred = torch.empty(K, L, k, dtype=torch.int32, device="cuda")
+    dm.spec_step(block, amax, out, nu, pred)
+    torch.cuda.synchronize()
+    assert block[1:].cpu().tolist() == drafts
+    assert amax.cpu().tolist() == [int(v) for v in t]
+    assert out.cpu().tolist() == [n, bonus]
+    ver = traces[-1]
+    assert nu.cpu().tolist() == [len(set(np.asarray(i).ravel().tolist())) for i in ver.idx]
+    want_pred = np.stack([np.stack([np.asarray(i)[0] for i in tr.idx]) for tr in traces[:K]])
+    np.testing.assert_array_equal(pred.cpu().numpy(), want_pred)
+    # Verify logits through the forward call on the same block.
+    logits = torch.empty(K + 1, model.vocab, dtype=torch.float32, device="cuda")
+    am2 = torch.empty(K + 1, dtype=torch.int32, device="cuda")
+    dm.forward(block, de.DE_TARGET, logits, am2)
+    torch.cuda.synchronize()
+    err = rel_err(logits.cpu().numpy(), ver.logits)
+    print(f"{name}: verify logits rel err {err:.2e}", flush=True)
+    assert err < 1e-4
+    assert torch.equal(am2, amax)
+    # Draft logits of the first position.
+    dl = torch.empty(1, model.vocab, dtype=torch.float32, device="cuda")
+    dm.forward(block[:1], de.DE_DRAFT, dl)
+    torch.cuda.synchronize()
+    assert rel_err(dl.cpu().numpy(), traces[0].logits) < 1e-4
+
+
+@pytest.fixture(scope="module")
+def full_model():
+    model = configs.CFG4
+    dm = device_model(model, model.k_draft + 1)
+    yield model, dm
+    del dm
+    torch.cuda.empty_cache()
+
+
+def test_full_stack_spec_step_emits_greedy_tokens(full_model):
+    from workloads import gen
+    model, dm = full_model
+    K, L = model.k_draft, model.n_moe_layers
+    amax = torch.empty(K + 1, dtype=torch.int32, device="cuda")
+    out = torch.empty(2, dtype=torch.int32, device="cuda")
+    nu = torch.empty(L, dtype=torch.int32, device="cuda")
+    pred = torch.empty(K, L, model.moe.top_k, dtype=torch.int32, device="cuda")
+    for r in range(3):
+        c = gen.start_token(model, redraw=r)
+        block = dm.new_block(K, c)
+        dm.spec_step(block, amax, out, nu, pred)
+        torch.cuda.synchronize()
+        n, bonus = out.cpu().tolist()
+        emitted = block[1:n + 1].cpu().tolist() + [bonus]
+        toks = torch.zeros(n + 2, dtype=torch.int32, device="cuda")
+        toks[0] = c
+        dm.greedy(toks)
+        torch.cuda.synchronize()
+        print(f"start {c}: n {n} emitted {emitted} union {nu.cpu().tolist()}", flush=True)
+        assert toks[1:].cpu().tolist() == emitted
+        assert 0 <= n <= K
+        u = nu.cpu().numpy()
+        assert np.all(u >= model.moe.top_k) and np.all(u <= min(model.moe.n_experts, (K + 1) * 6))
+        p = pred.cpu().numpy()
+        assert p.min() >= 0 and p.max() < model.moe.n_experts
+        assert all(len(set(row.tolist())) == model.moe.top_k for row in p.reshape(-1, 6))
+
+
+def test_full_stack_step_is_deterministic(full_model):
+    from workloads import gen
+    model, dm = full_model
+    K = model.k_draft
+    res = []
+    for _ in range(2):
+        block = dm.new_block(K, gen.start_token(model, redraw=7))
+        amax = torch.empty(K + 1, dtype=torch.int32, device="cuda")
+        out = torch.empty(2, dtype=torch.int32, device="cuda")
+        nu = torch.empty(model.n_moe_layers, dtype=torch.int32, device="cuda")
+        dm.spec_step(block, amax, out, nu)
+        torch.cuda.synchronize()
+        res.append((block.cpu().tolist(), amax.cpu().tolist(), out.cpu().tolist(), nu.cpu().tolist()))
+    assert res[0] == res[1]

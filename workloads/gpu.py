@@ -95,3 +95,28 @@ def to_device(a: np.ndarray, device="cuda") -> torch.Tensor:
 
 def router(cfg: MoECfg, layer: int, device="cuda", redraw: int = 0) -> torch.Tensor:
     return to_device(gen.router_weight(cfg, layer, redraw), device)
+
+
+def model_tensors(model: ModelCfg, device="cuda", redraw: int = 0) -> dict:
+    """Every weight of a stacked model, resident in HBM.
+
+    MoE layer l (1..L) uses the layer-l streams of the per-layer generators;
+    layer 0 is the dense layer.  Returns {"emb", "dense", "lm", "layers"}, each
+    layer a dict with "router", "bias", "routed", "shared", "draft"."""
+    m = model.moe
+    layers = []
+    for l in range(1, model.n_moe_layers + 1):
+        b = gen.router_bias(m, l, redraw)
+        layers.append(dict(
+            router=router(m, l, device, redraw),
+            bias=None if b is None else to_device(b, device),
+            routed=routed_experts(m, l, device, redraw),
+            shared=shared_block(m, l, device, redraw) if m.shared_inter else None,
+            draft=draft_block(m, l, device, redraw) if m.draft_inter else None,
+        ))
+    return dict(
+        emb=embedding(model, device, redraw),
+        dense=dense_block(model, device, redraw) if model.dense_inter else None,
+        lm=lm_head(model.cfg_id, model.vocab, m.hidden, model.lm_std, device, redraw),
+        layers=layers,
+    )
