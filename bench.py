@@ -73,6 +73,9 @@ def parse():
     p.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     p.add_argument("--cpu-seconds", type=float, default=12.0)
     p.add_argument("--no-probe", action="store_true", help="skip the HBM read-ceiling probe")
+    p.add_argument("--no-full-step", action="store_true",
+                   help="skip the 26-layer draft+verify step measurement")
+    p.add_argument("--full-steps", type=int, default=12)
     return p.parse_args()
 
 
@@ -209,6 +212,8 @@ def main():
                 + (T * cfg.top_k * cfg.inter + T * cfg.shared_inter) * 4 + (T * cfg.top_k + T) * H * 4)
     dn_gbs = float(dn_bytes.sum() / (sum(dn_ms) * 1e-3) / 1e9)
 
+    full = None if args.no_full_step else full_step(args, de, configs, gen, wgpu, torch, np)
+
     probe_gbs = None
     if not args.no_probe:
         nbytes = 4 << 30
@@ -277,9 +282,103 @@ def main():
             "traffic_vs_algorithmic": PMC_TRAFFIC["vs_algorithmic"] if pmc_traffic() else None,
             "algorithmic_bytes_per_launch": int(round(float(gu_bytes.mean()))),
         },
+        "full_step": full,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
+
+
+def full_step(args, de, configs, gen, wgpu, torch, np):
+    """Decode with the full V2-Lite-shaped stack: dense layer 0 + 26 MoE layers,
+    K = 8 drafts per step, 102400-vocab head.  Steps run back to back on the
+    device (each step's bonus token is the next step's last committed token,
+    copied on the device), so the timed region has no host synchronisation."""
+    model = configs.CFG4
+    m = model.moe
+    K, Lyr, V, H = model.k_draft, model.n_moe_layers, model.vocab, m.hidden
+    dev = "cuda"
+    t0 = time.perf_counter()
+    t = wgpu.model_tensors(model, dev)
+    desc = de.make_desc(m.hidden, m.n_experts, m.top_k, m.inter, m.shared_inter, m.draft_inter,
+                        m.score_func, m.norm_topk, m.routed_scale, m.wdtype)
+    dm = de.DeviceModel(desc, t["layers"], V, t["emb"], t["lm"], t["dense"], model.dense_inter,
+                        de.DE_BF16, model.eps, m.gamma, K + 1, dev)
+    torch.cuda.synchronize()
+    fill_s = time.perf_counter() - t0
+    W, S = 2, args.full_steps
+    n_all = W + S
+    blocks = torch.zeros(n_all, K + 1, dtype=torch.int32, device=dev)
+    amax = torch.empty(n_all, K + 1, dtype=torch.int32, device=dev)
+    outs = torch.empty(n_all, 2, dtype=torch.int32, device=dev)
+    nus = torch.empty(n_all, Lyr, dtype=torch.int32, device=dev)
+    blocks[0, 0] = gen.start_token(model)
+
+    def run(i):
+        dm.spec_step(blocks[i], amax[i], outs[i], nus[i])
+        if i + 1 < n_all:
+            blocks[i + 1, :1].copy_(outs[i, 1:])
+
+    for i in range(W):
+        run(i)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for i in range(W, n_all):
+        run(i)
+    e1.record()
+    torch.cuda.synchronize()
+    step_ms = e0.elapsed_time(e1) / S
+
+    # The two halves of a step, timed apart: one draft position, one verify block.
+    lg = torch.empty(K + 1, V, dtype=torch.float32, device=dev)
+    am = torch.empty(K + 1, dtype=torch.int32, device=dev)
+    reps = 6
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    ev[0].record()
+    for i in range(reps):
+        dm.forward(blocks[W + i, :1], de.DE_DRAFT, lg[:1], am[:1])
+    ev[1].record()
+    for i in range(reps):
+        dm.forward(blocks[W + i], de.DE_TARGET, lg, am)
+    ev[2].record()
+    torch.cuda.synchronize()
+    draft_ms = ev[0].elapsed_time(ev[1]) / reps
+    verify_ms = ev[1].elapsed_time(ev[2]) / reps
+
+    o = outs[W:].cpu().numpy()
+    nu = nus[W:].cpu().numpy().astype(np.float64)
+    emitted = int((o[:, 0] + 1).sum())
+    eb = m.expert_bytes()
+    shared_b = m.expert_bytes(m.shared_inter)
+    draft_b = m.expert_bytes(m.draft_inter)
+    router_b = m.n_experts * H * 4
+    dense_b = 3 * model.dense_inter * H * 2
+    head_b = V * H * 2
+    draft_bytes = dense_b + Lyr * (router_b + shared_b + eb + draft_b) + head_b
+    verify_bytes = dense_b + Lyr * (router_b + shared_b) + float(nu.sum(axis=1).mean()) * eb + head_b
+    step_bytes = K * draft_bytes + verify_bytes
+    res = {
+        "workload": "v2lite-step-K8: dense layer 0 (I=10944) + 26 V2-Lite MoE layers, K=8 drafts "
+                    "(shared + top-1 + draft expert), one 9-position verify block, 102400-vocab "
+                    "bf16 LM head, greedy accept; random weights, so acceptance is that of an "
+                    "untrained drafter",
+        "steps": S,
+        "ms_per_step": round(step_ms, 3),
+        "tokens_per_s": round(emitted / (S * step_ms * 1e-3), 2),
+        "accept_mean": round(float(o[:, 0].mean()), 3),
+        "tokens_per_s_if_all_accepted": round((K + 1) / (step_ms * 1e-3), 2),
+        "draft_position_ms": round(draft_ms, 3),
+        "verify_block_ms": round(verify_ms, 3),
+        "union_mean_per_layer": round(float(nu.mean()), 2),
+        "union_per_layer_min_max": [int(nu.min()), int(nu.max())],
+        "step_gb": round(step_bytes / 1e9, 3),
+        "step_hbm_gbs": round(step_bytes / (step_ms * 1e-3) / 1e9, 1),
+        "step_hbm_frac": round(step_bytes / (step_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+        "weights_fill_s": round(fill_s, 2),
+    }
+    del dm, t
+    torch.cuda.empty_cache()
+    return res
 
 
 def cpu_baseline(cfg, x, budget_s):
