@@ -278,6 +278,115 @@ int de_spec_step(const de_model* m, int K, int32_t* block, int32_t* target_argma
 int de_greedy_decode(const de_model* m, int n_steps, int32_t* tokens, void* ws, size_t ws_bytes,
                      hipStream_t stream);
 
+/* ---- Expert cache over a pinned host pool (Section 3.5, Algorithm 1) ----
+ *
+ * Routed experts live in a pinned host pool; each MoE layer has n_slots HBM
+ * slots.  The cache keeps the accelerator expert set C (which expert is in
+ * which slot), starts copies on its own streams (prefetches of predicted
+ * verifier experts, on-demand loads of misses), and hands the kernels a
+ * per-layer slot table in which exactly the experts of the current request
+ * are marked resident.  Bookkeeping is host-side and deterministic; only the
+ * stall time depends on timing.
+ *
+ * Policy (the paper names the sets but no eviction rule):
+ *   - a free slot (lowest index) is used first; otherwise the least recently
+ *     used slot (ties: lowest index) whose expert is neither needed by the
+ *     current request nor predicted for the current block; a demand load may
+ *     fall back to a predicted, unneeded expert; a prefetch may not, and is
+ *     skipped when no slot qualifies;
+ *   - an expert in flight counts as resident: a request for it waits on its
+ *     copy (hits include such waits);
+ *   - "use" (LRU time) is a request or a copy; a prefetch of a resident
+ *     expert changes nothing but the predicted set. */
+typedef struct de_cache de_cache; /* opaque */
+
+typedef struct de_cache_cfg {
+  int32_t n_layers;          /* L */
+  int32_t n_experts;         /* N routed experts per layer */
+  int32_t n_slots;           /* HBM slots per layer, 1..N */
+  int32_t fake_copies;       /* 1: copies are host memcpy and every pointer below is
+                                host memory (bookkeeping without a GPU) */
+  int64_t expert_bytes;      /* bytes of one expert block, multiple of 16 */
+  int64_t slot_stride_bytes; /* >= expert_bytes, multiple of 256 */
+  const void* host_pool;     /* pinned host [L][N] blocks, stride expert_bytes */
+  void* slot_pool;           /* device [L][n_slots] blocks, stride slot_stride_bytes */
+  int32_t* slot_map;         /* device int32 [L][N]: the slot tables the kernels read */
+} de_cache_cfg;
+
+typedef struct de_cache_counts {
+  int64_t prefetch_issued;  /* copies started by de_cache_prefetch */
+  int64_t prefetch_used;    /* ... needed by a verify request of the same block */
+  int64_t prefetch_wasted;  /* ... evicted, or left when their block ended, unused */
+  int64_t prefetch_skipped; /* predictions dropped for want of an evictable slot */
+  int64_t draft_needed;     /* experts requested by the draft path (top-1) */
+  int64_t draft_hits;       /* ... found resident or in flight */
+  int64_t verify_needed;    /* experts requested by verify chunks */
+  int64_t verify_hits;      /* ... found resident or in flight */
+  int64_t demand_loads;     /* copies started by de_cache_ensure (misses) */
+  int64_t evictions;
+  int64_t bytes_copied;     /* host-to-device bytes of all copies */
+  double stall_us;          /* time the compute stream waited for copies */
+  int64_t draft_layers;     /* MoE layers run by de_spec_step_cached on the draft path */
+  double draft_layer_us;    /* ... their summed duration on the compute stream */
+  int64_t verify_layers;    /* verify MoE layers run by de_spec_step_cached */
+  double verify_layer_us;   /* ... their summed duration (routing, readback, copies
+                               waited for, every chunk, combine) */
+} de_cache_counts;
+
+#define DE_NEED_DRAFT 0  /* the draft path's top-1 expert (Eq. 5) */
+#define DE_NEED_VERIFY 1 /* a chunk of the verify union (Eq. 3) */
+
+/* Creates a cold cache (every slot empty; slot_map filled with -1).  The
+ * caller owns the three memory regions; the cache owns two copy streams
+ * (default priority), per-slot events and a small pinned scratch. */
+int de_cache_create(const de_cache_cfg* cfg, de_cache** out);
+/* Waits for outstanding copies and frees the cache's own objects. */
+int de_cache_destroy(de_cache* c);
+/* Empties every slot and zeroes the statistics (waits for copies first). */
+int de_cache_reset(de_cache* c);
+/* Starts a new draft/verify block: prefetched experts the ending block's
+ * verify never requested count as wasted; every predicted set is cleared. */
+int de_cache_begin_block(de_cache* c);
+/* Records experts_host[0..n) (host array) as predicted verifier experts of
+ * `layer` for the current block and starts a copy for each that is neither
+ * resident nor in flight (Algorithm 1: prefetch of the newly predicted set
+ * minus C and P).  Returns without waiting. */
+int de_cache_prefetch(de_cache* c, int layer, const int32_t* experts_host, int n);
+/* Makes the n distinct experts needed_host[0..n) (n <= n_slots) resident in
+ * `layer`, starting on-demand copies for misses; `compute` waits for every
+ * copy they depend on; then the layer's slot table is rewritten on `compute`
+ * with exactly these n experts resident (-1 elsewhere).  Host-synchronous
+ * bookkeeping; the GPU work is enqueued. */
+int de_cache_ensure(de_cache* c, int layer, const int32_t* needed_host, int n, int purpose,
+                    hipStream_t compute);
+/* The work enqueued on `compute` so far is the last to read `layer`'s slots:
+ * later copies into them wait for it. */
+int de_cache_release(de_cache* c, int layer, hipStream_t compute);
+/* The expert table of `layer` (base = its first slot, slot_of_expert = its
+ * row of slot_map). */
+int de_cache_table(const de_cache* c, int layer, de_expert_table* table);
+/* Statistics since creation or the last reset (waits for every copy and
+ * event it reads). */
+int de_cache_stats(de_cache* c, de_cache_counts* stats);
+/* Host view of which slot holds each expert of `layer` (-1: none), into
+ * slot_of_expert_host [N]. */
+int de_cache_slots(const de_cache* c, int layer, int32_t* slot_of_expert_host);
+
+/* de_spec_step with the routed experts behind the cache (Algorithm 1 with
+ * offload).  At every draft position and MoE layer the drafter's router runs
+ * first; its top-k is read back to the host, the top-1 expert is requested
+ * (DE_NEED_DRAFT) and the whole top-k is prefetched for verification; then
+ * the layer's grouped part runs on the cached slots.  Verification reads each
+ * layer's union back, requests it in chunks of at most n_slots members
+ * (members resident or in flight first, then the rest, each part in
+ * ascending id), and combines after the last chunk, which gives the same
+ * bits as the resident step.  The routed tables of m->layers are not used.
+ * Synchronises the host with `stream` once per layer and position.
+ * Arguments as de_spec_step; pred_idx [K, n_layers, k] may be NULL. */
+int de_spec_step_cached(const de_model* m, de_cache* cache, int K, int32_t* block,
+                        int32_t* target_argmax, int32_t* out, int32_t* n_union, int32_t* pred_idx,
+                        void* ws, size_t ws_bytes, hipStream_t stream);
+
 /* Pure streaming read of `bytes` (multiple of 16) from buf: the measured HBM
  * read ceiling.  sink [1] receives a value that depends on every byte. */
 int de_stream_probe(const void* buf, size_t bytes, float* sink, hipStream_t stream);

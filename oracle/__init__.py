@@ -10,10 +10,11 @@ Modules
             target output (Eq. 4), draft output (Eq. 5), RMSNorm, greedy accept
     decode  the stacked model, the exact draft/verify step and greedy AR
             decoding (Algorithm 1)
-    cache   the expert cache with draft-router prefetch (Section 3.5)
+    cache_sim  the expert cache bookkeeping with draft-router prefetch
+               (Section 3.5, Algorithm 1)
 
 Pins (tests/test_oracle_*.py) tie every function to the paper or to
 mathematics independent of this code; functions without such a pin say
 "parity unpinned" in their docstring.
 """
-from . import decode, moe  # noqa: F401
+from . import cache_sim, decode, moe  # noqa: F401

@@ -31,12 +31,16 @@ C_FUNCS = [
     "de_lm_head", "de_rmsnorm", "de_embed_gather", "de_dense_workspace_bytes", "de_dense_swiglu",
     "de_stream_probe", "de_time_next_phase",
     "de_check_model", "de_model_workspace_bytes", "de_model_forward", "de_spec_step",
-    "de_greedy_decode",
+    "de_greedy_decode", "de_cache_create", "de_cache_destroy", "de_cache_reset",
+    "de_cache_begin_block", "de_cache_prefetch", "de_cache_ensure", "de_cache_release",
+    "de_cache_table", "de_cache_stats", "de_cache_slots", "de_spec_step_cached",
 ]
 DE_PHASE_GATEUP = 0
 DE_PHASE_DOWN = 1
 DE_TARGET = 0
 DE_DRAFT = 1
+DE_NEED_DRAFT = 0
+DE_NEED_VERIFY = 1
 
 
 class DEError(RuntimeError):
@@ -82,6 +86,27 @@ class Model(ctypes.Structure):
     ]
 
 
+class CacheCfg(ctypes.Structure):
+    _fields_ = [
+        ("n_layers", ctypes.c_int32), ("n_experts", ctypes.c_int32), ("n_slots", ctypes.c_int32),
+        ("fake_copies", ctypes.c_int32), ("expert_bytes", ctypes.c_int64),
+        ("slot_stride_bytes", ctypes.c_int64), ("host_pool", ctypes.c_void_p),
+        ("slot_pool", ctypes.c_void_p), ("slot_map", ctypes.c_void_p),
+    ]
+
+
+CACHE_COUNTS = ("prefetch_issued", "prefetch_used", "prefetch_wasted", "prefetch_skipped",
+                "draft_needed", "draft_hits", "verify_needed", "verify_hits", "demand_loads",
+                "evictions", "bytes_copied")
+
+
+class CacheCounts(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int64) for n in CACHE_COUNTS] + [
+        ("stall_us", ctypes.c_double), ("draft_layers", ctypes.c_int64),
+        ("draft_layer_us", ctypes.c_double), ("verify_layers", ctypes.c_int64),
+        ("verify_layer_us", ctypes.c_double)]
+
+
 def _load(path: str = LIB_PATH):
     if not os.path.exists(path):
         raise ImportError(f"{path} is missing: build it with `python paper_2607_24434_amd/build.py`")
@@ -94,6 +119,9 @@ def _load(path: str = LIB_PATH):
     TP = ctypes.POINTER(ExpertTable)
     EP = ctypes.POINTER(Epilogue)
     MP = ctypes.POINTER(Model)
+    CP = ctypes.POINTER(CacheCfg)
+    KP = ctypes.POINTER(CacheCounts)
+    I32P = ctypes.POINTER(ctypes.c_int32)
     sig = {
         "de_abi_version": (I, []),
         "de_error_string": (ctypes.c_char_p, [I]),
@@ -119,6 +147,17 @@ def _load(path: str = LIB_PATH):
         "de_model_forward": (I, [MP, I, P, I, P, P, P, P, SZ, P]),
         "de_spec_step": (I, [MP, I, P, P, P, P, P, P, SZ, P]),
         "de_greedy_decode": (I, [MP, I, P, P, SZ, P]),
+        "de_cache_create": (I, [CP, ctypes.POINTER(P)]),
+        "de_cache_destroy": (I, [P]),
+        "de_cache_reset": (I, [P]),
+        "de_cache_begin_block": (I, [P]),
+        "de_cache_prefetch": (I, [P, I, I32P, I]),
+        "de_cache_ensure": (I, [P, I, I32P, I, I, P]),
+        "de_cache_release": (I, [P, I, P]),
+        "de_cache_table": (I, [P, I, TP]),
+        "de_cache_stats": (I, [P, KP]),
+        "de_cache_slots": (I, [P, I, I32P]),
+        "de_spec_step_cached": (I, [MP, P, I, P, P, P, P, P, P, SZ, P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -343,3 +382,86 @@ def de_greedy_decode(model, n_steps, tokens, ws=None, stream=None):
     _check("de_greedy_decode", LIB.de_greedy_decode(
         ctypes.byref(model), int(n_steps), _ptr(tokens), _ptr(ws),
         ws.numel() if ws is not None else 0, _stream(stream)))
+
+
+def _i32(values):
+    vals = [int(v) for v in values]
+    return (ctypes.c_int32 * max(1, len(vals)))(*vals), len(vals)
+
+
+class ExpertCache:
+    """Owner of a ``de_cache``: per-layer HBM slots over a host pool of expert blocks.
+
+    ``host_pool`` is a pinned CPU tensor [L, N, expert_bytes] (uint8 view of the
+    blocks).  With ``fake=True`` the slot pool and slot map are CPU tensors and
+    copies are host memcpy (bookkeeping without a GPU)."""
+
+    def __init__(self, n_layers, n_experts, n_slots, expert_bytes, host_pool, fake=False,
+                 device="cuda"):
+        stride = (int(expert_bytes) + 255) // 256 * 256
+        dev = "cpu" if fake else device
+        self.slot_pool = torch.empty(n_layers * n_slots * stride, dtype=torch.uint8, device=dev)
+        self.slot_map = torch.empty(n_layers * n_experts, dtype=torch.int32, device=dev)
+        self.host_pool = host_pool
+        self.cfg = CacheCfg(int(n_layers), int(n_experts), int(n_slots), int(bool(fake)),
+                            int(expert_bytes), stride, _ptr(host_pool), _ptr(self.slot_pool),
+                            _ptr(self.slot_map))
+        self.n_layers, self.n_experts, self.n_slots = int(n_layers), int(n_experts), int(n_slots)
+        self.stride = stride
+        h = ctypes.c_void_p()
+        _check("de_cache_create", LIB.de_cache_create(ctypes.byref(self.cfg), ctypes.byref(h)))
+        self.handle = h
+
+    def close(self):
+        if self.handle is not None and self.handle.value:
+            _check("de_cache_destroy", LIB.de_cache_destroy(self.handle))
+        self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:  # noqa: BLE001
+            pass
+
+    def reset(self):
+        _check("de_cache_reset", LIB.de_cache_reset(self.handle))
+
+    def begin_block(self):
+        _check("de_cache_begin_block", LIB.de_cache_begin_block(self.handle))
+
+    def prefetch(self, layer, experts):
+        arr, n = _i32(experts)
+        _check("de_cache_prefetch", LIB.de_cache_prefetch(self.handle, int(layer), arr, n))
+
+    def ensure(self, layer, needed, purpose, stream=None):
+        arr, n = _i32(needed)
+        s = None if self.cfg.fake_copies else _stream(stream)
+        _check("de_cache_ensure", LIB.de_cache_ensure(self.handle, int(layer), arr, n,
+                                                      int(purpose), s))
+
+    def release(self, layer, stream=None):
+        s = None if self.cfg.fake_copies else _stream(stream)
+        _check("de_cache_release", LIB.de_cache_release(self.handle, int(layer), s))
+
+    def table(self, layer) -> ExpertTable:
+        t = ExpertTable()
+        _check("de_cache_table", LIB.de_cache_table(self.handle, int(layer), ctypes.byref(t)))
+        return t
+
+    def stats(self) -> dict:
+        k = CacheCounts()
+        _check("de_cache_stats", LIB.de_cache_stats(self.handle, ctypes.byref(k)))
+        return {n: getattr(k, n) for n, _ in CacheCounts._fields_}
+
+    def slots(self, layer) -> list:
+        arr = (ctypes.c_int32 * self.n_experts)()
+        _check("de_cache_slots", LIB.de_cache_slots(self.handle, int(layer), arr))
+        return list(arr)
+
+
+def de_spec_step_cached(model, cache, K, block, target_argmax, out, n_union=None, pred_idx=None,
+                        ws=None, stream=None):
+    _check("de_spec_step_cached", LIB.de_spec_step_cached(
+        ctypes.byref(model), cache.handle, int(K), _ptr(block), _ptr(target_argmax), _ptr(out),
+        _ptr(n_union), _ptr(pred_idx), _ptr(ws), ws.numel() if ws is not None else 0,
+        _stream(stream)))

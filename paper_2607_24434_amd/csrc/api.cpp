@@ -177,10 +177,14 @@ de::RoutedSrc routed_src(const de_moe_desc& d, int T, const de_expert_table* tab
 
 // gate/up + down + combine over the union (kk entries per position) and the
 // dense sources (shared path with gate 1, optionally the draft expert).
+// With dense_on false the dense sources are left out of the two grouped
+// launches (their partials from an earlier call stay in the workspace); with
+// combine_on false the combine is not launched.  Both true for a whole layer.
 int run_grouped(const de_moe_desc& d, int T, const float* x, const de::RoutedSrc& r,
                 const int32_t* pair_pos, int kk, const void* shared_w, const void* draft_w,
                 float gamma, float* y, const de_epilogue* epi, const Layout& L, void* ws,
-                const de::TopkUnionArgs* fused_sel, hipStream_t s) {
+                const de::TopkUnionArgs* fused_sel, hipStream_t s, bool dense_on = true,
+                bool combine_on = true) {
   const size_t esz = elem_bytes(d.wdtype);
   de::GroupedArgs g{};
   if (fused_sel != nullptr) {
@@ -197,13 +201,13 @@ int run_grouped(const de_moe_desc& d, int T, const float* x, const de::RoutedSrc
   c.T = T;
   c.H = d.hidden;
   c.n_dense = 0;
-  if (shared_w != nullptr && d.shared_inter > 0) {
+  if (dense_on && shared_w != nullptr && d.shared_inter > 0) {
     de::DenseSrc& ds = g.dense[g.n_dense++];
     ds.w = shared_w;
     ds.inter = d.shared_inter;
     ds.out = at<float>(ws, L.a_s);
   }
-  if (draft_w != nullptr && d.draft_inter > 0) {
+  if (dense_on && draft_w != nullptr && d.draft_inter > 0) {
     de::DenseSrc& ds = g.dense[g.n_dense++];
     ds.w = draft_w;
     ds.inter = d.draft_inter;
@@ -250,7 +254,7 @@ int run_grouped(const de_moe_desc& d, int T, const float* x, const de::RoutedSrc
     ds.out_stride = d.hidden;
     c.dense_p[c.n_dense++] = ds.out;
   }
-  g.n_dense = nd;
+  g.n_dense = dense_on ? nd : 0;  // the combine reads the dense partials either way
   g.fuse_route = 0;
   c.p_r = r.p;
   c.pair_pos = pair_pos;
@@ -262,10 +266,63 @@ int run_grouped(const de_moe_desc& d, int T, const float* x, const de::RoutedSrc
   c.eps = epi ? epi->eps : 0.f;
   e = timed_phase(DE_PHASE_DOWN, s, [&] { return de::launch_down(g, d.wdtype, s); });
   if (e != hipSuccess) return DE_ERR_HIP;
+  if (!combine_on) return DE_OK;
   return hip_status(de::launch_combine(c, s));
 }
 
 }  // namespace
+
+namespace de {
+
+// The grouped part of a layer whose routing already ran: the union of the
+// first `ucols` entries of each position's lists idx / gate [T, k] (device),
+// built in the gate/up prologue, then gate/up and down over the members the
+// table marks resident, with the dense sources when dense_on, and the combine
+// when combine_on.  Calls over the same lists with disjoint resident members
+// (dense_on in exactly one, combine_on in the last) produce the same bits as
+// one call with every member resident: each pair's partial is written once,
+// and the combine sums them in list order.
+int layer_after_route(const de_moe_desc& d, int T, const float* x, const de_expert_table* routed,
+                      const int32_t* idx, const float* gate, int ucols, const void* shared_w,
+                      const void* draft_w, float gamma, float* y, const de_epilogue* epi,
+                      bool dense_on, bool combine_on, int32_t* n_union, void* ws,
+                      size_t ws_bytes, hipStream_t stream) {
+  int rc = de_check_desc(&d);
+  if (rc != DE_OK) return rc;
+  if ((rc = check_T(T)) != DE_OK) return rc;
+  if (!x || !idx || !gate || !y || !aligned16(x) || ucols < 1 || ucols > d.top_k)
+    return DE_ERR_INVALID;
+  if (d.shared_inter > 0 && (shared_w == nullptr || !aligned16(shared_w))) return DE_ERR_INVALID;
+  if (draft_w != nullptr && !aligned16(draft_w)) return DE_ERR_INVALID;
+  if (!std::isfinite(gamma)) return DE_ERR_INVALID;
+  if ((rc = check_table(d, routed)) != DE_OK) return rc;
+  if ((rc = check_epi(epi)) != DE_OK) return rc;
+  if ((rc = check_ws(d, T, ws, ws_bytes)) != DE_OK) return rc;
+  const Layout L = layout(d, T);
+  TopkUnionArgs a{};
+  a.T = T;
+  a.N = d.n_experts;
+  a.k = d.top_k;
+  a.score_func = d.score_func;
+  a.norm_topk = d.norm_topk;
+  a.routed_scale = d.routed_scale;
+  a.idx_out = const_cast<int32_t*>(idx);  // read only: the prologue copies the lists
+  a.gate_out = const_cast<float*>(gate);
+  a.ucols = ucols;
+  a.n_union = n_union ? n_union : at<int32_t>(ws, L.nu);
+  a.union_ids = at<int32_t>(ws, L.uids);
+  a.offsets = at<int32_t>(ws, L.offs);
+  a.tok_list = at<int32_t>(ws, L.tok);
+  a.gate_list = at<float>(ws, L.glist);
+  a.pair_pos = at<int32_t>(ws, L.ppos);
+  a.z = at<float>(ws, L.z);
+  const RoutedSrc r = routed_src(d, T, routed, a.n_union, a.union_ids, a.offsets, a.tok_list,
+                                 a.gate_list, at<float>(ws, L.a_r), at<float>(ws, L.p_r));
+  return run_grouped(d, T, x, r, a.pair_pos, ucols, shared_w, draft_w, gamma, y, epi, L, ws, &a,
+                     stream, dense_on, combine_on);
+}
+
+}  // namespace de
 
 extern "C" {
 

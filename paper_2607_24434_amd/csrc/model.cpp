@@ -6,12 +6,25 @@
 // device memory, so a whole step runs without a host synchronisation.
 #include "../../include/draftexpert.h"
 
+#include <algorithm>
 #include <cmath>
 #include <cstdint>
 #include <utility>
+#include <vector>
 
 namespace de {
 int check_table(const de_moe_desc& d, const de_expert_table* t);
+int layer_after_route(const de_moe_desc& d, int T, const float* x, const de_expert_table* routed,
+                      const int32_t* idx, const float* gate, int ucols, const void* shared_w,
+                      const void* draft_w, float gamma, float* y, const de_epilogue* epi,
+                      bool dense_on, bool combine_on, int32_t* n_union, void* ws,
+                      size_t ws_bytes, hipStream_t stream);
+int32_t* cache_readback(de_cache* c);
+int cache_slots_per_layer(const de_cache* c);
+int cache_experts(const de_cache* c);
+int cache_layers(const de_cache* c);
+bool cache_resident(const de_cache* c, int layer, int e);
+int cache_span(de_cache* c, bool end, int purpose, hipStream_t s);
 }
 
 namespace {
@@ -34,6 +47,7 @@ struct ModelLayout {
   size_t layer_ws, layer_bytes;
   size_t dense_ws, dense_bytes;
   size_t misc;                // int32 [2]: acceptance output of the argmax-only calls
+  size_t ridx, rgate;         // top-k lists of the cached step's routing [64, k]
   size_t h, n0, n1, logits;   // residual stream, two normed buffers, logits
   size_t total;
 };
@@ -54,6 +68,8 @@ ModelLayout model_layout(const de_model& m, int T) {
   L.layer_ws = take(L.layer_bytes);
   L.dense_ws = take(L.dense_bytes);
   L.misc = take(8);
+  L.ridx = take((size_t)kMaxBlock * m.moe.top_k * 4);
+  L.rgate = take((size_t)kMaxBlock * m.moe.top_k * 4);
   L.h = take((size_t)T * H * 4);
   L.n0 = take((size_t)T * H * 4);
   L.n1 = take((size_t)T * H * 4);
@@ -81,11 +97,78 @@ struct ArgmaxOut {
   const int32_t* drafts;  // [T-1] (NULL when T is 1)
 };
 
+// MoE layer l with its routed experts behind the cache.  The routing runs
+// first and its lists come back to the host (one synchronisation).  Draft
+// (T = 1): the top-1 expert is requested, the top-k prefetched, then the
+// grouped part runs over the top-1 column.  Verify: the union's members are
+// requested in chunks of at most n_slots (resident or in flight first, then
+// the rest, each in ascending id); every chunk runs gate/up and down over its
+// members, the first also over the shared path, the last also the combine.
+int cached_layer(const de_model& m, de_cache* c, int l, int T, bool draft, const float* x,
+                 float* h, float* normed_out, int32_t* n_union, int32_t* pred_out, void* ws,
+                 const ModelLayout& L, hipStream_t s) {
+  const de_layer_weights& w = m.layers[l];
+  const int k = m.moe.top_k, N = m.moe.n_experts;
+  const int purpose = draft ? DE_NEED_DRAFT : DE_NEED_VERIFY;
+  void* lws = at<void>(ws, L.layer_ws);
+  int32_t* ridx = at<int32_t>(ws, L.ridx);
+  float* rgate = at<float>(ws, L.rgate);
+  int rc = de::cache_span(c, false, purpose, s);
+  if (rc != DE_OK) return rc;
+  rc = de_route_topk(&m.moe, T, x, w.w_router, w.bias, ridx, rgate, lws, L.layer_bytes, s);
+  if (rc != DE_OK) return rc;
+  if (pred_out != nullptr &&
+      hipMemcpyAsync(pred_out, ridx, (size_t)T * k * 4, hipMemcpyDeviceToDevice, s) != hipSuccess)
+    return DE_ERR_HIP;
+  int32_t* hb = de::cache_readback(c);
+  if (hipMemcpyAsync(hb, ridx, (size_t)T * k * 4, hipMemcpyDeviceToHost, s) != hipSuccess ||
+      hipStreamSynchronize(s) != hipSuccess)
+    return DE_ERR_HIP;
+  for (int i = 0; i < T * k; ++i)
+    if (hb[i] < 0 || hb[i] >= N) return DE_ERR_INVALID;
+  de_expert_table tab;
+  if ((rc = de_cache_table(c, l, &tab)) != DE_OK) return rc;
+  const de_epilogue epi{h, normed_out, m.eps};
+  if (draft) {
+    const int32_t e1 = hb[0];
+    if ((rc = de_cache_ensure(c, l, &e1, 1, DE_NEED_DRAFT, s)) != DE_OK) return rc;
+    if ((rc = de_cache_prefetch(c, l, hb, k)) != DE_OK) return rc;
+    rc = de::layer_after_route(m.moe, 1, x, &tab, ridx, rgate, 1, w.shared_w, w.draft_w, w.gamma,
+                               h, &epi, true, true, nullptr, lws, L.layer_bytes, s);
+    if (rc != DE_OK) return rc;
+    if ((rc = de_cache_release(c, l, s)) != DE_OK) return rc;
+    return de::cache_span(c, true, purpose, s);
+  }
+  std::vector<uint8_t> in_union(N, 0);
+  for (int i = 0; i < T * k; ++i) in_union[hb[i]] = 1;
+  std::vector<int32_t> order;
+  for (int pass = 0; pass < 2; ++pass)
+    for (int e = 0; e < N; ++e)
+      if (in_union[e] && de::cache_resident(c, l, e) == (pass == 0)) order.push_back(e);
+  const int S = de::cache_slots_per_layer(c);
+  const int n = (int)order.size();
+  const int chunks = (n + S - 1) / S;
+  for (int ci = 0; ci < chunks; ++ci) {
+    const int lo = ci * S, cnt = std::min(S, n - lo);
+    if ((rc = de_cache_ensure(c, l, order.data() + lo, cnt, DE_NEED_VERIFY, s)) != DE_OK)
+      return rc;
+    rc = de::layer_after_route(m.moe, T, x, &tab, ridx, rgate, k, w.shared_w, nullptr, 0.f, h,
+                               &epi, ci == 0, ci == chunks - 1, n_union ? n_union + l : nullptr,
+                               lws, L.layer_bytes, s);
+    if (rc != DE_OK) return rc;
+    // The next chunk's copies may evict this chunk's members: they wait for
+    // the launches just enqueued.
+    if ((rc = de_cache_release(c, l, s)) != DE_OK) return rc;
+  }
+  return de::cache_span(c, true, purpose, s);
+}
+
 // Logits of T positions through the whole stack; the last MoE layer's fused
 // epilogue leaves RMSNorm(h) in the normed buffer, which the LM head reads.
+// With a cache the routed experts come through it (cached_layer).
 int forward(const de_model& m, int T, const int32_t* tokens, int mode, float* logits,
             const ArgmaxOut& am, int32_t* n_union, int32_t* pred_idx, size_t pred_stride,
-            void* ws, const ModelLayout& L, hipStream_t s) {
+            void* ws, const ModelLayout& L, hipStream_t s, de_cache* cache = nullptr) {
   const int H = m.moe.hidden;
   float* h = at<float>(ws, L.h);
   float* ncur = at<float>(ws, L.n0);
@@ -103,7 +186,11 @@ int forward(const de_model& m, int T, const int32_t* tokens, int mode, float* lo
   for (int l = 0; l < m.n_layers; ++l) {
     const de_layer_weights& w = m.layers[l];
     const de_epilogue epi{h, nnext, m.eps};
-    if (mode == DE_TARGET) {
+    if (cache != nullptr) {
+      rc = cached_layer(m, cache, l, T, mode == DE_DRAFT, ncur, h, nnext,
+                        mode == DE_TARGET ? n_union : nullptr,
+                        pred_idx ? pred_idx + l * pred_stride : nullptr, ws, L, s);
+    } else if (mode == DE_TARGET) {
       rc = de_verify_layer(&m.moe, T, ncur, w.w_router, w.bias, &w.routed, w.shared_w, h, nullptr,
                            nullptr, n_union ? n_union + l : nullptr, nullptr, nullptr, nullptr,
                            nullptr, nullptr, &epi, lws, L.layer_bytes, s);
@@ -213,6 +300,38 @@ int de_greedy_decode(const de_model* m, int n_steps, int32_t* tokens, void* ws, 
     if (rc != DE_OK) return rc;
   }
   return DE_OK;
+}
+
+int de_spec_step_cached(const de_model* m, de_cache* cache, int K, int32_t* block,
+                        int32_t* target_argmax, int32_t* out, int32_t* n_union, int32_t* pred_idx,
+                        void* ws, size_t ws_bytes, hipStream_t stream) {
+  int rc = de_check_model(m);
+  if (rc != DE_OK) return rc;
+  if (cache == nullptr || de::cache_layers(cache) != m->n_layers ||
+      de::cache_experts(cache) != m->moe.n_experts)
+    return DE_ERR_INVALID;
+  for (int l = 0; l < m->n_layers; ++l) {
+    de_expert_table tab;
+    if (de_cache_table(cache, l, &tab) != DE_OK || de::check_table(m->moe, &tab) != DE_OK)
+      return DE_ERR_INVALID;
+  }
+  if (K < 0 || K > 63 || block == nullptr || target_argmax == nullptr || out == nullptr)
+    return DE_ERR_INVALID;
+  if ((rc = check_block(*m, K + 1, ws, ws_bytes)) != DE_OK) return rc;
+  const ModelLayout L = model_layout(*m, K + 1);
+  float* logits = at<float>(ws, L.logits);
+  const size_t k = (size_t)m->moe.top_k;
+  if ((rc = de_cache_begin_block(cache)) != DE_OK) return rc;
+  for (int i = 0; i < K; ++i) {
+    const ArgmaxOut am{block + i + 1, at<int32_t>(ws, L.misc), nullptr};
+    rc = forward(*m, 1, block + i, DE_DRAFT, logits, am, nullptr,
+                 pred_idx ? pred_idx + (size_t)i * m->n_layers * k : nullptr, k, ws, L, stream,
+                 cache);
+    if (rc != DE_OK) return rc;
+  }
+  const ArgmaxOut am{target_argmax, out, K > 0 ? block + 1 : nullptr};
+  return forward(*m, K + 1, block, DE_TARGET, logits, am, n_union, nullptr, 0, ws, L, stream,
+                 cache);
 }
 
 }  // extern "C"

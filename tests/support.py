@@ -116,7 +116,10 @@ class OracleModel:
     def __init__(self, model: configs.ModelCfg):
         m = model.moe
         self.cfg = model
-        self.layers = [OracleLayer(m, l) for l in range(1, model.n_moe_layers + 1)]
+        self.layers = [
+            OracleLayer(m, l, bias=gen.zipf_bias(model, l, model.zipf_lam) if model.zipf_s > 0
+                        else None)
+            for l in range(1, model.n_moe_layers + 1)]
         emb = gen.embedding(model)
         dense = moe.split_expert(gen.dense_block(model), model.dense_inter, m.hidden)
         lm = moe.to_f64(gen.lm_head(model.cfg_id, model.vocab, m.hidden, model.lm_std))

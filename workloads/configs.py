@@ -71,6 +71,7 @@ class ModelCfg:
     lm_std: float = 0.02
     eps: float = 1e-6
     zipf_s: float = 0.0     # 0 = no popularity skew
+    zipf_lam: float = 0.0   # scale of the Zipf router bias (tests/golden/calibrate_zipf.py)
     cache_slots: int = 0    # 0 = every expert resident in HBM
 
 
@@ -110,7 +111,7 @@ CFG4 = ModelCfg(
 # 16 HBM cache slots per layer over a pinned host pool.
 CFG5 = ModelCfg(
     name="v2lite-offload", cfg_id=5, moe=replace(CFG2, cfg_id=5), n_moe_layers=26,
-    dense_inter=10944, vocab=102400, k_draft=16, zipf_s=1.1, cache_slots=16,
+    dense_inter=10944, vocab=102400, k_draft=16, zipf_s=1.1, zipf_lam=2.7449, cache_slots=16,
 )
 
 

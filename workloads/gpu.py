@@ -107,6 +107,8 @@ def model_tensors(model: ModelCfg, device="cuda", redraw: int = 0) -> dict:
     layers = []
     for l in range(1, model.n_moe_layers + 1):
         b = gen.router_bias(m, l, redraw)
+        if model.zipf_s > 0:
+            b = gen.zipf_bias(model, l, model.zipf_lam, redraw)
         layers.append(dict(
             router=router(m, l, device, redraw),
             bias=None if b is None else to_device(b, device),
