@@ -76,6 +76,9 @@ def parse():
     p.add_argument("--no-full-step", action="store_true",
                    help="skip the 26-layer draft+verify step measurement")
     p.add_argument("--full-steps", type=int, default=12)
+    p.add_argument("--no-offload", action="store_true",
+                   help="skip the expert-cache (offload) step measurement")
+    p.add_argument("--offload-steps", type=int, default=3)
     return p.parse_args()
 
 
@@ -213,6 +216,7 @@ def main():
     dn_gbs = float(dn_bytes.sum() / (sum(dn_ms) * 1e-3) / 1e9)
 
     full = None if args.no_full_step else full_step(args, de, configs, gen, wgpu, torch, np)
+    offload = None if args.no_offload else offload_step(args, de, configs, gen, wgpu, torch, np)
 
     probe_gbs = None
     if not args.no_probe:
@@ -283,6 +287,7 @@ def main():
             "algorithmic_bytes_per_launch": int(round(float(gu_bytes.mean()))),
         },
         "full_step": full,
+        "offload_step": offload,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
@@ -377,6 +382,94 @@ def full_step(args, de, configs, gen, wgpu, torch, np):
         "weights_fill_s": round(fill_s, 2),
     }
     del dm, t
+    torch.cuda.empty_cache()
+    return res
+
+
+def offload_step(args, de, configs, gen, wgpu, torch, np):
+    """The skewed-routing offload workload: the 26-layer stack with Zipf(1.1)
+    router biases, K = 16, routed experts in pinned host memory behind a
+    16-slot HBM cache per layer.  One cold step, then warm steps back to back
+    (each continuing from the previous bonus token); the cache counts of the
+    warm steps are reported."""
+    model = configs.CFG5
+    m = model.moe
+    K, Lyr, N, V = model.k_draft, model.n_moe_layers, m.n_experts, model.vocab
+    dev = "cuda"
+    t = wgpu.model_tensors(model, dev)
+    desc = de.make_desc(m.hidden, m.n_experts, m.top_k, m.inter, m.shared_inter, m.draft_inter,
+                        m.score_func, m.norm_topk, m.routed_scale, m.wdtype)
+    eb = m.expert_bytes()
+    host = torch.empty(Lyr * N * eb, dtype=torch.uint8, pin_memory=True)
+    hv = host.view(Lyr, N, eb)
+    for l in range(Lyr):
+        hv[l].copy_(t["layers"][l]["routed"].view(torch.uint8).view(N, eb))
+        t["layers"][l]["routed"] = None  # the device copy is dropped: experts live in host memory
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    # The resident tables are never read by the cached step; a placeholder slot
+    # table keeps the model description valid.
+    cache = de.ExpertCache(Lyr, N, model.cache_slots, eb, host, device=dev)
+    layers = []
+    for l in range(Lyr):
+        d = dict(t["layers"][l])
+        d["table"] = cache.table(l)
+        layers.append(d)
+    dm = de.DeviceModel(desc, layers, V, t["emb"], t["lm"], t["dense"], model.dense_inter,
+                        de.DE_BF16, model.eps, m.gamma, K + 1, dev)
+    S = args.offload_steps
+    blocks = torch.zeros(S + 1, K + 1, dtype=torch.int32, device=dev)
+    amax = torch.empty(S + 1, K + 1, dtype=torch.int32, device=dev)
+    outs = torch.empty(S + 1, 2, dtype=torch.int32, device=dev)
+    nus = torch.empty(S + 1, Lyr, dtype=torch.int32, device=dev)
+    blocks[0, 0] = gen.start_token(model)
+
+    def run(i):
+        de.de_spec_step_cached(dm.model, cache, K, blocks[i], amax[i], outs[i], nus[i], None,
+                               dm.ws)
+        if i + 1 <= S:
+            blocks[i + 1, :1].copy_(outs[i, 1:])
+
+    t_cold = time.perf_counter()
+    run(0)  # cold
+    torch.cuda.synchronize()
+    cold_ms = 1e3 * (time.perf_counter() - t_cold)
+    cold = cache.stats()
+    cache_t0 = time.perf_counter()
+    base = cache.stats()
+    for i in range(1, S + 1):
+        run(i)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - cache_t0
+    st = cache.stats()
+    d = {k: st[k] - base[k] for k in st}
+    o = outs[1:].cpu().numpy()
+    nu = nus[1:].cpu().numpy().astype(np.float64)
+    res = {
+        "workload": "v2lite-offload-K16: dense layer 0 + 26 V2-Lite MoE layers with Zipf(1.1) "
+                    "router biases, K=16 drafts, 17-position verify block, routed experts "
+                    "(28.8 GB) in pinned host memory, 16 HBM slots per layer, draft-router "
+                    "prefetch; random weights",
+        "steps": S,
+        "ms_per_step": round(1e3 * wall / S, 2),
+        "tokens_per_s": round(float((o[:, 0] + 1).sum()) / wall, 2),
+        "accept_mean": round(float(o[:, 0].mean()), 3),
+        "union_mean_per_layer": round(float(nu.mean()), 2),
+        "prefetch_hit_rate": round(d["prefetch_used"] / max(1, d["prefetch_issued"]), 4),
+        "prefetch_waste_rate": round(d["prefetch_wasted"] / max(1, d["prefetch_issued"]), 4),
+        "verify_coverage": round(d["verify_hits"] / max(1, d["verify_needed"]), 4),
+        "draft_top1_hit_rate": round(d["draft_hits"] / max(1, d["draft_needed"]), 4),
+        "stall_us_per_step": round(d["stall_us"] / S, 1),
+        "verify_layer_us": round(d["verify_layer_us"] / max(1, d["verify_layers"]), 1),
+        "draft_layer_us": round(d["draft_layer_us"] / max(1, d["draft_layers"]), 1),
+        "host_to_hbm_gb_per_step": round(d["bytes_copied"] / S / 1e9, 3),
+        "host_to_hbm_gbs": round(d["bytes_copied"] / wall / 1e9, 2),
+        "counts": {k: d[k] for k in de.CACHE_COUNTS},
+        "cold_step_ms": round(cold_ms, 2),
+        "cold_bytes_gb": round(cold["bytes_copied"] / 1e9, 3),
+    }
+    cache.close()
+    del dm, t, host
     torch.cuda.empty_cache()
     return res
 
