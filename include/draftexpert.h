@@ -95,6 +95,9 @@ typedef struct de_epilogue {
 
 int de_abi_version(void);
 const char* de_error_string(int code);
+/* The HIP runtime's message for the last failed HIP call the library saw on
+ * this host thread ("" if none): the detail behind DE_ERR_HIP. */
+const char* de_hip_error_detail(void);
 
 /* Host-only validation of a layer descriptor (DE_OK or an error code). */
 int de_check_desc(const de_moe_desc* d);

@@ -25,7 +25,7 @@ DE_F32 = 0
 DE_BF16 = 1
 
 C_FUNCS = [
-    "de_abi_version", "de_error_string", "de_check_desc", "de_workspace_bytes",
+    "de_abi_version", "de_error_string", "de_hip_error_detail", "de_check_desc", "de_workspace_bytes",
     "de_workspace_init", "de_route_topk",
     "de_expert_union", "de_grouped_swiglu", "de_draft_layer", "de_verify_layer", "de_accept_workspace_bytes", "de_accept_len",
     "de_lm_head", "de_rmsnorm", "de_embed_gather", "de_dense_workspace_bytes", "de_dense_swiglu",
@@ -107,7 +107,7 @@ class CacheCounts(ctypes.Structure):
         ("verify_layer_us", ctypes.c_double)]
 
 
-def _load(path: str = LIB_PATH):
+def _load(path: str = LIB_PATH, strict: bool = True):
     if not os.path.exists(path):
         raise ImportError(f"{path} is missing: build it with `python paper_2607_24434_amd/build.py`")
     lib = ctypes.CDLL(path)
@@ -125,6 +125,7 @@ def _load(path: str = LIB_PATH):
     sig = {
         "de_abi_version": (I, []),
         "de_error_string": (ctypes.c_char_p, [I]),
+        "de_hip_error_detail": (ctypes.c_char_p, []),
         "de_check_desc": (I, [DP]),
         "de_workspace_bytes": (SZ, [DP, I]),
         "de_workspace_init": (I, [P, SZ, P]),
@@ -160,6 +161,8 @@ def _load(path: str = LIB_PATH):
         "de_spec_step_cached": (I, [MP, P, I, P, P, P, P, P, P, SZ, P]),
     }
     for name, (res, args) in sig.items():
+        if not strict and not hasattr(lib, name):
+            continue
         fn = getattr(lib, name)
         fn.restype = res
         fn.argtypes = args
@@ -185,7 +188,10 @@ def _stream(stream):
 
 def _check(fn: str, rc: int):
     if rc != 0:
-        raise DEError(fn, rc, LIB.de_error_string(rc).decode())
+        msg = LIB.de_error_string(rc).decode()
+        if rc == -3:
+            msg += f" ({LIB.de_hip_error_detail().decode()})"
+        raise DEError(fn, rc, msg)
 
 
 def make_desc(hidden, n_experts, top_k, inter, shared_inter, draft_inter, score_func, norm_topk,

@@ -37,6 +37,13 @@ int check_table(const de_moe_desc& d, const de_expert_table* t) {
   return DE_OK;
 }
 
+thread_local hipError_t t_last_hip = hipSuccess;
+
+hipError_t note_hip(hipError_t e) {
+  if (e != hipSuccess) t_last_hip = e;
+  return e;
+}
+
 }  // namespace de
 
 namespace {
@@ -116,7 +123,7 @@ int check_epi(const de_epilogue* epi) {
   return DE_OK;
 }
 
-int hip_status(hipError_t e) { return e == hipSuccess ? DE_OK : DE_ERR_HIP; }
+int hip_status(hipError_t e) { return de::note_hip(e) == hipSuccess ? DE_OK : DE_ERR_HIP; }
 
 // Router logits (into the workspace) and the ordered top-k lists of every
 // position; the layer calls build the union in their gate/up kernel.
@@ -327,6 +334,10 @@ int layer_after_route(const de_moe_desc& d, int T, const float* x, const de_expe
 extern "C" {
 
 int de_abi_version(void) { return DE_ABI_VERSION; }
+
+const char* de_hip_error_detail(void) {
+  return de::t_last_hip == hipSuccess ? "" : hipGetErrorString(de::t_last_hip);
+}
 
 const char* de_error_string(int code) {
   switch (code) {

@@ -26,23 +26,37 @@ __device__ __forceinline__ float row16_sum(float v) {
   return v;
 }
 
-// Sum / max over the 64 lanes: four DPP steps inside each 16-lane row, then two
-// cross-row shuffles; every lane receives the same bits.
+// Whole-wave reductions without LDS: the 16-lane row steps above, then
+// row_bcast:15 (rows 1 and 3 take the row below's lane 15) and row_bcast:31
+// (rows 2 and 3 take lane 31), which leaves the total in lane 63; readlane
+// hands it to every lane.  A sum pairs the rows as (r3 + r2) + (r1 + r0).
 __device__ __forceinline__ float wave_sum(float v) {
   v = row16_sum(v);
-  v += __shfl_xor(v, 16, kWave);
-  v += __shfl_xor(v, 32, kWave);
-  return v;
+  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x142, 0xA, 0xF, false));
+  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x143, 0xC, 0xF, false));
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
 }
 
 __device__ __forceinline__ float wave_max(float v) {
-  v = fmaxf(v, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0xB1, 0xF, 0xF, false)));
-  v = fmaxf(v, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x4E, 0xF, 0xF, false)));
-  v = fmaxf(v, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x141, 0xF, 0xF, false)));
-  v = fmaxf(v, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x140, 0xF, 0xF, false)));
-  v = fmaxf(v, __shfl_xor(v, 16, kWave));
-  v = fmaxf(v, __shfl_xor(v, 32, kWave));
-  return v;
+  const int ni = __float_as_int(-INFINITY);
+  v = fmaxf(v, __int_as_float(__builtin_amdgcn_update_dpp(ni, __float_as_int(v), 0xB1, 0xF, 0xF, false)));
+  v = fmaxf(v, __int_as_float(__builtin_amdgcn_update_dpp(ni, __float_as_int(v), 0x4E, 0xF, 0xF, false)));
+  v = fmaxf(v, __int_as_float(__builtin_amdgcn_update_dpp(ni, __float_as_int(v), 0x141, 0xF, 0xF, false)));
+  v = fmaxf(v, __int_as_float(__builtin_amdgcn_update_dpp(ni, __float_as_int(v), 0x140, 0xF, 0xF, false)));
+  v = fmaxf(v, __int_as_float(__builtin_amdgcn_update_dpp(ni, __float_as_int(v), 0x142, 0xA, 0xF, false)));
+  v = fmaxf(v, __int_as_float(__builtin_amdgcn_update_dpp(ni, __float_as_int(v), 0x143, 0xC, 0xF, false)));
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
+}
+
+__device__ __forceinline__ int wave_min_i32(int v) {
+  const int big = 0x7fffffff;
+  v = min(v, __builtin_amdgcn_update_dpp(big, v, 0xB1, 0xF, 0xF, false));
+  v = min(v, __builtin_amdgcn_update_dpp(big, v, 0x4E, 0xF, 0xF, false));
+  v = min(v, __builtin_amdgcn_update_dpp(big, v, 0x141, 0xF, 0xF, false));
+  v = min(v, __builtin_amdgcn_update_dpp(big, v, 0x140, 0xF, 0xF, false));
+  v = min(v, __builtin_amdgcn_update_dpp(big, v, 0x142, 0xA, 0xF, false));
+  v = min(v, __builtin_amdgcn_update_dpp(big, v, 0x143, 0xC, 0xF, false));
+  return __builtin_amdgcn_readlane(v, 63);
 }
 
 __device__ __forceinline__ float silu_f(float v) { return v / (1.0f + expf(-v)); }
@@ -143,9 +157,9 @@ struct GroupedArgs {
   int n_dense;
   DenseSrc dense[3];
   int lds_floats;      // set by the launcher: staged-input capacity of a block
-  // Gate/up only: recompute the top-k and the union from sel.z in every block
-  // (block 0 also writes sel's outputs); r.n_union ... r.gate_list are then
-  // not read.
+  // Gate/up only: build the union from the top-k lists sel.idx_out /
+  // sel.gate_out in every block (block 0 also writes sel's union outputs);
+  // r.n_union ... r.gate_list are then not read.
   int fuse_route;
   TopkUnionArgs sel;
 };
@@ -158,6 +172,10 @@ struct DevInfo {
 };
 const DevInfo& dev_info();
 
+// Records a failed HIP call for de_hip_error_detail (per host thread) and
+// returns its code.
+hipError_t note_hip(hipError_t e);
+
 
 // Router logits and top-k of every position (one block per position).
 struct RouteArgs {
@@ -165,14 +183,16 @@ struct RouteArgs {
   const float* x;          // [T, H]
   const float* w;          // [N, H] fp32 router
   int H;
-  float* z;                // [T, N] logits out, or NULL
-  unsigned* counter;       // [T] arrival counters, zero between calls (split launch)
+  float* z;                // [T, N] logits out (each position's last block reads them back)
+  unsigned* counter;       // [T] arrival counters, zero between calls
 };
 hipError_t launch_route(const RouteArgs& r, hipStream_t s);
 // Union only, from caller-supplied lists (sel.idx_in / sel.gate_in).
 hipError_t launch_union(const TopkUnionArgs& a, hipStream_t s);
 
 hipError_t launch_gateup(const GroupedArgs& a, int wdtype, hipStream_t s);
+// Raises a kernel's dynamic LDS limit to `lds` bytes when above the default.
+hipError_t allow_lds(const void* fn, size_t lds);
 hipError_t launch_down(const GroupedArgs& a, int wdtype, hipStream_t s);
 
 

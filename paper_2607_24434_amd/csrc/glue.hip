@@ -166,18 +166,18 @@ int accept_chunks(int V) { return (V + kAmChunk - 1) / kAmChunk; }
 hipError_t launch_argmax_accept(const AcceptArgs& a, hipStream_t s) {
   hipLaunchKernelGGL(argmax_accept_kernel, dim3(accept_chunks(a.V), a.K + 1), dim3(kAmThreads), 0,
                      s, a);
-  return hipGetLastError();
+  return note_hip(hipGetLastError());
 }
 
 hipError_t launch_rmsnorm(int T, int H, const float* x, float eps, float* out, hipStream_t s) {
   hipLaunchKernelGGL(rmsnorm_kernel, dim3(T), dim3(256), 0, s, H, x, eps, out);
-  return hipGetLastError();
+  return note_hip(hipGetLastError());
 }
 
 hipError_t launch_embed(int T, int H, int V, const int32_t* tokens, const uint16_t* emb, float* h,
                         float* normed, float eps, hipStream_t s) {
   hipLaunchKernelGGL(embed_kernel, dim3(T), dim3(256), 0, s, H, V, tokens, emb, h, normed, eps);
-  return hipGetLastError();
+  return note_hip(hipGetLastError());
 }
 
 hipError_t launch_stream_probe(const void* buf, size_t bytes, float* sink, hipStream_t s) {
@@ -185,7 +185,7 @@ hipError_t launch_stream_probe(const void* buf, size_t bytes, float* sink, hipSt
   const int grid = dev_info().num_cus * 8;
   hipLaunchKernelGGL(stream_probe_kernel, dim3(grid), dim3(256), 0, s,
                      static_cast<const u32x4*>(buf), n, sink);
-  return hipGetLastError();
+  return note_hip(hipGetLastError());
 }
 
 }  // namespace de

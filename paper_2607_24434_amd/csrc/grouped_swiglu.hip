@@ -31,6 +31,10 @@
 #include "de_common.h"
 #include "topk_union.h"
 
+#include <mutex>
+#include <utility>
+#include <vector>
+
 // Build-time tuning knobs (kept at the measured best by default).
 #ifndef DE_NT_LOADS
 #define DE_NT_LOADS 1
@@ -173,12 +177,7 @@ __device__ __forceinline__ void stage_rows_at(float* dst, const float* g, int gs
 
 // Total of a per-lane partial over the 64 lanes of a wave; every lane receives
 // the same bits.
-__device__ __forceinline__ float row_total(float v) {
-  v = row16_sum(v);
-  v += __shfl_xor(v, 16, kWave);
-  v += __shfl_xor(v, 32, kWave);
-  return v;
-}
+__device__ __forceinline__ float row_total(float v) { return wave_sum(v); }
 
 __host__ __device__ __forceinline__ int cdiv(int a, int b) { return (a + b - 1) / b; }
 
@@ -885,18 +884,17 @@ int occupancy_blocks(K kernel, size_t lds) {
 template <typename K>
 hipError_t launch_persistent(K kernel, int max_tiles, size_t lds, const GroupedArgs& a,
                              hipStream_t s) {
-  static bool attr_set = false;
-  if (!attr_set) {
-    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(kernel),
-                              hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
-    attr_set = true;
+  const hipError_t e = allow_lds(reinterpret_cast<const void*>(kernel), lds);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();  // the failure is returned here, not left for a later check
+    return note_hip(e);
   }
   const int occ = occupancy_blocks(kernel, lds);
   const int cap = dev_info().num_cus * occ;
   const int want = cdiv(max_tiles, kWavesPB);
   const int g = want < 1 ? 1 : (want < cap ? want : cap);
   hipLaunchKernelGGL(kernel, dim3(g), dim3(kBlock), lds, s, a);
-  return hipGetLastError();
+  return note_hip(hipGetLastError());
 }
 
 int max_tiles(const GroupedArgs& a, bool gateup) {
@@ -939,6 +937,23 @@ hipError_t down_typed(GroupedArgs a, hipStream_t s) {
 
 }  // namespace
 
+// Raises a kernel's dynamic LDS limit to `lds` when a launch needs more than
+// the default 64 KB (once per kernel and size; the limit counts the kernel's
+// static LDS too, so the request is the exact size, never a blanket maximum).
+hipError_t allow_lds(const void* fn, size_t lds) {
+  if (lds <= 64 * 1024) return hipSuccess;
+  static std::mutex mu;
+  static std::vector<std::pair<const void*, size_t>> granted;
+  std::lock_guard<std::mutex> lock(mu);
+  for (auto& g : granted)
+    if (g.first == fn && g.second >= lds) return hipSuccess;
+  const hipError_t e =
+      hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (e != hipSuccess) return e;
+  granted.emplace_back(fn, lds);
+  return hipSuccess;
+}
+
 hipError_t launch_gateup(const GroupedArgs& a, int wdtype, hipStream_t s) {
   return wdtype == 1 ? gateup_typed<uint16_t>(a, s) : gateup_typed<float>(a, s);
 }
@@ -949,7 +964,7 @@ hipError_t launch_down(const GroupedArgs& a, int wdtype, hipStream_t s) {
 
 hipError_t launch_combine(const CombineArgs& a, hipStream_t s) {
   hipLaunchKernelGGL(combine_kernel, dim3(a.T), dim3(kCombThreads), 0, s, a);
-  return hipGetLastError();
+  return note_hip(hipGetLastError());
 }
 
 }  // namespace de

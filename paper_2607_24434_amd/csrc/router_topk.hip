@@ -2,9 +2,9 @@
 // launch, and the standalone union launch (Eq. 2, Eq. 3).
 //
 // route_split_kernel: (position, 16 experts) blocks compute the logits; the
-//   last block of each position selects its ordered top-k (selection device
-//   functions shared with the grouped gate/up kernel, whose prologue builds
-//   the union from the lists in every block in the layer calls).
+//   last block of each position selects its ordered top-k (the grouped
+//   gate/up kernel's prologue then builds the union from the lists in every
+//   block).
 // union_kernel: the union from caller-supplied top-k lists.
 #include "de_common.h"
 #include "topk_union.h"
@@ -98,69 +98,6 @@ __global__ __launch_bounds__(kRsThreads) void route_split_kernel(RouteArgs r) {
   }
 }
 
-// Block t: the logits of position t for all N experts (x_t staged in LDS;
-// wave w dots the router rows w, w+16, ..., two rows per round with all their
-// loads in flight), then the ordered top-k from the logits in LDS.  No
-// cross-block step; one CU streams the whole router.
-__global__ __launch_bounds__(kRsThreads) void route_select_kernel(RouteArgs r) {
-  __shared__ float zrow[kMaxN];
-  __shared__ int32_t lidx[kMaxK];
-  __shared__ float lsc[kMaxK];
-  extern __shared__ __align__(16) float4 s_x4[];
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int t = blockIdx.x;
-  const int H4 = r.H >> 2, N = r.sel.N, k = r.sel.k;
-  const float4* xg = reinterpret_cast<const float4*>(r.x) + (size_t)t * H4;
-  const float4* w4 = reinterpret_cast<const float4*>(r.w);
-  for (int i = threadIdx.x; i < H4; i += kRsThreads) s_x4[i] = xg[i];
-  __syncthreads();
-  for (int e0 = wave; e0 < N; e0 += 2 * kRsWaves) {
-    const int e1 = e0 + kRsWaves;
-    const bool has1 = e1 < N;
-    float acc0 = 0.f, acc1 = 0.f;
-    for (int h0 = 0; h0 < H4; h0 += kWave * 8) {
-      float4 v0[8], v1[8];
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const int h = min(h0 + lane + j * kWave, H4 - 1);  // clamped: in bounds, skipped below
-        v0[j] = w4[(size_t)e0 * H4 + h];
-        v1[j] = w4[(size_t)(has1 ? e1 : e0) * H4 + h];
-      }
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const int h = h0 + lane + j * kWave;
-        if (h < H4) {
-          const float4 xv = s_x4[h];
-          acc0 = fmaf(v0[j].x, xv.x, acc0);
-          acc0 = fmaf(v0[j].y, xv.y, acc0);
-          acc0 = fmaf(v0[j].z, xv.z, acc0);
-          acc0 = fmaf(v0[j].w, xv.w, acc0);
-          acc1 = fmaf(v1[j].x, xv.x, acc1);
-          acc1 = fmaf(v1[j].y, xv.y, acc1);
-          acc1 = fmaf(v1[j].z, xv.z, acc1);
-          acc1 = fmaf(v1[j].w, xv.w, acc1);
-        }
-      }
-    }
-    acc0 = wave_sum(acc0);
-    acc1 = wave_sum(acc1);
-    if (lane == 0) {
-      zrow[e0] = acc0;
-      if (has1) zrow[e1] = acc1;
-    }
-  }
-  __syncthreads();
-  if (wave == 0) topk_row(r.sel, zrow, lidx, lsc);
-  __syncthreads();
-  if (threadIdx.x < k) {
-    const int i = t * k + threadIdx.x;
-    r.sel.idx_out[i] = lidx[threadIdx.x];
-    r.sel.gate_out[i] = topk_gate(r.sel, lsc, threadIdx.x);
-  }
-  if (r.z != nullptr)
-    for (int e = threadIdx.x; e < N; e += kRsThreads) r.z[(size_t)t * N + e] = zrow[e];
-}
-
 __global__ __launch_bounds__(kSelThreads) void union_kernel(TopkUnionArgs a) {
   __shared__ SelShared sel;
   const SelView v = view_of(sel);
@@ -174,23 +111,18 @@ __global__ __launch_bounds__(kSelThreads) void union_kernel(TopkUnionArgs a) {
 
 }  // namespace
 
-// Split launch for small blocks (one CU streaming the whole router is the
-// bottleneck there) and for rows too long to stage; one block per position
-// otherwise (no cross-block step).
+// Grid (T, ceil(N / 16)): every (position, 16 experts) pair in its own block,
+// so all the router rows of a position stream in parallel and each position's
+// selection runs in its own last block.
 hipError_t launch_route(const RouteArgs& r, hipStream_t s) {
-  if (r.sel.T <= 8 || (size_t)r.H * sizeof(float) > 64 * 1024) {
-    const dim3 grid(r.sel.T, (r.sel.N + kRsWaves - 1) / kRsWaves);
-    hipLaunchKernelGGL(route_split_kernel, grid, dim3(kRsThreads), 0, s, r);
-  } else {
-    hipLaunchKernelGGL(route_select_kernel, dim3(r.sel.T), dim3(kRsThreads),
-                       (size_t)r.H * sizeof(float), s, r);
-  }
-  return hipGetLastError();
+  const dim3 grid(r.sel.T, (r.sel.N + kRsWaves - 1) / kRsWaves);
+  hipLaunchKernelGGL(route_split_kernel, grid, dim3(kRsThreads), 0, s, r);
+  return note_hip(hipGetLastError());
 }
 
 hipError_t launch_union(const TopkUnionArgs& a, hipStream_t s) {
   hipLaunchKernelGGL(union_kernel, dim3(1), dim3(kSelThreads), 0, s, a);
-  return hipGetLastError();
+  return note_hip(hipGetLastError());
 }
 
 }  // namespace de

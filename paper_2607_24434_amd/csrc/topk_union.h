@@ -1,14 +1,11 @@
 // Top-k selection with gates (Eq. 1, Eq. 4) and the block union with
-// per-expert position lists (Eq. 2, Eq. 3), as block-level device functions
-// over LDS arrays.  Used by the standalone selection kernel and by the
-// prologue of the grouped gate/up kernel, which recomputes them in every block
-// from the router logits instead of waiting for a separate launch.
+// per-expert position lists (Eq. 2, Eq. 3), as device functions over LDS
+// arrays.  The routing launch selects; the union kernel and the prologue of
+// the grouped gate/up kernel (in every block, from the selected lists) build
+// the union.
 //
-// Selection: one wave per position.  Lane l holds the candidates l, l+64, ...
-// (N <= 256); a candidate's rank is the number of candidates with a larger key
-// (ties to the lower id), counted against every key broadcast with readlane,
-// so no chain of cross-lane shuffles is needed.  Rank < k places it in the
-// ordered list.  Gates are normalised in list order.
+// Selection: one wave per position, k rounds of a wave-wide argmax (largest
+// key, ties to the lower id).  Gates are normalised in list order.
 //
 // Union: integer work only.  Every (position, slot) entry sets its position
 // bit in the expert's 64-bit mask with an LDS atomic OR (a bit already set
@@ -18,6 +15,8 @@
 #pragma once
 
 #include "de_common.h"
+
+#include <climits>
 
 namespace de {
 
@@ -52,20 +51,24 @@ __device__ inline SelView sel_view_at(char* p, int T, int k, int N) {
 }
 
 // Ordered top-k of position t from its N logits zrow (one wave; zrow may be
-// in LDS or global memory): ids into idx[0..k), scores into sc[0..k).
+// in LDS or global memory): ids into idx[0..k), scores into sc_out[0..k).
+// Lane l holds the candidates l, l + 64, ... (N <= 256).  Each of the k rounds
+// takes the largest remaining key, ties to the lower id: every lane offers
+// its best remaining candidate, a wave max finds the key, a wave min the
+// lowest id offering it, and the owning lane records and retires it.  A NaN
+// key counts as -inf; a candidate id >= N never competes.
 __device__ inline void topk_row(const TopkUnionArgs& a, const float* zrow, int32_t* idx,
                                 float* sc_out) {
   const int lane = threadIdx.x & 63;
   const int N = a.N, k = a.k;
-  const int nq = (N + kWave - 1) / kWave;  // candidates per lane (<= 4)
   float key[4], sc[4];
-  bool valid[4];
+  bool left[4];
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
     const int e = lane + q * kWave;
-    valid[q] = q < nq && e < N;
-    const float zz = valid[q] ? zrow[e] : 0.f;
-    const float b = (valid[q] && a.bias != nullptr) ? a.bias[e] : 0.f;
+    left[q] = e < N;
+    const float zz = left[q] ? zrow[e] : 0.f;
+    const float b = (left[q] && a.bias != nullptr) ? a.bias[e] : 0.f;
     float kk, sv;
     if (a.score_func == 0) {  // softmax(z + b): key z + b
       kk = zz + b;
@@ -75,47 +78,47 @@ __device__ inline void topk_row(const TopkUnionArgs& a, const float* zrow, int32
       kk = sv + b;
     }
     if (!(kk == kk)) kk = -INFINITY;  // a NaN never wins
-    key[q] = valid[q] ? kk : -INFINITY;
+    key[q] = left[q] ? kk : -INFINITY;
     sc[q] = sv;
   }
   if (a.score_func == 0) {
     float m = -INFINITY;
 #pragma unroll
     for (int q = 0; q < 4; ++q)
-      if (valid[q]) m = fmaxf(m, key[q]);
+      if (left[q]) m = fmaxf(m, key[q]);
     m = wave_max(m);
     float ex[4], sum = 0.f;
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      ex[q] = valid[q] ? expf(key[q] - m) : 0.f;
+      ex[q] = left[q] ? expf(key[q] - m) : 0.f;
       sum += ex[q];
     }
     sum = wave_sum(sum);
 #pragma unroll
     for (int q = 0; q < 4; ++q) sc[q] = ex[q] / sum;
   }
-  // rank[q] = number of candidates that beat candidate (key[q], id).
-  int rank[4] = {0, 0, 0, 0};
+  for (int j = 0; j < k; ++j) {
+    float bk = -INFINITY;
+    int bid = INT_MAX;
 #pragma unroll
-  for (int q2 = 0; q2 < 4; ++q2) {
-    if (q2 >= nq) break;
-    const int n2 = min(kWave, N - q2 * kWave);
-    for (int l = 0; l < n2; ++l) {
-      const float kb = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(key[q2]), l));
-      const int eb = q2 * kWave + l;
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        if (q >= nq) break;
-        const int e = lane + q * kWave;
-        rank[q] += (kb > key[q] || (kb == key[q] && eb < e)) ? 1 : 0;
+    for (int q = 0; q < 4; ++q) {
+      const int e = lane + q * kWave;
+      if (left[q] && (key[q] > bk || (key[q] == bk && e < bid))) {
+        bk = key[q];
+        bid = e;
       }
     }
-  }
+    const float m = wave_max(bk);
+    const int win = wave_min_i32(bk == m ? bid : INT_MAX);
+    if (bid == win) {
 #pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    if (valid[q] && rank[q] < k) {
-      idx[rank[q]] = lane + q * kWave;
-      sc_out[rank[q]] = sc[q];
+      for (int q = 0; q < 4; ++q) {
+        if (q == (win >> 6)) {
+          left[q] = false;
+          idx[j] = win;
+          sc_out[j] = sc[q];
+        }
+      }
     }
   }
 }
@@ -130,25 +133,6 @@ __device__ inline float topk_gate(const TopkUnionArgs& a, const float* sc, int j
     g = g / gsum;
   }
   return g * a.routed_scale;
-}
-
-// Top-k of every position from the logits a.z [T, N] into s.idx / s.gate;
-// with write_out also into a.idx_out / a.gate_out.  All threads of the block;
-// ends with a barrier.
-__device__ inline void select_topk(const TopkUnionArgs& a, const SelView& s, bool write_out) {
-  const int wave = threadIdx.x >> 6;
-  const int nwaves = blockDim.x >> 6;
-  const int T = a.T, N = a.N, k = a.k;
-  for (int t = wave; t < T; t += nwaves) topk_row(a, a.z + (size_t)t * N, s.idx + t * k, s.sc + t * k);
-  __syncthreads();
-  for (int i = threadIdx.x; i < T * k; i += blockDim.x) {
-    const int t = i / k;
-    const float g = topk_gate(a, s.sc + t * k, i - t * k);
-    s.gate[i] = g;
-    if (write_out && a.idx_out) a.idx_out[i] = s.idx[i];
-    if (write_out && a.gate_out) a.gate_out[i] = g;
-  }
-  __syncthreads();
 }
 
 // Union of the first a.ucols entries of every position's list in s.idx /
