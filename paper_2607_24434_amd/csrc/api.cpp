@@ -128,9 +128,11 @@ int hip_status(hipError_t e) { return de::note_hip(e) == hipSuccess ? DE_OK : DE
 // Router logits (into the workspace) and the ordered top-k lists of every
 // position; the layer calls build the union in their gate/up kernel.
 hipError_t route(const de_moe_desc& d, int T, const float* x, const float* w_router,
-                 const Layout& L, void* ws, const de::TopkUnionArgs& sel, hipStream_t s) {
+                 const Layout& L, void* ws, const de::TopkUnionArgs& sel, hipStream_t s,
+                 bool select = true) {
   de::RouteArgs r{};
   r.sel = sel;
+  r.select = select ? 1 : 0;
   r.x = x;
   r.w = w_router;
   r.H = d.hidden;
@@ -191,11 +193,12 @@ int run_grouped(const de_moe_desc& d, int T, const float* x, const de::RoutedSrc
                 const int32_t* pair_pos, int kk, const void* shared_w, const void* draft_w,
                 float gamma, float* y, const de_epilogue* epi, const Layout& L, void* ws,
                 const de::TopkUnionArgs* fused_sel, hipStream_t s, bool dense_on = true,
-                bool combine_on = true) {
+                bool combine_on = true, bool fuse_select = false) {
   const size_t esz = elem_bytes(d.wdtype);
   de::GroupedArgs g{};
   if (fused_sel != nullptr) {
     g.fuse_route = 1;
+    g.fuse_select = fuse_select ? 1 : 0;
     g.sel = *fused_sel;
   }
   g.T = T;
@@ -485,11 +488,12 @@ int de_draft_layer(const de_moe_desc* d, int T, const float* x, const float* w_r
   a.gate_list = at<float>(ws, L.glist);
   a.pair_pos = at<int32_t>(ws, L.ppos);
   a.z = at<float>(ws, L.z);
-  if (route(*d, T, x, w_router, L, ws, a, stream) != hipSuccess) return DE_ERR_HIP;
+  // Logits only; the gate/up prologue selects the top-k in every block.
+  if (route(*d, T, x, w_router, L, ws, a, stream, false) != hipSuccess) return DE_ERR_HIP;
   const de::RoutedSrc r = routed_src(*d, T, routed, a.n_union, a.union_ids, a.offsets, a.tok_list,
                                      a.gate_list, at<float>(ws, L.a_r), at<float>(ws, L.p_r));
   return run_grouped(*d, T, x, r, a.pair_pos, 1, shared_w, draft_w, gamma, y, epi, L, ws, &a,
-                     stream);
+                     stream, true, true, true);
 }
 
 int de_verify_layer(const de_moe_desc* d, int T, const float* x, const float* w_router,
@@ -526,11 +530,12 @@ int de_verify_layer(const de_moe_desc* d, int T, const float* x, const float* w_
   a.gate_list = gate_list ? gate_list : at<float>(ws, L.glist);
   a.pair_pos = pair_pos ? pair_pos : at<int32_t>(ws, L.ppos);
   a.z = at<float>(ws, L.z);
-  if (route(*d, T, x, w_router, L, ws, a, stream) != hipSuccess) return DE_ERR_HIP;
+  // Logits only; the gate/up prologue selects the top-k in every block.
+  if (route(*d, T, x, w_router, L, ws, a, stream, false) != hipSuccess) return DE_ERR_HIP;
   const de::RoutedSrc r = routed_src(*d, T, routed, a.n_union, a.union_ids, a.offsets, a.tok_list,
                                      a.gate_list, at<float>(ws, L.a_r), at<float>(ws, L.p_r));
   return run_grouped(*d, T, x, r, a.pair_pos, d->top_k, shared_w, nullptr, 0.f, y, epi, L, ws, &a,
-                     stream);
+                     stream, true, true, true);
 }
 
 size_t de_accept_workspace_bytes(int K, int V) {

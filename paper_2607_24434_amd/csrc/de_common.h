@@ -157,10 +157,12 @@ struct GroupedArgs {
   int n_dense;
   DenseSrc dense[3];
   int lds_floats;      // set by the launcher: staged-input capacity of a block
-  // Gate/up only: build the union from the top-k lists sel.idx_out /
-  // sel.gate_out in every block (block 0 also writes sel's union outputs);
-  // r.n_union ... r.gate_list are then not read.
+  // Gate/up only: build the union in every block (block 0 also writes sel's
+  // outputs); r.n_union ... r.gate_list are then not read.  The lists come
+  // from sel.idx_out / sel.gate_out, or with fuse_select every block selects
+  // them itself from the logits sel.z (block 0 writes them out).
   int fuse_route;
+  int fuse_select;
   TopkUnionArgs sel;
 };
 
@@ -185,6 +187,7 @@ struct RouteArgs {
   int H;
   float* z;                // [T, N] logits out (each position's last block reads them back)
   unsigned* counter;       // [T] arrival counters, zero between calls
+  int select;              // 0: logits only (the gate/up prologue selects)
 };
 hipError_t launch_route(const RouteArgs& r, hipStream_t s);
 // Union only, from caller-supplied lists (sel.idx_in / sel.gate_in).

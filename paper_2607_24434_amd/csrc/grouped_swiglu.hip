@@ -681,12 +681,31 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
   fill_dense(a, tb);
   int nu;
   if (a.fuse_route) {
-    // The union of the top-k lists, in every block; block 0 also publishes it
-    // for the down and combine launches.
+    // The union of the top-k lists (selected here from the logits, or given),
+    // in every block; block 0 also publishes it for the down and combine
+    // launches.
     const SelView v = sel_at(a, tb);
-    for (int i = threadIdx.x; i < a.T * a.sel.k; i += kBlock) {
-      v.idx[i] = a.sel.idx_out[i];
-      v.gate[i] = a.sel.gate_out[i];
+    if (a.fuse_select) {
+      // Every block selects each position's top-k from the logits (one wave
+      // per position); block 0 also writes the lists out.
+      const int k = a.sel.k;
+      for (int t = wave; t < a.T; t += kWavesPB)
+        topk_row(a.sel, a.sel.z + (size_t)t * a.sel.N, v.idx + t * k, v.sc + t * k);
+      __syncthreads();
+      for (int i = threadIdx.x; i < a.T * k; i += kBlock) {
+        const int t = i / k;
+        const float g = topk_gate(a.sel, v.sc + t * k, i - t * k);
+        v.gate[i] = g;
+        if (blockIdx.x == 0) {
+          a.sel.idx_out[i] = v.idx[i];
+          a.sel.gate_out[i] = g;
+        }
+      }
+    } else {
+      for (int i = threadIdx.x; i < a.T * a.sel.k; i += kBlock) {
+        v.idx[i] = a.sel.idx_out[i];
+        v.gate[i] = a.sel.gate_out[i];
+      }
     }
     __syncthreads();
     build_union(a.sel, v, blockIdx.x == 0, tb.tok, tb.gate);

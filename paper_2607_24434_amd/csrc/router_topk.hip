@@ -40,7 +40,7 @@ __device__ inline SelView view_of(SelShared& s) {
 
 // Block (t, g): router logits of position t (Eq. 1) for experts
 // 16g .. 16g+15, one per wave, each router row's and x_t's loads in flight
-// together.  The logits go to z; the last of the position's
+// together.  The logits go to z.  With r.select, the last of the position's
 // blocks to finish (device-scope counter, release / acquire fences so logits
 // written on other XCDs are visible; the counter is left at zero) selects the
 // position's ordered top-k and gates.
@@ -78,6 +78,7 @@ __global__ __launch_bounds__(kRsThreads) void route_split_kernel(RouteArgs r) {
     acc = wave_sum(acc);
     if (lane == 0) r.z[(size_t)t * N + e] = acc;
   }
+  if (!r.select) return;
   __syncthreads();
   if (threadIdx.x == 0) {
     __threadfence();
@@ -113,7 +114,7 @@ __global__ __launch_bounds__(kSelThreads) void union_kernel(TopkUnionArgs a) {
 
 // Grid (T, ceil(N / 16)): every (position, 16 experts) pair in its own block,
 // so all the router rows of a position stream in parallel and each position's
-// selection runs in its own last block.
+// selection (when r.select) runs in its own last block.
 hipError_t launch_route(const RouteArgs& r, hipStream_t s) {
   const dim3 grid(r.sel.T, (r.sel.N + kRsWaves - 1) / kRsWaves);
   hipLaunchKernelGGL(route_split_kernel, grid, dim3(kRsThreads), 0, s, r);
