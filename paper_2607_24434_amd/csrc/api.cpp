@@ -163,9 +163,11 @@ T* at(void* ws, size_t off) {
   return reinterpret_cast<T*>(static_cast<char*>(ws) + off);
 }
 
-de::RoutedSrc routed_src(const de_moe_desc& d, int T, const de_expert_table* tab, const int32_t* nu,
-                         const int32_t* uids, const int32_t* offs, const int32_t* tok,
-                         const float* glist, float* a_r, float* p_r) {
+// kk: list entries per position that can enter the union (k, or 1 for the
+// drafter's top-1), which bounds the union by T * kk.
+de::RoutedSrc routed_src(const de_moe_desc& d, int T, int kk, const de_expert_table* tab,
+                         const int32_t* nu, const int32_t* uids, const int32_t* offs,
+                         const int32_t* tok, const float* glist, float* a_r, float* p_r) {
   de::RoutedSrc r{};
   r.base = static_cast<const char*>(tab->base);
   r.stride = tab->slot_stride_bytes;
@@ -176,7 +178,8 @@ de::RoutedSrc routed_src(const de_moe_desc& d, int T, const de_expert_table* tab
   r.offsets = offs;
   r.tok_list = tok;
   r.gate_list = glist;
-  r.max_union = d.n_experts;
+  r.max_union = T * kk < d.n_experts ? T * kk : d.n_experts;
+  r.n_experts = d.n_experts;
   r.pairs_max = T * d.top_k;  // capacity of the lists, A_r and P_r
   r.inter = d.inter;
   r.a = a_r;
@@ -326,8 +329,9 @@ int layer_after_route(const de_moe_desc& d, int T, const float* x, const de_expe
   a.gate_list = at<float>(ws, L.glist);
   a.pair_pos = at<int32_t>(ws, L.ppos);
   a.z = at<float>(ws, L.z);
-  const RoutedSrc r = routed_src(d, T, routed, a.n_union, a.union_ids, a.offsets, a.tok_list,
-                                 a.gate_list, at<float>(ws, L.a_r), at<float>(ws, L.p_r));
+  const RoutedSrc r = routed_src(d, T, ucols, routed, a.n_union, a.union_ids, a.offsets,
+                                 a.tok_list, a.gate_list, at<float>(ws, L.a_r),
+                                 at<float>(ws, L.p_r));
   return run_grouped(d, T, x, r, a.pair_pos, ucols, shared_w, draft_w, gamma, y, epi, L, ws, &a,
                      stream, dense_on, combine_on);
 }
@@ -447,7 +451,8 @@ int de_grouped_swiglu(const de_moe_desc* d, int T, const float* x, const de_expe
   if ((rc = check_epi(epi)) != DE_OK) return rc;
   if ((rc = check_ws(*d, T, ws, ws_bytes)) != DE_OK) return rc;
   const Layout L = layout(*d, T);
-  const de::RoutedSrc r = routed_src(*d, T, routed, n_union, union_ids, offsets, tok_list, gate_list,
+  const de::RoutedSrc r = routed_src(*d, T, d->top_k, routed, n_union, union_ids, offsets,
+                                     tok_list, gate_list,
                                      at<float>(ws, L.a_r), at<float>(ws, L.p_r));
   return run_grouped(*d, T, x, r, pair_pos, d->top_k, shared_w, nullptr, 0.f, y, epi, L, ws,
                      nullptr, stream);
@@ -490,8 +495,9 @@ int de_draft_layer(const de_moe_desc* d, int T, const float* x, const float* w_r
   a.z = at<float>(ws, L.z);
   // Logits only; the gate/up prologue selects the top-k in every block.
   if (route(*d, T, x, w_router, L, ws, a, stream, false) != hipSuccess) return DE_ERR_HIP;
-  const de::RoutedSrc r = routed_src(*d, T, routed, a.n_union, a.union_ids, a.offsets, a.tok_list,
-                                     a.gate_list, at<float>(ws, L.a_r), at<float>(ws, L.p_r));
+  const de::RoutedSrc r = routed_src(*d, T, 1, routed, a.n_union, a.union_ids, a.offsets,
+                                     a.tok_list, a.gate_list, at<float>(ws, L.a_r),
+                                     at<float>(ws, L.p_r));
   return run_grouped(*d, T, x, r, a.pair_pos, 1, shared_w, draft_w, gamma, y, epi, L, ws, &a,
                      stream, true, true, true);
 }
@@ -532,8 +538,9 @@ int de_verify_layer(const de_moe_desc* d, int T, const float* x, const float* w_
   a.z = at<float>(ws, L.z);
   // Logits only; the gate/up prologue selects the top-k in every block.
   if (route(*d, T, x, w_router, L, ws, a, stream, false) != hipSuccess) return DE_ERR_HIP;
-  const de::RoutedSrc r = routed_src(*d, T, routed, a.n_union, a.union_ids, a.offsets, a.tok_list,
-                                     a.gate_list, at<float>(ws, L.a_r), at<float>(ws, L.p_r));
+  const de::RoutedSrc r = routed_src(*d, T, d->top_k, routed, a.n_union, a.union_ids,
+                                     a.offsets, a.tok_list, a.gate_list, at<float>(ws, L.a_r),
+                                     at<float>(ws, L.p_r));
   return run_grouped(*d, T, x, r, a.pair_pos, d->top_k, shared_w, nullptr, 0.f, y, epi, L, ws, &a,
                      stream, true, true, true);
 }

@@ -108,7 +108,8 @@ struct RoutedSrc {
   const int32_t* offsets;
   const int32_t* tok_list;
   const float* gate_list;
-  int max_union;               // N: bound on the union size and on expert ids
+  int max_union;               // bound on the union size: min(N, T * entries per position)
+  int n_experts;               // N: bound on expert ids
   int pairs_max;               // T*k: capacity of the token lists, A_r and P_r
   int inter;                   // I
   float* a;                    // A_r [pairs, I]

@@ -58,7 +58,6 @@ constexpr int kNS = 4;                      // weight rows per tile
 constexpr int kRoutedNT = 4;                // positions per pass of a union member
 constexpr int kDenseNT = DE_DENSE_NT;       // positions per pass of a dense source
 constexpr int kMaxStaged = 32;              // union members with input rows staged per block (down)
-constexpr int kGuPairs = kNS / 2;           // gate/up: (G, U) row pairs per tile
 constexpr int kRing = DE_RING;              // 16-byte iterations in flight per lane (x kNS), members
 constexpr int kDenseRing = DE_DENSE_RING;   // the same, dense sources
 constexpr int kLdsBudget = 144 * 1024;      // staged activations + tables per block (gate/up)
@@ -241,7 +240,7 @@ __device__ __forceinline__ void members_from_union(const GroupedArgs& a, const T
   for (int e = threadIdx.x; e < a.sel.N; e += kBlock) {
     const unsigned long long m = v.mask[e];
     if (m == 0ull) continue;
-    const int slot = e < r.max_union ? (r.slot_of_expert ? r.slot_of_expert[e] : e) : -1;
+    const int slot = e < r.n_experts ? (r.slot_of_expert ? r.slot_of_expert[e] : e) : -1;
     Member mb{nullptr, v.off[e], (int)__popcll(m), -1, 0};
     if (slot >= 0 && slot < r.n_slots) mb.blk = r.base + (size_t)slot * r.stride;
     tb.mem[v.upos[e]] = mb;
@@ -294,7 +293,7 @@ __device__ __forceinline__ void fill_tables(const GroupedArgs& a, const Tables& 
     Member m{nullptr, 0, 0, -1, 0};
     const int e = r.union_ids[j];
     const int slot =
-        (e >= 0 && e < r.max_union) ? (r.slot_of_expert ? r.slot_of_expert[e] : e) : -1;
+        (e >= 0 && e < r.n_experts) ? (r.slot_of_expert ? r.slot_of_expert[e] : e) : -1;
     const int off = r.offsets[j], end = r.offsets[j + 1];
     if (slot >= 0 && slot < r.n_slots && off >= 0 && end >= off && end <= r.pairs_max) {
       m.blk = r.base + (size_t)slot * r.stride;
@@ -361,9 +360,11 @@ struct Layout {
   }
 };
 
+// Tiles of RT weight rows (gate/up: RT / 2 (G, U) pairs).
+template <int RT>
 __device__ __forceinline__ Layout make_layout(const GroupedArgs& a, int nu, bool gateup) {
   Layout ly;
-  const int per = gateup ? kGuPairs : kNS;
+  const int per = gateup ? RT / 2 : RT;
   const int n0 = a.n_dense > 0 ? uni(cdiv(gateup ? a.dense[0].inter : a.dense[0].rows, per)) : 0;
   const int n1 = a.n_dense > 1 ? uni(cdiv(gateup ? a.dense[1].inter : a.dense[1].rows, per)) : 0;
   const int n2 = a.n_dense > 2 ? uni(cdiv(gateup ? a.dense[2].inter : a.dense[2].rows, per)) : 0;
@@ -385,7 +386,7 @@ struct Cursor {
 };
 
 // The passes of a wave's tiles in [lo, hi) (tiles b*8 + w + k * step).
-template <typename WT, bool GATEUP, int NT>
+template <typename WT, bool GATEUP, int NT, int RT>
 struct Walker {
   Layout ly;      // by value: a reference to a local would live in per-lane scratch
   Tables tb;
@@ -414,10 +415,10 @@ struct Walker {
       if constexpr (GATEUP) {
         const size_t rb = (size_t)H * esz;
         const char* U = blk + (size_t)I * rb;
-        p.r0 = rg * kGuPairs;
+        p.r0 = rg * (RT / 2);
         p.rows = I;
 #pragma unroll
-        for (int q = 0; q < kGuPairs; ++q) {
+        for (int q = 0; q < RT / 2; ++q) {
           const size_t rc = (size_t)min(p.r0 + q, I - 1);
           p.row[2 * q] = blk + rc * rb;
           p.row[2 * q + 1] = U + rc * rb;
@@ -432,10 +433,10 @@ struct Walker {
       } else {
         const size_t rb = (size_t)I * esz;
         const char* D = blk + 2 * (size_t)I * H * esz;
-        p.r0 = rg * kNS;
+        p.r0 = rg * RT;
         p.rows = H;
 #pragma unroll
-        for (int k = 0; k < kNS; ++k) p.row[k] = D + (size_t)min(p.r0 + k, H - 1) * rb;
+        for (int k = 0; k < RT; ++k) p.row[k] = D + (size_t)min(p.r0 + k, H - 1) * rb;
         p.L = (int)(rb / 16);
         const int act = uni(mb.act);
         if (act >= 0) {
@@ -465,10 +466,10 @@ struct Walker {
       if constexpr (GATEUP) {
         const size_t rb = (size_t)H * esz;
         const char* U = W + (size_t)d.inter * rb;
-        p.r0 = rg * kGuPairs;
+        p.r0 = rg * (RT / 2);
         p.rows = d.inter;
 #pragma unroll
-        for (int q = 0; q < kGuPairs; ++q) {
+        for (int q = 0; q < RT / 2; ++q) {
           const size_t rc = (size_t)min(p.r0 + q, d.inter - 1);
           p.row[2 * q] = W + rc * rb;
           p.row[2 * q + 1] = U + rc * rb;
@@ -481,10 +482,10 @@ struct Walker {
         p.ostride = d.inter;
       } else {
         const size_t rb = (size_t)(d.ld > 0 ? d.ld : d.inter) * esz;
-        p.r0 = rg * kNS;
+        p.r0 = rg * RT;
         p.rows = d.rows;
 #pragma unroll
-        for (int k = 0; k < kNS; ++k) p.row[k] = W + (size_t)min(p.r0 + k, d.rows - 1) * rb;
+        for (int k = 0; k < RT; ++k) p.row[k] = W + (size_t)min(p.r0 + k, d.rows - 1) * rb;
         p.L = (int)((size_t)d.inter * esz / 16);
         const int act = dact;
         if (act >= 0) {
@@ -526,19 +527,19 @@ struct Walker {
   }
 };
 
-// Loads iteration `it` of pass p (kNS rows) into r.  Past a row's end the lane
+// Loads iteration `it` of pass p (RT rows) into r.  Past a row's end the lane
 // re-reads the last unit (always in bounds); consume() zeroes it.
-template <int NT>
-__device__ __forceinline__ void issue(const Pass<NT>& p, int it, u32x4 (&r)[kNS], int lane) {
+template <int NT, int RT>
+__device__ __forceinline__ void issue(const Pass<NT>& p, int it, u32x4 (&r)[RT], int lane) {
   const uint32_t uc = (uint32_t)min(it * kWave + lane, p.L - 1) * 16u;
 #pragma unroll
-  for (int k = 0; k < kNS; ++k) r[k] = load_w16(p.row[k] + uc);
+  for (int k = 0; k < RT; ++k) r[k] = load_w16(p.row[k] + uc);
 }
 
 // Accumulates iteration `it` of pass p.
-template <typename WT, int NT>
-__device__ __forceinline__ void consume(const Pass<NT>& p, int it, const u32x4 (&r)[kNS], int lane,
-                                        float (&acc)[kNS][NT]) {
+template <typename WT, int NT, int RT>
+__device__ __forceinline__ void consume(const Pass<NT>& p, int it, const u32x4 (&r)[RT], int lane,
+                                        float (&acc)[RT][NT]) {
   constexpr int EPU = WTr<WT>::EPU;
   const int u = it * kWave + lane;
   const bool ok = u < p.L;
@@ -549,7 +550,7 @@ __device__ __forceinline__ void consume(const Pass<NT>& p, int it, const u32x4 (
       float xv[EPU];
       act_frag<EPU>(p.act, p.vo[m], uc, xv);
 #pragma unroll
-      for (int k = 0; k < kNS; ++k) {
+      for (int k = 0; k < RT; ++k) {
         const u32x4 rr = ok ? r[k] : u32x4{0u, 0u, 0u, 0u};
         float w[EPU];
         unpack(rr, w);
@@ -564,15 +565,15 @@ __device__ __forceinline__ void consume(const Pass<NT>& p, int it, const u32x4 (
 }
 
 // Reduces the pass's sums and writes them; clears acc.
-template <bool GATEUP, int NT>
+template <bool GATEUP, int NT, int RT>
 __device__ __forceinline__ void finish(const Pass<NT>& p, const Tables& tb, int lane,
-                                       float (&acc)[kNS][NT]) {
+                                       float (&acc)[RT][NT]) {
 #pragma unroll
   for (int m = 0; m < NT; ++m) {
     if (m < p.nt) {
       if constexpr (GATEUP) {
 #pragma unroll
-        for (int q = 0; q < kGuPairs; ++q) {
+        for (int q = 0; q < RT / 2; ++q) {
           const float g = row_total(acc[2 * q][m]);
           const float u = row_total(acc[2 * q + 1][m]);
           if (lane == m && p.r0 + q < p.rows)
@@ -582,7 +583,7 @@ __device__ __forceinline__ void finish(const Pass<NT>& p, const Tables& tb, int 
       } else {
         const float gm = p.goff >= 0 ? tb.gate[p.goff + m] : p.gscalar;
 #pragma unroll
-        for (int k = 0; k < kNS; ++k) {
+        for (int k = 0; k < RT; ++k) {
           const float v = row_total(acc[k][m]);
           if (lane == m && p.r0 + k < p.rows) {
             // A global (not flat) store: a flat store also counts against the
@@ -594,22 +595,23 @@ __device__ __forceinline__ void finish(const Pass<NT>& p, const Tables& tb, int 
     }
   }
 #pragma unroll
-  for (int k = 0; k < kNS; ++k)
+  for (int k = 0; k < RT; ++k)
 #pragma unroll
     for (int m = 0; m < NT; ++m) acc[k][m] = 0.f;
 }
 
 // Streams the wave's pass sequence: the loader runs RING iterations ahead of
 // the consumer, across pass and tile boundaries.
-template <typename WT, bool GATEUP, int NT, int RING>
-__device__ __forceinline__ void run_stream(const GroupedArgs& a, const Walker<WT, GATEUP, NT> wk,
-                                           int first_tile, int lane) {
+template <typename WT, bool GATEUP, int NT, int RING, int RT>
+__device__ __forceinline__ void run_stream(const GroupedArgs& a,
+                                           const Walker<WT, GATEUP, NT, RT> wk, int first_tile,
+                                           int lane) {
   Cursor lc{first_tile, 0, 0}, cc{first_tile, 0, 0};
   Pass<NT> lp, cp;
   bool l_ok = wk.seek(a, lc, lp);
   bool c_ok = wk.seek(a, cc, cp);
   int l_it = 0, c_it = 0;
-  u32x4 raw[RING][kNS];
+  u32x4 raw[RING][RT];
 #pragma unroll
   for (int q = 0; q < RING; ++q) {
     if (l_ok) {
@@ -620,18 +622,18 @@ __device__ __forceinline__ void run_stream(const GroupedArgs& a, const Walker<WT
       }
     }
   }
-  float acc[kNS][NT];
+  float acc[RT][NT];
 #pragma unroll
-  for (int k = 0; k < kNS; ++k)
+  for (int k = 0; k < RT; ++k)
 #pragma unroll
     for (int m = 0; m < NT; ++m) acc[k][m] = 0.f;
   while (c_ok) {
 #pragma unroll
     for (int q = 0; q < RING; ++q) {
       if (c_ok) {
-        consume<WT, NT>(cp, c_it, raw[q], lane, acc);
+        consume<WT, NT, RT>(cp, c_it, raw[q], lane, acc);
         if (++c_it == cp.nit) {
-          finish<GATEUP, NT>(cp, wk.tb, lane, acc);
+          finish<GATEUP, NT, RT>(cp, wk.tb, lane, acc);
           c_ok = wk.next(a, cc, cp);
           c_it = 0;
         }
@@ -649,19 +651,19 @@ __device__ __forceinline__ void run_stream(const GroupedArgs& a, const Walker<WT
 
 // A wave's tiles: first, first + step, ...  The dense tiles [0, ndt) run with
 // passes of kDenseNT positions, the members' tiles with kRoutedNT.
-template <typename WT, bool GATEUP>
+template <typename WT, bool GATEUP, int RT>
 __device__ __forceinline__ void run_tiles(const GroupedArgs& a, const Layout ly, const Tables& tb,
                                           int xstride, bool xlds, int lane, int wave) {
   const int step = (int)gridDim.x * kWavesPB;
   const int first = (int)blockIdx.x * kWavesPB + wave;
   if (first < ly.ndt) {
-    const Walker<WT, GATEUP, kDenseNT> wd{ly, tb, step, 0, ly.ndt, xstride, xlds};
-    run_stream<WT, GATEUP, kDenseNT, kDenseRing>(a, wd, first, lane);
+    const Walker<WT, GATEUP, kDenseNT, RT> wd{ly, tb, step, 0, ly.ndt, xstride, xlds};
+    run_stream<WT, GATEUP, kDenseNT, kDenseRing, RT>(a, wd, first, lane);
   }
   if (ly.nr > 0) {
     const int f2 = first >= ly.ndt ? first : first + cdiv(ly.ndt - first, step) * step;
-    const Walker<WT, GATEUP, kRoutedNT> wr{ly, tb, step, ly.ndt, ly.total, xstride, xlds};
-    run_stream<WT, GATEUP, kRoutedNT, kRing>(a, wr, f2, lane);
+    const Walker<WT, GATEUP, kRoutedNT, RT> wr{ly, tb, step, ly.ndt, ly.total, xstride, xlds};
+    run_stream<WT, GATEUP, kRoutedNT, kRing, RT>(a, wr, f2, lane);
   }
 }
 
@@ -670,7 +672,7 @@ __device__ __forceinline__ void run_tiles(const GroupedArgs& a, const Layout ly,
 
 // Gate/up: A = silu(G x) * (U x) for the dense sources and the union members'
 // pairs.  LDSX: the block of positions is staged in LDS.
-template <typename WT, bool LDSX>
+template <typename WT, bool LDSX, int RT>
 __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) void gateup_kernel(
     GroupedArgs a) {
   constexpr int EPU = WTr<WT>::EPU;
@@ -717,15 +719,15 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
     if (a.has_routed) fill_tables(a, tb, nu);
   }
   __syncthreads();
-  const Layout ly = make_layout(a, nu, true);
-  run_tiles<WT, true>(a, ly, tb, LDSX ? staged_stride<EPU>(a.H) : a.H, LDSX, lane, wave);
+  const Layout ly = make_layout<RT>(a, nu, true);
+  run_tiles<WT, true, RT>(a, ly, tb, LDSX ? staged_stride<EPU>(a.H) : a.H, LDSX, lane, wave);
 }
 
 // Down projection / row-dot: out = gate * (M v) for the dense sources and the
 // union members' D rows.  A block stages in LDS the input rows of the members
 // its tiles visit (one or two per sweep of the grid) and of the dense sources
 // it meets, as far as they fit; the rest are read from global memory.
-template <typename WT>
+template <typename WT, int RT>
 __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) void down_kernel(
     GroupedArgs a) {
   constexpr int EPU = WTr<WT>::EPU;
@@ -735,7 +737,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
   fill_dense(a, tb);
   if (a.has_routed) fill_tables(a, tb, nu);
   __syncthreads();
-  Layout ly = make_layout(a, nu, false);
+  Layout ly = make_layout<RT>(a, nu, false);
   __shared__ int s_dact[3];
   __shared__ int s_list[kMaxStaged + 1];
   __shared__ int s_nlist;
@@ -797,7 +799,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
   ly.act0 = uni(s_dact[0]);
   ly.act1 = uni(s_dact[1]);
   ly.act2 = uni(s_dact[2]);
-  run_tiles<WT, false>(a, ly, tb, 0, false, lane, wave);
+  run_tiles<WT, false, RT>(a, ly, tb, 0, false, lane, wave);
 }
 
 // ------------------------------------------------------------------ combine
@@ -916,8 +918,8 @@ hipError_t launch_persistent(K kernel, int max_tiles, size_t lds, const GroupedA
   return note_hip(hipGetLastError());
 }
 
-int max_tiles(const GroupedArgs& a, bool gateup) {
-  const int per = gateup ? kGuPairs : kNS;
+int max_tiles(const GroupedArgs& a, bool gateup, int rt) {
+  const int per = gateup ? rt / 2 : rt;
   int t = a.has_routed ? a.r.max_union * cdiv(gateup ? a.r.inter : a.H, per) : 0;
   for (int s = 0; s < a.n_dense; ++s) t += cdiv(gateup ? a.dense[s].inter : a.dense[s].rows, per);
   return t;
@@ -929,15 +931,27 @@ size_t staged_bytes(int rows, int len) {
 }
 
 // The whole block of positions is staged in LDS when it fits the budget.
+// Small launches (fewer full tiles than the device has waves) use tiles of
+// one (G, U) pair or two rows, so that more waves share the rows (one row per
+// down tile measured slower: every block then stages every source's input).
+bool small_launch(const GroupedArgs& a, bool gateup) {
+  return max_tiles(a, gateup, kNS) < dev_info().num_cus * 2 * kWavesPB;
+}
+
+template <typename WT, bool LDSX>
+hipError_t gateup_tiles(const GroupedArgs& a, size_t lds, hipStream_t s) {
+  if (small_launch(a, true))
+    return launch_persistent(gateup_kernel<WT, LDSX, 2>, max_tiles(a, true, 2), lds, a, s);
+  return launch_persistent(gateup_kernel<WT, LDSX, kNS>, max_tiles(a, true, kNS), lds, a, s);
+}
+
 template <typename WT>
 hipError_t gateup_typed(const GroupedArgs& a, hipStream_t s) {
-  const int tiles = max_tiles(a, true);
-  if (tiles == 0) return hipSuccess;
+  if (max_tiles(a, true, kNS) == 0) return hipSuccess;
   const size_t tabs = tables_bytes(a);
   const size_t lds = staged_bytes<WT>(a.T, a.H);
-  if (lds + tabs <= (size_t)kLdsBudget)
-    return launch_persistent(gateup_kernel<WT, true>, tiles, lds + tabs, a, s);
-  return launch_persistent(gateup_kernel<WT, false>, tiles, tabs, a, s);
+  if (lds + tabs <= (size_t)kLdsBudget) return gateup_tiles<WT, true>(a, lds + tabs, s);
+  return gateup_tiles<WT, false>(a, tabs, s);
 }
 
 // The down kernel stages the inputs of the sources a block visits: a fixed
@@ -945,13 +959,14 @@ hipError_t gateup_typed(const GroupedArgs& a, hipStream_t s) {
 // and the few members' rows of the grouped down in the common case.
 template <typename WT>
 hipError_t down_typed(GroupedArgs a, hipStream_t s) {
-  const int tiles = max_tiles(a, false);
-  if (tiles == 0) return hipSuccess;
+  if (max_tiles(a, false, kNS) == 0) return hipSuccess;
   const size_t tabs = tables_bytes(a);
   const size_t budget = (size_t)kDownLds > tabs + 4096 ? (size_t)kDownLds - tabs : 4096;
   a.lds_floats = (int)(budget / sizeof(float)) & ~3;
-  return launch_persistent(down_kernel<WT>, tiles, (size_t)a.lds_floats * sizeof(float) + tabs, a,
-                           s);
+  const size_t lds = (size_t)a.lds_floats * sizeof(float) + tabs;
+  if (small_launch(a, false))
+    return launch_persistent(down_kernel<WT, 2>, max_tiles(a, false, 2), lds, a, s);
+  return launch_persistent(down_kernel<WT, kNS>, max_tiles(a, false, kNS), lds, a, s);
 }
 
 }  // namespace
