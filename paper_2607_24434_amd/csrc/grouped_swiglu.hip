@@ -634,8 +634,23 @@ __device__ __forceinline__ void run_stream(const GroupedArgs& a,
         consume<WT, NT, RT>(cp, c_it, raw[q], lane, acc);
         if (++c_it == cp.nit) {
           finish<GATEUP, NT, RT>(cp, wk.tb, lane, acc);
+          const int prev_tile = cc.tile;
           c_ok = wk.next(a, cc, cp);
           c_it = 0;
+          // Dense sources over many positions are arithmetic-heavy: a wave
+          // with more tiles left gets a higher issue priority, so the waves
+          // of a CU finish together instead of the oldest first.
+          if (NT == kDenseNT && a.T >= 8 && c_ok && cc.tile != prev_tile) {
+            const int rem = (wk.hi - 1 - cc.tile) / wk.step;
+            if (rem >= 3)
+              __builtin_amdgcn_s_setprio(3);
+            else if (rem == 2)
+              __builtin_amdgcn_s_setprio(2);
+            else if (rem == 1)
+              __builtin_amdgcn_s_setprio(1);
+            else
+              __builtin_amdgcn_s_setprio(0);
+          }
         }
         if (l_ok) {
           issue(lp, l_it, raw[q], lane);
@@ -660,6 +675,7 @@ __device__ __forceinline__ void run_tiles(const GroupedArgs& a, const Layout ly,
     const Walker<WT, GATEUP, kDenseNT, RT> wd{ly, tb, step, 0, ly.ndt, xstride, xlds};
     run_stream<WT, GATEUP, kDenseNT, kDenseRing, RT>(a, wd, first, lane);
   }
+  __builtin_amdgcn_s_setprio(0);
   if (ly.nr > 0) {
     const int f2 = first >= ly.ndt ? first : first + cdiv(ly.ndt - first, step) * step;
     const Walker<WT, GATEUP, kRoutedNT, RT> wr{ly, tb, step, ly.ndt, ly.total, xstride, xlds};
