@@ -235,9 +235,9 @@ __device__ __forceinline__ SelView sel_at(const GroupedArgs& a, const Tables& tb
 // The member table from a union built in LDS: member j = the expert with
 // union index j.  All threads; the caller synchronises.
 __device__ __forceinline__ void members_from_union(const GroupedArgs& a, const Tables& tb,
-                                                   const SelView& v) {
+                                                   const SelView& v, int first, int stride) {
   const RoutedSrc& r = a.r;
-  for (int e = threadIdx.x; e < a.sel.N; e += kBlock) {
+  for (int e = first; e < a.sel.N; e += stride) {
     const unsigned long long m = v.mask[e];
     if (m == 0ull) continue;
     const int slot = e < r.n_experts ? (r.slot_of_expert ? r.slot_of_expert[e] : e) : -1;
@@ -695,46 +695,78 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
   const int lane = threadIdx.x & 63, wave = uni((int)(threadIdx.x >> 6));
   const int act_floats = LDSX ? a.T * staged_stride<EPU>(a.H) : 0;
   const Tables tb = tables_at(a, act_floats);
+  // Fused selection: the wave's first two positions' logits are loaded
+  // before the staging so that their latency overlaps it.
+  const bool sel = a.fuse_route && a.fuse_select;
+  float z0[2][4];
+#pragma unroll
+  for (int r = 0; r < 2; ++r) {
+    // Clamped position: in bounds; a position past T is never selected.
+    const int t = min(wave + r * kWavesPB, a.T - 1);
+    if (sel) {
+      topk_load(a.sel, a.sel.z + (size_t)t * a.sel.N, z0[r]);
+    } else {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) z0[r][q] = 0.f;
+    }
+  }
   if constexpr (LDSX) stage_rows<EPU>(a.x, a.H, a.T, a.H);
   fill_dense(a, tb);
   int nu;
   if (a.fuse_route) {
-    // The union of the top-k lists (selected here from the logits, or given),
-    // in every block; block 0 also publishes it for the down and combine
-    // launches.
+    // The top-k lists (selected here from the logits, or given), then their
+    // union, in every block; block 0 also publishes both for the down and
+    // combine launches.
     const SelView v = sel_at(a, tb);
-    if (a.fuse_select) {
-      // Every block selects each position's top-k from the logits (one wave
-      // per position); block 0 also writes the lists out.
-      const int k = a.sel.k;
-      for (int t = wave; t < a.T; t += kWavesPB)
-        topk_row(a.sel, a.sel.z + (size_t)t * a.sel.N, v.idx + t * k, v.sc + t * k);
-      __syncthreads();
-      for (int i = threadIdx.x; i < a.T * k; i += kBlock) {
-        const int t = i / k;
-        const float g = topk_gate(a.sel, v.sc + t * k, i - t * k);
-        v.gate[i] = g;
-        if (blockIdx.x == 0) {
-          a.sel.idx_out[i] = v.idx[i];
-          a.sel.gate_out[i] = g;
+    const int k = a.sel.k;
+    if (sel) {
+      // Wave w selects positions w, w + 8 (two interleaved), then w + 16, ...
+      for (int t = wave; t < a.T; t += 2 * kWavesPB) {
+        const int t1 = t + kWavesPB;
+        if (t != wave) {
+          topk_load(a.sel, a.sel.z + (size_t)t * a.sel.N, z0[0]);
+          if (t1 < a.T) topk_load(a.sel, a.sel.z + (size_t)t1 * a.sel.N, z0[1]);
+        }
+        if (t1 < a.T) {
+          topk_regs<2>(a.sel, z0, v.idx + t * k, v.sc + t * k, v.idx + t1 * k, v.sc + t1 * k);
+        } else {
+          float z1[1][4];
+#pragma unroll
+          for (int q = 0; q < 4; ++q) z1[0][q] = z0[0][q];
+          topk_regs<1>(a.sel, z1, v.idx + t * k, v.sc + t * k);
+        }
+        for (int r = 0; r < 2; ++r) {
+          const int tt = t + r * kWavesPB;
+          if (tt < a.T && lane < k) {
+            const float g = topk_gate(a.sel, v.sc + tt * k, lane);
+            v.gate[tt * k + lane] = g;
+            if (blockIdx.x == 0) {
+              a.sel.idx_out[tt * k + lane] = v.idx[tt * k + lane];
+              a.sel.gate_out[tt * k + lane] = g;
+            }
+          }
         }
       }
     } else {
-      for (int i = threadIdx.x; i < a.T * a.sel.k; i += kBlock) {
+      for (int i = threadIdx.x; i < a.T * k; i += kBlock) {
         v.idx[i] = a.sel.idx_out[i];
         v.gate[i] = a.sel.gate_out[i];
       }
     }
     __syncthreads();
-    build_union(a.sel, v, blockIdx.x == 0, tb.tok, tb.gate);
+    if (wave == 0) {
+      build_union_wave(a.sel, v, blockIdx.x == 0, tb.tok, tb.gate);
+      const int n = uni(v.misc[1]);
+      if (n > 0) members_from_union(a, tb, v, lane, kWave);
+    }
+    __syncthreads();
     nu = uni(v.misc[1]);
     nu = nu < 0 ? 0 : min(nu, a.r.max_union);
-    if (nu > 0) members_from_union(a, tb, v);
   } else {
     nu = routed_count(a);
     if (a.has_routed) fill_tables(a, tb, nu);
+    __syncthreads();
   }
-  __syncthreads();
   const Layout ly = make_layout<RT>(a, nu, true);
   run_tiles<WT, true, RT>(a, ly, tb, LDSX ? staged_stride<EPU>(a.H) : a.H, LDSX, lane, wave);
 }

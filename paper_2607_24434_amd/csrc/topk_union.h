@@ -50,77 +50,125 @@ __device__ inline SelView sel_view_at(char* p, int T, int k, int N) {
   return v;
 }
 
-// Ordered top-k of position t from its N logits zrow (one wave; zrow may be
-// in LDS or global memory): ids into idx[0..k), scores into sc_out[0..k).
-// Lane l holds the candidates l, l + 64, ... (N <= 256).  Each of the k rounds
-// takes the largest remaining key, ties to the lower id: every lane offers
-// its best remaining candidate, a wave max finds the key, a wave min the
-// lowest id offering it, and the owning lane records and retires it.  A NaN
-// key counts as -inf; a candidate id >= N never competes.
-__device__ inline void topk_row(const TopkUnionArgs& a, const float* zrow, int32_t* idx,
-                                float* sc_out) {
+// Loads a position's N logits into the lane layout of the selection: lane l
+// holds candidates l, l + 64, ... (N <= 256; zrow in LDS or global memory).
+__device__ __forceinline__ void topk_load(const TopkUnionArgs& a, const float* zrow,
+                                          float (&z)[4]) {
   const int lane = threadIdx.x & 63;
-  const int N = a.N, k = a.k;
-  float key[4], sc[4];
-  bool left[4];
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
     const int e = lane + q * kWave;
-    left[q] = e < N;
-    const float zz = left[q] ? zrow[e] : 0.f;
-    const float b = (left[q] && a.bias != nullptr) ? a.bias[e] : 0.f;
-    float kk, sv;
-    if (a.score_func == 0) {  // softmax(z + b): key z + b
-      kk = zz + b;
-      sv = 0.f;
-    } else {                  // sigmoid(z): key sigmoid(z) + b
-      sv = 1.0f / (1.0f + expf(-zz));
-      kk = sv + b;
-    }
-    if (!(kk == kk)) kk = -INFINITY;  // a NaN never wins
-    key[q] = left[q] ? kk : -INFINITY;
-    sc[q] = sv;
+    z[q] = e < a.N ? zrow[e] : 0.f;
   }
-  if (a.score_func == 0) {
-    float m = -INFINITY;
+}
+
+// Ordered top-k of R positions at once from their logits in registers (R
+// independent chains interleaved, so their reduction latencies overlap):
+// ids into idx0 / idx1 [0..k), scores into sc0 / sc1 [0..k).  Each of the k rounds
+// takes the largest remaining key, ties to the lower id: every lane offers
+// its best remaining candidate, a wave max finds the key, a wave min the
+// lowest id offering it, and the owning lane records and retires it.  A NaN
+// key counts as -inf; a candidate id >= N never competes.  One wave.
+template <int R>
+__device__ __forceinline__ void topk_regs(const TopkUnionArgs& a, const float (&z)[R][4],
+                                          int32_t* idx0, float* sc0, int32_t* idx1 = nullptr,
+                                          float* sc1 = nullptr) {
+  const int lane = threadIdx.x & 63;
+  const int N = a.N, k = a.k;
+  float key[R][4], sc[R][4];
+  bool left[R][4];
 #pragma unroll
-    for (int q = 0; q < 4; ++q)
-      if (left[q]) m = fmaxf(m, key[q]);
-    m = wave_max(m);
-    float ex[4], sum = 0.f;
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      ex[q] = left[q] ? expf(key[q] - m) : 0.f;
-      sum += ex[q];
-    }
-    sum = wave_sum(sum);
-#pragma unroll
-    for (int q = 0; q < 4; ++q) sc[q] = ex[q] / sum;
-  }
-  for (int j = 0; j < k; ++j) {
-    float bk = -INFINITY;
-    int bid = INT_MAX;
+  for (int r = 0; r < R; ++r) {
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const int e = lane + q * kWave;
-      if (left[q] && (key[q] > bk || (key[q] == bk && e < bid))) {
-        bk = key[q];
-        bid = e;
+      left[r][q] = e < N;
+      const float b = (left[r][q] && a.bias != nullptr) ? a.bias[e] : 0.f;
+      float kk, sv;
+      if (a.score_func == 0) {  // softmax(z + b): key z + b
+        kk = z[r][q] + b;
+        sv = 0.f;
+      } else {                  // sigmoid(z): key sigmoid(z) + b
+        sv = 1.0f / (1.0f + expf(-z[r][q]));
+        kk = sv + b;
       }
+      if (!(kk == kk)) kk = -INFINITY;  // a NaN never wins
+      key[r][q] = left[r][q] ? kk : -INFINITY;
+      sc[r][q] = sv;
     }
-    const float m = wave_max(bk);
-    const int win = wave_min_i32(bk == m ? bid : INT_MAX);
-    if (bid == win) {
+  }
+  if (a.score_func == 0) {
+    float m[R], sum[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      m[r] = -INFINITY;
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        if (left[r][q]) m[r] = fmaxf(m[r], key[r][q]);
+    }
+#pragma unroll
+    for (int r = 0; r < R; ++r) m[r] = wave_max(m[r]);
+    float ex[R][4];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      sum[r] = 0.f;
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        if (q == (win >> 6)) {
-          left[q] = false;
-          idx[j] = win;
-          sc_out[j] = sc[q];
+        ex[r][q] = left[r][q] ? expf(key[r][q] - m[r]) : 0.f;
+        sum[r] += ex[r][q];
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < R; ++r) sum[r] = wave_sum(sum[r]);
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) sc[r][q] = ex[r][q] / sum[r];
+  }
+  for (int j = 0; j < k; ++j) {
+    float bk[R];
+    int bid[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      bk[r] = -INFINITY;
+      bid[r] = INT_MAX;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int e = lane + q * kWave;
+        if (left[r][q] && (key[r][q] > bk[r] || (key[r][q] == bk[r] && e < bid[r]))) {
+          bk[r] = key[r][q];
+          bid[r] = e;
+        }
+      }
+    }
+    float m[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) m[r] = wave_max(bk[r]);
+    int win[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) win[r] = wave_min_i32(bk[r] == m[r] ? bid[r] : INT_MAX);
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      if (bid[r] == win[r]) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          if (q == (win[r] >> 6)) {
+            left[r][q] = false;
+            (r == 0 ? idx0 : idx1)[j] = win[r];
+            (r == 0 ? sc0 : sc1)[j] = sc[r][q];
+          }
         }
       }
     }
   }
+}
+
+// Ordered top-k of one position from its N logits zrow (one wave).
+__device__ inline void topk_row(const TopkUnionArgs& a, const float* zrow, int32_t* idx,
+                                float* sc_out) {
+  float z[1][4];
+  topk_load(a, zrow, z[0]);
+  topk_regs<1>(a, z, idx, sc_out);
 }
 
 // Gate of list entry j of a position from the list's scores: score_j
@@ -238,6 +286,99 @@ __device__ inline void build_union(const TopkUnionArgs& a, const SelView& s, boo
     }
   }
   __syncthreads();
+}
+
+// The union of build_union by one wave, with no block barrier (the caller
+// synchronises the block afterwards): position masks by LDS atomics, the
+// expert scan, and the lists.  Same results as build_union.
+__device__ inline void build_union_wave(const TopkUnionArgs& a, const SelView& s, bool write_out,
+                                        int32_t* ptok, float* pgate) {
+  const int lane = threadIdx.x & 63;
+  const int T = a.T, N = a.N, k = a.k, uc = a.ucols;
+  for (int e = lane; e < N; e += kWave) s.mask[e] = 0ull;
+  bool bad = false;
+  for (int i = lane; i < T * uc; i += kWave) {
+    const int t = i / uc, j = i - t * uc;
+    const int e = s.idx[t * k + j];
+    if (e < 0 || e >= N) {
+      bad = true;
+    } else {
+      const unsigned long long bit = 1ull << t;
+      const unsigned long long old = atomicOr(&s.mask[e], bit);
+      if (old & bit) bad = true;
+    }
+  }
+  if (__ballot(bad) != 0ull) {
+    if (lane == 0) {
+      s.misc[1] = -1;
+      s.misc[2] = 0;
+      if (write_out) *a.n_union = -1;
+    }
+    return;
+  }
+  int cnt[4], flg[4], csum = 0, fsum = 0;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int e = lane * 4 + q;
+    const unsigned long long m = e < N ? s.mask[e] : 0ull;
+    cnt[q] = (int)__popcll(m);
+    flg[q] = m != 0ull;
+    csum += cnt[q];
+    fsum += flg[q];
+  }
+  int ci = csum, fi = fsum;
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) {
+    const int cu = __shfl_up(ci, o, kWave);
+    const int fu = __shfl_up(fi, o, kWave);
+    if (lane >= o) {
+      ci += cu;
+      fi += fu;
+    }
+  }
+  int cbase = ci - csum, fbase = fi - fsum;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int e = lane * 4 + q;
+    if (e < N) {
+      s.off[e] = cbase;
+      s.upos[e] = fbase;
+    }
+    cbase += cnt[q];
+    fbase += flg[q];
+  }
+  const int nu = __builtin_amdgcn_readlane(fi, 63), total = __builtin_amdgcn_readlane(ci, 63);
+  if (lane == 0) {
+    s.misc[1] = nu;
+    s.misc[2] = total;
+  }
+  if (write_out) {
+    for (int e = lane; e < N; e += kWave) {
+      if (s.mask[e] != 0ull) {
+        a.union_ids[s.upos[e]] = e;
+        a.offsets[s.upos[e]] = s.off[e];
+      }
+    }
+    for (int u = nu + lane; u < N; u += kWave) a.union_ids[u] = -1;
+    for (int u = nu + lane; u <= N; u += kWave) a.offsets[u] = total;
+    if (lane == 0) *a.n_union = nu;
+  }
+  for (int i = lane; i < T * uc; i += kWave) {
+    const int t = i / uc, j = i - t * uc;
+    const int e = s.idx[t * k + j];
+    const unsigned long long below = t == 0 ? 0ull : (s.mask[e] & (~0ull >> (64 - t)));
+    const int p = s.off[e] + (int)__popcll(below);
+    const float g = s.gate[t * k + j];
+    if (write_out) {
+      a.tok_list[p] = t;
+      a.gate_list[p] = g;
+      a.pair_pos[i] = p;
+    }
+    if (ptok != nullptr) {
+      ptok[p] = t;
+      pgate[p] = g;
+    }
+  }
 }
 
 }  // namespace de
