@@ -12,9 +12,11 @@ Modules
             decoding (Algorithm 1)
     cache_sim  the expert cache bookkeeping with draft-router prefetch
                (Section 3.5, Algorithm 1)
+    truncation confidence-expansion truncation of the draft loop
+               (Section 3.4, Eqs. 12-14, Algorithm 1)
 
 Pins (tests/test_oracle_*.py) tie every function to the paper or to
 mathematics independent of this code; functions without such a pin say
 "parity unpinned" in their docstring.
 """
-from . import cache_sim, decode, moe  # noqa: F401
+from . import cache_sim, decode, moe, truncation  # noqa: F401

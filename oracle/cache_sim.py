@@ -140,6 +140,22 @@ class CacheSim:
         self.ensure(layer, [topk[0]], DRAFT)
         self.prefetch(layer, topk)
 
+    def step_truncated(self, draft_topk, n_kept: int, verify_topk):
+        """One offloaded step with truncation (Algorithm 1 in its own order):
+        every evaluated draft token requests its top-1 expert in each layer;
+        only a kept token (the first n_kept) then prefetches its top-k in
+        every layer, after the keep decision; the stopped token prefetches
+        nothing."""
+        self.begin_block()
+        for i, per_layer in enumerate(draft_topk):
+            for layer, topk in enumerate(per_layer):
+                self.ensure(layer, [int(topk[0])], DRAFT)
+            if i < n_kept:
+                for layer, topk in enumerate(per_layer):
+                    self.prefetch(layer, topk)
+        for layer, lists in enumerate(verify_topk):
+            self.verify_layer(layer, [e for row in lists for e in row])
+
     def step(self, draft_topk, verify_topk):
         """One offloaded step: draft_topk[i][l] the drafter's top-k at draft
         position i in layer l; verify_topk[l] the verify block's [T, k] lists."""
