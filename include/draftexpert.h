@@ -390,6 +390,74 @@ int de_spec_step_cached(const de_model* m, de_cache* cache, int K, int32_t* bloc
                         int32_t* target_argmax, int32_t* out, int32_t* n_union, int32_t* pred_idx,
                         void* ws, size_t ws_bytes, hipStream_t stream);
 
+/* ---- Confidence-expansion truncation (Section 3.4, Eqs. 12-14; Algorithm 1) ----
+ *
+ * Drafting stops before appending draft token i when the token is uncertain
+ * and would grow the predicted verifier set too much: q_i < tau and
+ * Delta_i > B_i.  q_i is the largest softmax probability of the token's draft
+ * logits; the predicted verifier experts of the token in layer l are the
+ * drafter's router top-k there; the block-level predicted set is the union of
+ * those (layer, expert) pairs over the kept tokens and Delta_i is how many
+ * pairs token i would add.  B_i is a fixed count of layer-experts, or, with
+ * DE_BUDGET_CACHE, the room the predicted set still has in the expert cache:
+ * sum over layers of max(0, slots - pairs of the set in that layer). */
+#define DE_BUDGET_CACHE (-1)
+
+/* q [T] fp32 (device) = 1 / sum_v exp(l_v - max_v l_v) for each row of
+ * logits [T, V] fp32 (device, row-major).  A NaN logit counts as -infinity;
+ * a row with no logit above -infinity gives NaN.  One launch on `stream`. */
+int de_confidence(int T, int V, const float* logits, float* q, hipStream_t stream);
+
+/* Eq. 12-14 for one draft token, in one launch on `stream` (all pointers
+ * device):
+ *   pred_idx [L, k] int32: the token's predicted experts per layer (ids in
+ *     [0, N), N <= 256; an id outside is skipped and counted in out[4]);
+ *   uhat [L, ceil(N / 64)] uint64 (8-byte aligned): the block-level set,
+ *     bit e of layer l's words = pair (l, e); read as empty when `first` is
+ *     nonzero (no clearing needed before a block's first token); grown by
+ *     the token's pairs only when the token is kept;
+ *   q [1] fp32: the token's confidence (e.g. from de_confidence);
+ *   tau: the confidence threshold (not NaN);
+ *   budget: B_i >= 0, or DE_BUDGET_CACHE to derive it from `slots` per layer;
+ *   out [5] int32 = (Delta_i, stop (0/1), B_i used, set size after,
+ *     ids out of range).
+ * DE_ERR_INVALID on bad sizes or pointers. */
+int de_expansion(int L, int k, int N, const int32_t* pred_idx, uint64_t* uhat, int first,
+                 const float* q, float tau, int budget, int slots, int32_t* out,
+                 hipStream_t stream);
+
+typedef struct {
+  float tau;       /* confidence threshold */
+  int32_t budget;  /* B_i: a fixed count of layer-experts, or DE_BUDGET_CACHE */
+  int32_t slots;   /* slots per layer for DE_BUDGET_CACHE; 0 with a cache: its n_slots */
+} de_trunc_cfg;
+
+/* One exact draft-then-verify step with truncation (Algorithm 1): up to
+ * k_max drafts, each kept or stopped by Eq. 14 after its draft pass; the
+ * kept drafts d_1..d_n_drafted are verified as de_spec_step verifies K of
+ * them.  With `cache` (may be NULL) the routed experts come through it as in
+ * de_spec_step_cached, except that a draft token's verifier prefetches (its
+ * top-k in every layer) are started after the token is kept, and a stopped
+ * token starts none.
+ *   block [k_max+1]: block[0] input; block[1..n_drafted] the kept drafts
+ *     (entries after them unspecified);
+ *   target_argmax [k_max+1] (first n_drafted+1 written), out [2] = (n, bonus)
+ *     against the kept drafts, n_union [n_layers] (may be NULL);
+ *   n_drafted: HOST int32, the number of kept drafts;
+ *   pred_idx [k_max, n_layers, k] (required): the drafter's top-k per
+ *     evaluated token and layer;
+ *   q [k_max] fp32 (required): the confidence of every evaluated token;
+ *   trace [k_max, 4] int32 (may be NULL): per evaluated token
+ *     (Delta_i, stop, B_i, set size after).
+ * Tokens after the stopped one are not evaluated (their entries untouched).
+ * Synchronises the host with `stream` once per evaluated token (and, with a
+ * cache, once per layer and position).  Scratch:
+ * de_model_workspace_bytes(m, k_max + 1). */
+int de_spec_step_trunc(const de_model* m, de_cache* cache, int k_max, const de_trunc_cfg* cfg,
+                       int32_t* block, int32_t* target_argmax, int32_t* out, int32_t* n_drafted,
+                       int32_t* n_union, int32_t* pred_idx, float* q, int32_t* trace, void* ws,
+                       size_t ws_bytes, hipStream_t stream);
+
 /* Pure streaming read of `bytes` (multiple of 16) from buf: the measured HBM
  * read ceiling.  sink [1] receives a value that depends on every byte. */
 int de_stream_probe(const void* buf, size_t bytes, float* sink, hipStream_t stream);

@@ -34,6 +34,7 @@ C_FUNCS = [
     "de_greedy_decode", "de_cache_create", "de_cache_destroy", "de_cache_reset",
     "de_cache_begin_block", "de_cache_prefetch", "de_cache_ensure", "de_cache_release",
     "de_cache_table", "de_cache_stats", "de_cache_slots", "de_spec_step_cached",
+    "de_confidence", "de_expansion", "de_spec_step_trunc",
 ]
 DE_PHASE_GATEUP = 0
 DE_PHASE_DOWN = 1
@@ -41,6 +42,7 @@ DE_TARGET = 0
 DE_DRAFT = 1
 DE_NEED_DRAFT = 0
 DE_NEED_VERIFY = 1
+DE_BUDGET_CACHE = -1
 
 
 class DEError(RuntimeError):
@@ -98,6 +100,10 @@ class CacheCfg(ctypes.Structure):
 CACHE_COUNTS = ("prefetch_issued", "prefetch_used", "prefetch_wasted", "prefetch_skipped",
                 "draft_needed", "draft_hits", "verify_needed", "verify_hits", "demand_loads",
                 "evictions", "bytes_copied")
+
+
+class TruncCfg(ctypes.Structure):
+    _fields_ = [("tau", ctypes.c_float), ("budget", ctypes.c_int32), ("slots", ctypes.c_int32)]
 
 
 class CacheCounts(ctypes.Structure):
@@ -159,6 +165,10 @@ def _load(path: str = LIB_PATH, strict: bool = True):
         "de_cache_stats": (I, [P, KP]),
         "de_cache_slots": (I, [P, I, I32P]),
         "de_spec_step_cached": (I, [MP, P, I, P, P, P, P, P, P, SZ, P]),
+        "de_confidence": (I, [I, I, P, P, P]),
+        "de_expansion": (I, [I, I, I, P, P, I, P, F, I, I, P, P]),
+        "de_spec_step_trunc": (I, [MP, P, I, ctypes.POINTER(TruncCfg), P, P, P, I32P, P, P, P,
+                                   P, P, SZ, P]),
     }
     for name, (res, args) in sig.items():
         if not strict and not hasattr(lib, name):
@@ -471,3 +481,27 @@ def de_spec_step_cached(model, cache, K, block, target_argmax, out, n_union=None
         ctypes.byref(model), cache.handle, int(K), _ptr(block), _ptr(target_argmax), _ptr(out),
         _ptr(n_union), _ptr(pred_idx), _ptr(ws), ws.numel() if ws is not None else 0,
         _stream(stream)))
+
+
+def de_confidence(T, V, logits, q, stream=None):
+    _check("de_confidence", LIB.de_confidence(int(T), int(V), _ptr(logits), _ptr(q),
+                                              _stream(stream)))
+
+
+def de_expansion(L, k, N, pred_idx, uhat, first, q, tau, budget, slots, out, stream=None):
+    _check("de_expansion", LIB.de_expansion(
+        int(L), int(k), int(N), _ptr(pred_idx), _ptr(uhat), int(bool(first)), _ptr(q),
+        float(tau), int(budget), int(slots), _ptr(out), _stream(stream)))
+
+
+def de_spec_step_trunc(model, cache, k_max, tau, budget, slots, block, target_argmax, out,
+                       pred_idx, q, n_union=None, trace=None, ws=None, stream=None) -> int:
+    """Returns the number of kept drafts."""
+    cfg = TruncCfg(float(tau), int(budget), int(slots))
+    nd = ctypes.c_int32(0)
+    _check("de_spec_step_trunc", LIB.de_spec_step_trunc(
+        ctypes.byref(model), cache.handle if cache is not None else None, int(k_max),
+        ctypes.byref(cfg), _ptr(block), _ptr(target_argmax), _ptr(out), ctypes.byref(nd),
+        _ptr(n_union), _ptr(pred_idx), _ptr(q), _ptr(trace), _ptr(ws),
+        ws.numel() if ws is not None else 0, _stream(stream)))
+    return int(nd.value)

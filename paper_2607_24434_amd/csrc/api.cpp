@@ -667,6 +667,34 @@ int de_time_next_phase(int phase, hipEvent_t start, hipEvent_t stop) {
   return DE_OK;
 }
 
+int de_confidence(int T, int V, const float* logits, float* q, hipStream_t stream) {
+  if (T < 1 || T > 65536 || V < 1 || !logits || !q) return DE_ERR_INVALID;
+  return hip_status(de::launch_confidence(T, V, logits, q, stream));
+}
+
+int de_expansion(int L, int k, int N, const int32_t* pred_idx, uint64_t* uhat, int first,
+                 const float* q, float tau, int budget, int slots, int32_t* out,
+                 hipStream_t stream) {
+  if (L < 1 || L > 65536 || N < 1 || N > 256 || k < 1 || k > N) return DE_ERR_INVALID;
+  if (!pred_idx || !uhat || !q || !out || budget < DE_BUDGET_CACHE || slots < 0 ||
+      tau != tau)
+    return DE_ERR_INVALID;
+  if ((reinterpret_cast<uintptr_t>(uhat) & 7u) != 0) return DE_ERR_INVALID;
+  de::ExpansionArgs a{};
+  a.L = L;
+  a.k = k;
+  a.N = N;
+  a.pred = pred_idx;
+  a.uhat = reinterpret_cast<unsigned long long*>(uhat);
+  a.first = first != 0;
+  a.q = q;
+  a.tau = tau;
+  a.budget = budget;
+  a.slots = slots;
+  a.out = out;
+  return hip_status(de::launch_expansion(a, stream));
+}
+
 int de_stream_probe(const void* buf, size_t bytes, float* sink, hipStream_t stream) {
   if (!buf || !sink || bytes == 0 || bytes % 16 || !aligned16(buf)) return DE_ERR_INVALID;
   return hip_status(de::launch_stream_probe(buf, bytes, sink, stream));

@@ -220,4 +220,19 @@ hipError_t launch_embed(int T, int H, int V, const int32_t* tokens, const uint16
                         float* normed, float eps, hipStream_t s);
 hipError_t launch_stream_probe(const void* buf, size_t bytes, float* sink, hipStream_t s);
 
+// Truncation of the draft loop.
+struct ExpansionArgs {
+  int L, k, N;                 // layers, predicted experts per layer, experts per layer (<= 256)
+  const int32_t* pred;         // [L, k] the token's predicted experts
+  unsigned long long* uhat;    // [L, ceil(N / 64)] the block-level predicted set
+  int first;                   // the set is empty before this token
+  const float* q;              // the token's confidence (device scalar)
+  float tau;
+  int budget;                  // >= 0 fixed; < 0 the cache room
+  int slots;
+  int32_t* out;                // [5]
+};
+hipError_t launch_confidence(int T, int V, const float* logits, float* q, hipStream_t s);
+hipError_t launch_expansion(const ExpansionArgs& a, hipStream_t s);
+
 }  // namespace de

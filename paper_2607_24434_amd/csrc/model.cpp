@@ -49,6 +49,7 @@ struct ModelLayout {
   size_t misc;                // int32 [2]: acceptance output of the argmax-only calls
   size_t ridx, rgate;         // top-k lists of the cached step's routing [64, k]
   size_t h, n0, n1, logits;   // residual stream, two normed buffers, logits
+  size_t uhat, tctl;          // truncation: predicted verifier set [L, words], decision [5]
   size_t total;
 };
 
@@ -74,6 +75,8 @@ ModelLayout model_layout(const de_model& m, int T) {
   L.n0 = take((size_t)T * H * 4);
   L.n1 = take((size_t)T * H * 4);
   L.logits = take((size_t)T * m.vocab * 4);
+  L.uhat = take((size_t)m.n_layers * ((m.moe.n_experts + 63) / 64) * 8);
+  L.tctl = take(5 * 4);
   L.total = o;
   return L;
 }
@@ -99,14 +102,15 @@ struct ArgmaxOut {
 
 // MoE layer l with its routed experts behind the cache.  The routing runs
 // first and its lists come back to the host (one synchronisation).  Draft
-// (T = 1): the top-1 expert is requested, the top-k prefetched, then the
+// (T = 1): the top-1 expert is requested, the top-k prefetched (or, with
+// `deferred`, appended there for the caller to prefetch later), then the
 // grouped part runs over the top-1 column.  Verify: the union's members are
 // requested in chunks of at most n_slots (resident or in flight first, then
 // the rest, each in ascending id); every chunk runs gate/up and down over its
 // members, the first also over the shared path, the last also the combine.
 int cached_layer(const de_model& m, de_cache* c, int l, int T, bool draft, const float* x,
                  float* h, float* normed_out, int32_t* n_union, int32_t* pred_out, void* ws,
-                 const ModelLayout& L, hipStream_t s) {
+                 const ModelLayout& L, hipStream_t s, std::vector<int32_t>* deferred) {
   const de_layer_weights& w = m.layers[l];
   const int k = m.moe.top_k, N = m.moe.n_experts;
   const int purpose = draft ? DE_NEED_DRAFT : DE_NEED_VERIFY;
@@ -132,7 +136,10 @@ int cached_layer(const de_model& m, de_cache* c, int l, int T, bool draft, const
   if (draft) {
     const int32_t e1 = hb[0];
     if ((rc = de_cache_ensure(c, l, &e1, 1, DE_NEED_DRAFT, s)) != DE_OK) return rc;
-    if ((rc = de_cache_prefetch(c, l, hb, k)) != DE_OK) return rc;
+    if (deferred != nullptr)
+      deferred->insert(deferred->end(), hb, hb + k);
+    else if ((rc = de_cache_prefetch(c, l, hb, k)) != DE_OK)
+      return rc;
     rc = de::layer_after_route(m.moe, 1, x, &tab, ridx, rgate, 1, w.shared_w, w.draft_w, w.gamma,
                                h, &epi, true, true, nullptr, lws, L.layer_bytes, s);
     if (rc != DE_OK) return rc;
@@ -168,7 +175,8 @@ int cached_layer(const de_model& m, de_cache* c, int l, int T, bool draft, const
 // With a cache the routed experts come through it (cached_layer).
 int forward(const de_model& m, int T, const int32_t* tokens, int mode, float* logits,
             const ArgmaxOut& am, int32_t* n_union, int32_t* pred_idx, size_t pred_stride,
-            void* ws, const ModelLayout& L, hipStream_t s, de_cache* cache = nullptr) {
+            void* ws, const ModelLayout& L, hipStream_t s, de_cache* cache = nullptr,
+            std::vector<int32_t>* deferred = nullptr) {
   const int H = m.moe.hidden;
   float* h = at<float>(ws, L.h);
   float* ncur = at<float>(ws, L.n0);
@@ -189,7 +197,7 @@ int forward(const de_model& m, int T, const int32_t* tokens, int mode, float* lo
     if (cache != nullptr) {
       rc = cached_layer(m, cache, l, T, mode == DE_DRAFT, ncur, h, nnext,
                         mode == DE_TARGET ? n_union : nullptr,
-                        pred_idx ? pred_idx + l * pred_stride : nullptr, ws, L, s);
+                        pred_idx ? pred_idx + l * pred_stride : nullptr, ws, L, s, deferred);
     } else if (mode == DE_TARGET) {
       rc = de_verify_layer(&m.moe, T, ncur, w.w_router, w.bias, &w.routed, w.shared_w, h, nullptr,
                            nullptr, n_union ? n_union + l : nullptr, nullptr, nullptr, nullptr,
@@ -331,6 +339,73 @@ int de_spec_step_cached(const de_model* m, de_cache* cache, int K, int32_t* bloc
   }
   const ArgmaxOut am{target_argmax, out, K > 0 ? block + 1 : nullptr};
   return forward(*m, K + 1, block, DE_TARGET, logits, am, n_union, nullptr, 0, ws, L, stream,
+                 cache);
+}
+
+int de_spec_step_trunc(const de_model* m, de_cache* cache, int k_max, const de_trunc_cfg* cfg,
+                       int32_t* block, int32_t* target_argmax, int32_t* out, int32_t* n_drafted,
+                       int32_t* n_union, int32_t* pred_idx, float* q, int32_t* trace, void* ws,
+                       size_t ws_bytes, hipStream_t stream) {
+  int rc = de_check_model(m);
+  if (rc != DE_OK) return rc;
+  if (cfg == nullptr || cfg->tau != cfg->tau || cfg->budget < DE_BUDGET_CACHE || cfg->slots < 0)
+    return DE_ERR_INVALID;
+  if (k_max < 0 || k_max > 63 || block == nullptr || target_argmax == nullptr ||
+      out == nullptr || n_drafted == nullptr || pred_idx == nullptr || q == nullptr)
+    return DE_ERR_INVALID;
+  if (m->moe.n_experts > 256) return DE_ERR_UNSUPPORTED;
+  int slots = cfg->slots;
+  if (cache != nullptr) {
+    if (de::cache_layers(cache) != m->n_layers || de::cache_experts(cache) != m->moe.n_experts)
+      return DE_ERR_INVALID;
+    for (int l = 0; l < m->n_layers; ++l) {
+      de_expert_table tab;
+      if (de_cache_table(cache, l, &tab) != DE_OK || de::check_table(m->moe, &tab) != DE_OK)
+        return DE_ERR_INVALID;
+    }
+    if (slots == 0) slots = de::cache_slots_per_layer(cache);
+  }
+  if ((rc = check_block(*m, k_max + 1, ws, ws_bytes)) != DE_OK) return rc;
+  const ModelLayout L = model_layout(*m, k_max + 1);
+  float* logits = at<float>(ws, L.logits);
+  int32_t* tctl = at<int32_t>(ws, L.tctl);
+  const int k = m->moe.top_k, NL = m->n_layers;
+  if (cache != nullptr && (rc = de_cache_begin_block(cache)) != DE_OK) return rc;
+  int kept = 0;
+  std::vector<int32_t> deferred;
+  for (int i = 0; i < k_max; ++i) {
+    int32_t* pred = pred_idx + (size_t)i * NL * k;
+    deferred.clear();
+    const ArgmaxOut am{block + i + 1, at<int32_t>(ws, L.misc), nullptr};
+    rc = forward(*m, 1, block + i, DE_DRAFT, logits, am, nullptr, pred, (size_t)k, ws, L, stream,
+                 cache, cache != nullptr ? &deferred : nullptr);
+    if (rc != DE_OK) return rc;
+    if ((rc = de_confidence(1, m->vocab, logits, q + i, stream)) != DE_OK) return rc;
+    // A stack without MoE layers predicts nothing: every token is kept.
+    int32_t dec[5] = {0, 0, 0, 0, 0};
+    if (NL > 0) {
+      rc = de_expansion(NL, k, m->moe.n_experts, pred, at<uint64_t>(ws, L.uhat), i == 0, q + i,
+                        cfg->tau, cfg->budget, slots, tctl, stream);
+      if (rc != DE_OK) return rc;
+      if (trace != nullptr && hipMemcpyAsync(trace + 4 * i, tctl, 16, hipMemcpyDeviceToDevice,
+                                             stream) != hipSuccess)
+        return DE_ERR_HIP;
+      if (hipMemcpyAsync(dec, tctl, sizeof(dec), hipMemcpyDeviceToHost, stream) != hipSuccess ||
+          hipStreamSynchronize(stream) != hipSuccess)
+        return DE_ERR_HIP;
+      if (dec[4] != 0) return DE_ERR_INVALID;
+    }
+    if (dec[1] != 0) break;
+    ++kept;
+    if (cache != nullptr) {
+      for (int l = 0; l < NL; ++l)
+        if ((rc = de_cache_prefetch(cache, l, deferred.data() + (size_t)l * k, k)) != DE_OK)
+          return rc;
+    }
+  }
+  *n_drafted = kept;
+  const ArgmaxOut am{target_argmax, out, kept > 0 ? block + 1 : nullptr};
+  return forward(*m, kept + 1, block, DE_TARGET, logits, am, n_union, nullptr, 0, ws, L, stream,
                  cache);
 }
 
