@@ -79,6 +79,8 @@ def parse():
     p.add_argument("--no-offload", action="store_true",
                    help="skip the expert-cache (offload) step measurement")
     p.add_argument("--offload-steps", type=int, default=3)
+    p.add_argument("--no-verify-side", action="store_true",
+                   help="skip the truncation / prefetch comparison on the offload stack")
     return p.parse_args()
 
 
@@ -468,10 +470,88 @@ def offload_step(args, de, configs, gen, wgpu, torch, np):
         "cold_step_ms": round(cold_ms, 2),
         "cold_bytes_gb": round(cold["bytes_copied"] / 1e9, 3),
     }
+    if not args.no_verify_side:
+        res["verify_side"] = verify_side(args, de, model, dm, cache, gen, torch, np)
     cache.close()
     del dm, t, host
     torch.cuda.empty_cache()
     return res
+
+
+# Confidence threshold of the truncation rows: every token of the random-weight
+# stack is far less confident (its largest draft probability is about 1e-3).
+TRUNC_TAU = 0.5
+
+
+def verify_side(args, de, model, dm, cache, gen, torch, np):
+    """Verify-side cost control on the offload stack: fixed K against
+    confidence-expansion truncation (cache-derived budget), without and with
+    draft-router prefetch, each verify pass's cost relative to one-token
+    autoregressive decoding through the same cache.  Every policy starts from
+    an empty cache, runs one untimed step, then `offload_steps` steps back to
+    back; the verify cost is the time of the verify pass's MoE layers
+    (copy waits included) per step."""
+    K, L, k = model.k_draft, model.n_moe_layers, model.moe.top_k
+    S = args.offload_steps
+    dev = "cuda"
+    policies = [  # name, k_max, tau, budget, prefetch
+        ("ar", 0, 0.0, 0, False),
+        ("fixed_k", K, 0.0, 0, False),
+        ("conf_exp", K, TRUNC_TAU, de.DE_BUDGET_CACHE, False),
+        ("conf_exp_prefetch", K, TRUNC_TAU, de.DE_BUDGET_CACHE, True),
+        ("fixed_k_prefetch", K, 0.0, 0, True),
+    ]
+    rows = {}
+    for name, kmax, tau, budget, pf in policies:
+        cache.reset()
+        block = torch.zeros(kmax + 1, dtype=torch.int32, device=dev)
+        amax = torch.empty(kmax + 1, dtype=torch.int32, device=dev)
+        outv = torch.empty(2, dtype=torch.int32, device=dev)
+        pred = torch.empty(max(1, kmax), L, k, dtype=torch.int32, device=dev)
+        q = torch.empty(max(1, kmax), dtype=torch.float32, device=dev)
+        block[0] = gen.start_token(model)
+        kept, acc, qs = [], [], []
+
+        def one():
+            nd = dm.spec_step_trunc(block, amax, outv, pred, q, tau, budget, 0, cache=cache,
+                                    prefetch=pf)
+            o = outv.cpu().tolist()
+            if kmax > 0:
+                qs.extend(q[:min(kmax, nd + 1)].cpu().tolist())
+            block[0] = o[1]
+            return nd, o[0]
+
+        one()
+        base = cache.stats()
+        t0 = time.perf_counter()
+        for _ in range(S):
+            nd, n = one()
+            kept.append(nd)
+            acc.append(n)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        st = cache.stats()
+        d = {key: st[key] - base[key] for key in st}
+        rows[name] = {
+            "k_max": kmax, "tau": tau, "budget": "cache" if budget < 0 else budget,
+            "prefetch": pf,
+            "drafts_kept_mean": round(float(np.mean(kept)), 2),
+            "accept_mean": round(float(np.mean(acc)), 3),
+            "verify_ms_per_step": round(d["verify_layer_us"] / S / 1e3, 2),
+            "draft_ms_per_step": round(d["draft_layer_us"] / S / 1e3, 2),
+            "stall_ms_per_step": round(d["stall_us"] / S / 1e3, 2),
+            "ms_per_step": round(1e3 * wall / S, 2),
+            "tokens_per_s": round(float(sum(a + 1 for a in acc)) / wall, 2),
+            "prefetch_hit_rate": round(d["prefetch_used"] / max(1, d["prefetch_issued"]), 4),
+            "prefetch_waste_rate": round(d["prefetch_wasted"] / max(1, d["prefetch_issued"]), 4),
+            "host_to_hbm_gb_per_step": round(d["bytes_copied"] / S / 1e9, 3),
+            "q_below_tau": (round(float(np.mean(np.asarray(qs) < tau)), 3) if qs and tau > 0
+                            else None),
+        }
+    ar = rows["ar"]["verify_ms_per_step"]
+    for r in rows.values():
+        r["verify_cost_vs_ar"] = round(r["verify_ms_per_step"] / ar, 2) if ar > 0 else None
+    return rows
 
 
 def cpu_baseline(cfg, x, budget_s):

@@ -427,9 +427,10 @@ int de_expansion(int L, int k, int N, const int32_t* pred_idx, uint64_t* uhat, i
                  hipStream_t stream);
 
 typedef struct {
-  float tau;       /* confidence threshold */
-  int32_t budget;  /* B_i: a fixed count of layer-experts, or DE_BUDGET_CACHE */
-  int32_t slots;   /* slots per layer for DE_BUDGET_CACHE; 0 with a cache: its n_slots */
+  float tau;         /* confidence threshold */
+  int32_t budget;    /* B_i: a fixed count of layer-experts, or DE_BUDGET_CACHE */
+  int32_t slots;     /* slots per layer for DE_BUDGET_CACHE; 0 with a cache: its n_slots */
+  int32_t prefetch;  /* with a cache: nonzero starts the kept tokens' verifier prefetches */
 } de_trunc_cfg;
 
 /* One exact draft-then-verify step with truncation (Algorithm 1): up to
@@ -437,8 +438,9 @@ typedef struct {
  * kept drafts d_1..d_n_drafted are verified as de_spec_step verifies K of
  * them.  With `cache` (may be NULL) the routed experts come through it as in
  * de_spec_step_cached, except that a draft token's verifier prefetches (its
- * top-k in every layer) are started after the token is kept, and a stopped
- * token starts none.
+ * top-k in every layer) are started after the token is kept (only with
+ * cfg->prefetch), and a stopped token starts none.  tau = 0 never stops:
+ * the fixed-K step.
  *   block [k_max+1]: block[0] input; block[1..n_drafted] the kept drafts
  *     (entries after them unspecified);
  *   target_argmax [k_max+1] (first n_drafted+1 written), out [2] = (n, bonus)

@@ -103,7 +103,8 @@ CACHE_COUNTS = ("prefetch_issued", "prefetch_used", "prefetch_wasted", "prefetch
 
 
 class TruncCfg(ctypes.Structure):
-    _fields_ = [("tau", ctypes.c_float), ("budget", ctypes.c_int32), ("slots", ctypes.c_int32)]
+    _fields_ = [("tau", ctypes.c_float), ("budget", ctypes.c_int32), ("slots", ctypes.c_int32),
+                ("prefetch", ctypes.c_int32)]
 
 
 class CacheCounts(ctypes.Structure):
@@ -495,9 +496,10 @@ def de_expansion(L, k, N, pred_idx, uhat, first, q, tau, budget, slots, out, str
 
 
 def de_spec_step_trunc(model, cache, k_max, tau, budget, slots, block, target_argmax, out,
-                       pred_idx, q, n_union=None, trace=None, ws=None, stream=None) -> int:
+                       pred_idx, q, n_union=None, trace=None, ws=None, stream=None,
+                       prefetch=True) -> int:
     """Returns the number of kept drafts."""
-    cfg = TruncCfg(float(tau), int(budget), int(slots))
+    cfg = TruncCfg(float(tau), int(budget), int(slots), int(bool(prefetch)))
     nd = ctypes.c_int32(0)
     _check("de_spec_step_trunc", LIB.de_spec_step_trunc(
         ctypes.byref(model), cache.handle if cache is not None else None, int(k_max),

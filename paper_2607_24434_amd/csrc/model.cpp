@@ -397,7 +397,7 @@ int de_spec_step_trunc(const de_model* m, de_cache* cache, int k_max, const de_t
     }
     if (dec[1] != 0) break;
     ++kept;
-    if (cache != nullptr) {
+    if (cache != nullptr && cfg->prefetch != 0) {
       for (int l = 0; l < NL; ++l)
         if ((rc = de_cache_prefetch(cache, l, deferred.data() + (size_t)l * k, k)) != DE_OK)
           return rc;

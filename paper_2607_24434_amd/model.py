@@ -49,12 +49,13 @@ class DeviceModel:
         L.de_spec_step(self.model, K, block, target_argmax, out, n_union, pred_idx, self.ws, stream)
 
     def spec_step_trunc(self, block, target_argmax, out, pred_idx, q, tau, budget, slots=0,
-                        cache=None, n_union=None, trace=None, stream=None) -> int:
+                        cache=None, n_union=None, trace=None, stream=None,
+                        prefetch=True) -> int:
         """Algorithm 1 with confidence-expansion truncation; returns the kept draft count."""
         k_max = block.numel() - 1
         return L.de_spec_step_trunc(self.model, cache, k_max, tau, budget, slots, block,
                                     target_argmax, out, pred_idx, q, n_union, trace, self.ws,
-                                    stream)
+                                    stream, prefetch)
 
     def forward(self, tokens, mode, logits, argmax=None, n_union=None, stream=None):
         L.de_model_forward(self.model, tokens.numel(), tokens, mode, logits, argmax, n_union,

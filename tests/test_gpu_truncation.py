@@ -154,7 +154,7 @@ def _policies(q, L, k, n_mid):
     return pol
 
 
-def _run_trunc(dm, model, c, tau, budget, slots, cache=None):
+def _run_trunc(dm, model, c, tau, budget, slots, cache=None, prefetch=True):
     K, L, k = model.k_draft, model.n_moe_layers, model.moe.top_k
     block = dm.new_block(K, c)
     amax = torch.full((K + 1,), -7, dtype=torch.int32, device="cuda")
@@ -164,7 +164,7 @@ def _run_trunc(dm, model, c, tau, budget, slots, cache=None):
     q = torch.full((K,), -1.0, dtype=torch.float32, device="cuda")
     tr = torch.full((K, 4), -7, dtype=torch.int32, device="cuda")
     nd = dm.spec_step_trunc(block, amax, out, pred, q, tau, budget, slots, cache=cache,
-                            n_union=nu, trace=tr)
+                            n_union=nu, trace=tr, prefetch=prefetch)
     torch.cuda.synchronize()
     return nd, [x.cpu().numpy() for x in (block, amax, out, nu, pred, q, tr)]
 
@@ -218,12 +218,13 @@ def test_cached_truncated_step_equals_resident_and_simulation():
     # when it adds pairs, the others are kept.
     mids = _mids(qall)
     tau = mids[0] if mids else 2.0
-    for budget in (0, truncation.BUDGET_CACHE):
+    for budget, prefetch in ((0, True), (truncation.BUDGET_CACHE, True), (0, False)):
         traces: list = []
         r = truncation.truncated_step(om.weights, c, K, tau, budget, slots=model.cache_slots,
                                       traces=traces)
         nd_res, res = _run_trunc(dm, model, c, tau, budget, model.cache_slots)
-        nd, got = _run_trunc(dm, model, c, tau, budget, 0, cache=cache)
+        issued = cache.stats()["prefetch_issued"]
+        nd, got = _run_trunc(dm, model, c, tau, budget, 0, cache=cache, prefetch=prefetch)
         assert nd == nd_res == len(r["drafts"])
         for a, b, name in zip(got, res, ("block", "argmax", "out", "n_union", "pred", "q",
                                          "trace")):
@@ -231,9 +232,12 @@ def test_cached_truncated_step_equals_resident_and_simulation():
         ne = len(r["q"])
         draft_topk = [[np.asarray(traces[i].idx[l])[0] for l in range(L)] for i in range(ne)]
         verify_topk = [np.asarray(traces[-1].idx[l]) for l in range(L)]
-        sim.step_truncated(draft_topk, nd, verify_topk)
+        # Without prefetching no token starts a copy before verification.
+        sim.step_truncated(draft_topk, nd if prefetch else 0, verify_topk)
         st = cache.stats()
-        print(f"B {budget}: kept {nd} of {ne} evaluated; {st}", flush=True)
+        print(f"B {budget} prefetch {prefetch}: kept {nd} of {ne} evaluated; {st}", flush=True)
+        if not prefetch:
+            assert st["prefetch_issued"] == issued
         for name in de.CACHE_COUNTS:
             assert st[name] == sim.counts[name], name
     cache.close()
