@@ -135,33 +135,36 @@ class CacheSim:
         for chunk in self.verify_chunks(layer, union):
             self.ensure(layer, chunk, VERIFY)
 
-    def draft_layer(self, layer: int, topk):
+    def draft_layer(self, layer: int, topk, r: int = 1):
+        """The drafter's request (its r routed experts), then the prefetch of
+        the whole top-k."""
         topk = [int(e) for e in topk]
-        self.ensure(layer, [topk[0]], DRAFT)
+        self.ensure(layer, topk[:r], DRAFT)
         self.prefetch(layer, topk)
 
-    def step_truncated(self, draft_topk, n_kept: int, verify_topk):
+    def step_truncated(self, draft_topk, n_kept: int, verify_topk, r: int = 1):
         """One offloaded step with truncation (Algorithm 1 in its own order):
-        every evaluated draft token requests its top-1 expert in each layer;
-        only a kept token (the first n_kept) then prefetches its top-k in
-        every layer, after the keep decision; the stopped token prefetches
+        every evaluated draft token requests its r routed experts in each
+        layer; only a kept token (the first n_kept) then prefetches its top-k
+        in every layer, after the keep decision; the stopped token prefetches
         nothing."""
         self.begin_block()
         for i, per_layer in enumerate(draft_topk):
             for layer, topk in enumerate(per_layer):
-                self.ensure(layer, [int(topk[0])], DRAFT)
+                self.ensure(layer, [int(e) for e in topk[:r]], DRAFT)
             if i < n_kept:
                 for layer, topk in enumerate(per_layer):
                     self.prefetch(layer, topk)
         for layer, lists in enumerate(verify_topk):
             self.verify_layer(layer, [e for row in lists for e in row])
 
-    def step(self, draft_topk, verify_topk):
+    def step(self, draft_topk, verify_topk, r: int = 1):
         """One offloaded step: draft_topk[i][l] the drafter's top-k at draft
-        position i in layer l; verify_topk[l] the verify block's [T, k] lists."""
+        position i in layer l; verify_topk[l] the verify block's [T, k] lists;
+        the drafter requests its r routed experts."""
         self.begin_block()
         for per_layer in draft_topk:
             for layer, topk in enumerate(per_layer):
-                self.draft_layer(layer, topk)
+                self.draft_layer(layer, topk, r)
         for layer, lists in enumerate(verify_topk):
             self.verify_layer(layer, [e for row in lists for e in row])

@@ -44,6 +44,7 @@ class ModelWeights:
     layers: list                           # LayerWeights of MoE layers 1..L
     lm_head: np.ndarray                    # fp64 [V, H]
     eps: float = 1e-6
+    draft_topr: int = 1                    # routed experts per draft layer (Eq. 5: 1)
 
 
 @dataclass
@@ -71,7 +72,7 @@ def forward(model: ModelWeights, tokens, mode: str = "target", trace: Trace | No
         elif mode == "draft":
             y, idx, gate = moe.moe_draft(x, lw.w_router, lw.bias, lw.routed, lw.shared, lw.draft,
                                          lw.gamma, lw.top_k, lw.score_func, lw.norm_topk,
-                                         lw.routed_scale)
+                                         lw.routed_scale, model.draft_topr)
         else:
             raise ValueError(mode)
         if trace is not None:

@@ -176,21 +176,27 @@ def moe_target(x, w_router, bias, routed, shared, top_k: int, score_func: int,
 
 
 def moe_draft(x, w_router, bias, routed, shared, draft, gamma: float, top_k: int,
-              score_func: int, norm_topk: bool, routed_scale: float = 1.0):
+              score_func: int, norm_topk: bool, routed_scale: float = 1.0, r: int = 1):
     """Fixed-footprint draft output of Eq. (5), token by token.
 
     y^d_t = S(x_t) + g_{t,e1} E_{e1}(x_t) + gamma * E^d(x_t), where e1 is the
     expert with the largest selection key and g_{t,e1} is its target gate.
     ``draft`` is the draft expert's (G, U, D) or None (a zero draft expert).
+    With r > 1 the routed term runs over the r experts with the largest keys,
+    each with its target gate: the shared + top-r self-drafter the paper
+    compares against (Section 1, Table 3), with gamma = 0.
     The full top-k is still returned: it is the draft router's prediction of
     the verifier's experts (Section 3.4).  Returns (y, idx, gate).
     """
     x = np.atleast_2d(np.asarray(x, dtype=np.float64))
     idx, gate, _ = route_topk(x, w_router, bias, top_k, score_func, norm_topk, routed_scale)
+    if not 1 <= r <= top_k:
+        raise ValueError("r must lie in [1, top_k]")
     y = shared_path(x, shared)
     for t in range(x.shape[0]):
-        g, u, d = routed(int(idx[t, 0]))
-        y[t] += gate[t, 0] * swiglu(x[t:t + 1], g, u, d)[0]
+        for j in range(r):
+            g, u, d = routed(int(idx[t, j]))
+            y[t] += gate[t, j] * swiglu(x[t:t + 1], g, u, d)[0]
         if draft is not None:
             y[t] += gamma * swiglu(x[t:t + 1], *draft)[0]
     return y, idx, gate
