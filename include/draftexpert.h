@@ -159,6 +159,18 @@ int de_draft_layer(const de_moe_desc* d, int T, const float* x, const float* w_r
                    float* pred_gate, const de_epilogue* epi, void* ws, size_t ws_bytes,
                    hipStream_t stream);
 
+/* The same layer with the r (1 <= r <= k) leading experts of each position
+ * in the routed term, each with its target gate:
+ *   y^d_t = S(x_t) + sum_{j<r} g_{t,j} E_{idx[t,j]}(x_t) + gamma * E^d(x_t).
+ * r = 1 is de_draft_layer; draft_w NULL with r > 1 is the shared + top-r
+ * self-drafter the paper compares with (Section 1, Table 3).  Only the r
+ * experts are read.  DE_ERR_INVALID for r outside [1, k]. */
+int de_draft_layer_topr(const de_moe_desc* d, int T, const float* x, const float* w_router,
+                        const float* bias, const de_expert_table* routed, const void* shared_w,
+                        const void* draft_w, float gamma, int r, float* y, int32_t* pred_idx,
+                        float* pred_gate, const de_epilogue* epi, void* ws, size_t ws_bytes,
+                        hipStream_t stream);
+
 /* Target MoE layer over a verify block of T positions (Eq. 4): routing,
  * union build and the grouped SwiGLU in one call.  Every intermediate output
  * pointer (topk_idx .. pair_pos) may be NULL; non-NULL ones receive the same
@@ -235,6 +247,8 @@ typedef struct de_model {
   const void* dense_w;            /* dense block [G|U|D]; NULL when dense_inter is 0 */
   const void* lm_head;            /* bf16 [V, H] */
   const de_layer_weights* layers; /* HOST array [n_layers]; read during the call only */
+  int32_t draft_topr;             /* routed experts of every draft layer: 1 (Eq. 5, also
+                                     when 0) .. top_k (de_draft_layer_topr) */
 } de_model;
 
 /* Forward modes: the MoE layers as the target (Eq. 4) or the drafter (Eq. 5). */

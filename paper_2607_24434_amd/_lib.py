@@ -34,7 +34,7 @@ C_FUNCS = [
     "de_greedy_decode", "de_cache_create", "de_cache_destroy", "de_cache_reset",
     "de_cache_begin_block", "de_cache_prefetch", "de_cache_ensure", "de_cache_release",
     "de_cache_table", "de_cache_stats", "de_cache_slots", "de_spec_step_cached",
-    "de_confidence", "de_expansion", "de_spec_step_trunc",
+    "de_confidence", "de_expansion", "de_spec_step_trunc", "de_draft_layer_topr",
 ]
 DE_PHASE_GATEUP = 0
 DE_PHASE_DOWN = 1
@@ -84,7 +84,7 @@ class Model(ctypes.Structure):
         ("moe", MoEDesc), ("n_layers", ctypes.c_int32), ("vocab", ctypes.c_int32),
         ("dense_inter", ctypes.c_int32), ("dense_wdtype", ctypes.c_int32), ("eps", ctypes.c_float),
         ("emb", ctypes.c_void_p), ("dense_w", ctypes.c_void_p), ("lm_head", ctypes.c_void_p),
-        ("layers", ctypes.POINTER(LayerWeights)),
+        ("layers", ctypes.POINTER(LayerWeights)), ("draft_topr", ctypes.c_int32),
     ]
 
 
@@ -140,6 +140,7 @@ def _load(path: str = LIB_PATH, strict: bool = True):
         "de_expert_union": (I, [I, I, I, P, P, P, P, P, P, P, P, P]),
         "de_grouped_swiglu": (I, [DP, I, P, TP, P, P, P, P, P, P, P, P, EP, P, SZ, P]),
         "de_draft_layer": (I, [DP, I, P, P, P, TP, P, P, F, P, P, P, EP, P, SZ, P]),
+        "de_draft_layer_topr": (I, [DP, I, P, P, P, TP, P, P, F, I, P, P, P, EP, P, SZ, P]),
         "de_verify_layer": (I, [DP, I, P, P, P, TP, P, P, P, P, P, P, P, P, P, P, EP, P, SZ, P]),
         "de_accept_workspace_bytes": (SZ, [I, I]),
         "de_accept_len": (I, [I, I, P, P, P, P, P, SZ, P]),
@@ -282,6 +283,14 @@ def de_draft_layer(desc, T, x, w_router, bias, table, shared_w, draft_w, gamma, 
         _epi_arg(epi), _ptr(ws), ws.numel(), _stream(stream)))
 
 
+def de_draft_layer_topr(desc, T, x, w_router, bias, table, shared_w, draft_w, gamma, r, y,
+                        pred_idx, pred_gate, ws, epi=None, stream=None):
+    _check("de_draft_layer_topr", LIB.de_draft_layer_topr(
+        ctypes.byref(desc), int(T), _ptr(x), _ptr(w_router), _ptr(bias), ctypes.byref(table),
+        _ptr(shared_w), _ptr(draft_w), float(gamma), int(r), _ptr(y), _ptr(pred_idx),
+        _ptr(pred_gate), _epi_arg(epi), _ptr(ws), ws.numel(), _stream(stream)))
+
+
 def de_verify_layer(desc, T, x, w_router, bias, table, shared_w, y, topk_idx=None, topk_gate=None,
                     n_union=None, union_ids=None, offsets=None, tok_list=None, gate_list=None,
                     pair_pos=None, ws=None, epi=None, stream=None):
@@ -348,7 +357,7 @@ def de_time_next_phase(phase, start_event, stop_event):
 
 
 def make_model(desc, layers, vocab, emb, lm_head, dense_w=None, dense_inter=0,
-               dense_wdtype=DE_BF16, eps=1e-6):
+               dense_wdtype=DE_BF16, eps=1e-6, draft_topr=1):
     """A ``Model`` struct; ``layers`` is a list of dicts with the keys w_router,
     bias, table (an ExpertTable), shared_w, draft_w, gamma.  The returned
     struct keeps the layer array alive."""
@@ -358,7 +367,7 @@ def make_model(desc, layers, vocab, emb, lm_head, dense_w=None, dense_inter=0,
                               _ptr(l.get("shared_w")), _ptr(l.get("draft_w")),
                               float(l.get("gamma", 1.0)))
     m = Model(desc, len(layers), int(vocab), int(dense_inter), int(dense_wdtype), float(eps),
-              _ptr(emb), _ptr(dense_w), _ptr(lm_head), arr)
+              _ptr(emb), _ptr(dense_w), _ptr(lm_head), arr, int(draft_topr))
     m._layers = arr
     return m
 

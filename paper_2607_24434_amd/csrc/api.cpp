@@ -458,14 +458,15 @@ int de_grouped_swiglu(const de_moe_desc* d, int T, const float* x, const de_expe
                      nullptr, stream);
 }
 
-int de_draft_layer(const de_moe_desc* d, int T, const float* x, const float* w_router,
-                   const float* bias, const de_expert_table* routed, const void* shared_w,
-                   const void* draft_w, float gamma, float* y, int32_t* pred_idx,
-                   float* pred_gate, const de_epilogue* epi, void* ws, size_t ws_bytes,
-                   hipStream_t stream) {
+int de_draft_layer_topr(const de_moe_desc* d, int T, const float* x, const float* w_router,
+                        const float* bias, const de_expert_table* routed, const void* shared_w,
+                        const void* draft_w, float gamma, int r, float* y, int32_t* pred_idx,
+                        float* pred_gate, const de_epilogue* epi, void* ws, size_t ws_bytes,
+                        hipStream_t stream) {
   int rc = de_check_desc(d);
   if (rc != DE_OK) return rc;
   if ((rc = check_T(T)) != DE_OK) return rc;
+  if (r < 1 || r > d->top_k) return DE_ERR_INVALID;
   if (!x || !w_router || !y || !aligned16(x) || !aligned16(w_router) || d->hidden % 4)
     return DE_ERR_INVALID;
   if (d->shared_inter > 0 && (shared_w == nullptr || !aligned16(shared_w))) return DE_ERR_INVALID;
@@ -485,7 +486,7 @@ int de_draft_layer(const de_moe_desc* d, int T, const float* x, const float* w_r
   a.routed_scale = d->routed_scale;
   a.idx_out = pred_idx ? pred_idx : at<int32_t>(ws, L.idx);
   a.gate_out = pred_gate ? pred_gate : at<float>(ws, L.gate);
-  a.ucols = 1;  // the drafter reads only the top-1 expert of each position
+  a.ucols = r;  // the drafter reads only the r leading experts of each position
   a.n_union = at<int32_t>(ws, L.nu);
   a.union_ids = at<int32_t>(ws, L.uids);
   a.offsets = at<int32_t>(ws, L.offs);
@@ -495,11 +496,20 @@ int de_draft_layer(const de_moe_desc* d, int T, const float* x, const float* w_r
   a.z = at<float>(ws, L.z);
   // Logits only; the gate/up prologue selects the top-k in every block.
   if (route(*d, T, x, w_router, L, ws, a, stream, false) != hipSuccess) return DE_ERR_HIP;
-  const de::RoutedSrc r = routed_src(*d, T, 1, routed, a.n_union, a.union_ids, a.offsets,
-                                     a.tok_list, a.gate_list, at<float>(ws, L.a_r),
-                                     at<float>(ws, L.p_r));
-  return run_grouped(*d, T, x, r, a.pair_pos, 1, shared_w, draft_w, gamma, y, epi, L, ws, &a,
+  const de::RoutedSrc rs = routed_src(*d, T, r, routed, a.n_union, a.union_ids, a.offsets,
+                                      a.tok_list, a.gate_list, at<float>(ws, L.a_r),
+                                      at<float>(ws, L.p_r));
+  return run_grouped(*d, T, x, rs, a.pair_pos, r, shared_w, draft_w, gamma, y, epi, L, ws, &a,
                      stream, true, true, true);
+}
+
+int de_draft_layer(const de_moe_desc* d, int T, const float* x, const float* w_router,
+                   const float* bias, const de_expert_table* routed, const void* shared_w,
+                   const void* draft_w, float gamma, float* y, int32_t* pred_idx,
+                   float* pred_gate, const de_epilogue* epi, void* ws, size_t ws_bytes,
+                   hipStream_t stream) {
+  return de_draft_layer_topr(d, T, x, w_router, bias, routed, shared_w, draft_w, gamma, 1, y,
+                             pred_idx, pred_gate, epi, ws, ws_bytes, stream);
 }
 
 int de_verify_layer(const de_moe_desc* d, int T, const float* x, const float* w_router,

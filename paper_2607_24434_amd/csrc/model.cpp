@@ -93,6 +93,9 @@ int check_block(const de_model& m, int T, const void* ws, size_t ws_bytes) {
   return DE_OK;
 }
 
+// Routed experts of every draft layer.
+int draft_r(const de_model& m) { return m.draft_topr > 0 ? m.draft_topr : 1; }
+
 // Where the argmax of a forward goes.  amax NULL skips the acceptance launch.
 struct ArgmaxOut {
   int32_t* amax;          // [T]
@@ -134,13 +137,14 @@ int cached_layer(const de_model& m, de_cache* c, int l, int T, bool draft, const
   if ((rc = de_cache_table(c, l, &tab)) != DE_OK) return rc;
   const de_epilogue epi{h, normed_out, m.eps};
   if (draft) {
-    const int32_t e1 = hb[0];
-    if ((rc = de_cache_ensure(c, l, &e1, 1, DE_NEED_DRAFT, s)) != DE_OK) return rc;
+    // The drafter's own experts: its r leading ones.
+    const int r = draft_r(m);
+    if ((rc = de_cache_ensure(c, l, hb, r, DE_NEED_DRAFT, s)) != DE_OK) return rc;
     if (deferred != nullptr)
       deferred->insert(deferred->end(), hb, hb + k);
     else if ((rc = de_cache_prefetch(c, l, hb, k)) != DE_OK)
       return rc;
-    rc = de::layer_after_route(m.moe, 1, x, &tab, ridx, rgate, 1, w.shared_w, w.draft_w, w.gamma,
+    rc = de::layer_after_route(m.moe, 1, x, &tab, ridx, rgate, r, w.shared_w, w.draft_w, w.gamma,
                                h, &epi, true, true, nullptr, lws, L.layer_bytes, s);
     if (rc != DE_OK) return rc;
     if ((rc = de_cache_release(c, l, s)) != DE_OK) return rc;
@@ -203,9 +207,10 @@ int forward(const de_model& m, int T, const int32_t* tokens, int mode, float* lo
                            nullptr, n_union ? n_union + l : nullptr, nullptr, nullptr, nullptr,
                            nullptr, nullptr, &epi, lws, L.layer_bytes, s);
     } else {
-      rc = de_draft_layer(&m.moe, T, ncur, w.w_router, w.bias, &w.routed, w.shared_w, w.draft_w,
-                          w.gamma, h, pred_idx ? pred_idx + l * pred_stride : nullptr, nullptr,
-                          &epi, lws, L.layer_bytes, s);
+      rc = de_draft_layer_topr(&m.moe, T, ncur, w.w_router, w.bias, &w.routed, w.shared_w,
+                               w.draft_w, w.gamma, draft_r(m), h,
+                               pred_idx ? pred_idx + l * pred_stride : nullptr, nullptr, &epi, lws,
+                               L.layer_bytes, s);
     }
     if (rc != DE_OK) return rc;
     std::swap(ncur, nnext);
@@ -238,6 +243,7 @@ int de_check_model(const de_model* m) {
     if (m->dense_w == nullptr || !aligned16(m->dense_w)) return DE_ERR_INVALID;
   }
   if (m->n_layers > 0 && m->layers == nullptr) return DE_ERR_INVALID;
+  if (m->draft_topr < 0 || m->draft_topr > d.top_k) return DE_ERR_INVALID;
   for (int l = 0; l < m->n_layers; ++l) {
     const de_layer_weights& w = m->layers[l];
     if (w.w_router == nullptr || !aligned16(w.w_router) || d.hidden % 4) return DE_ERR_INVALID;

@@ -17,11 +17,13 @@ class DeviceModel:
 
     ``layers`` is a list of dicts with "router" (fp32 [N, H]), "bias" (fp32
     [N] or None), "table" (an ``ExpertTable``) or "routed" (resident [N, block]
-    tensor), "shared", "draft" and optionally "gamma".
+    tensor), "shared", "draft" and optionally "gamma".  ``draft_topr`` is the
+    number of routed experts of every draft layer (1: Eq. 5).
     """
 
     def __init__(self, desc, layers, vocab, emb, lm_head, dense=None, dense_inter=0,
-                 dense_wdtype=L.DE_BF16, eps=1e-6, gamma=1.0, max_block=17, device="cuda"):
+                 dense_wdtype=L.DE_BF16, eps=1e-6, gamma=1.0, max_block=17, device="cuda",
+                 draft_topr=1):
         self.desc = desc
         self.vocab = int(vocab)
         self.n_layers = len(layers)
@@ -36,7 +38,7 @@ class DeviceModel:
                                 gamma=l.get("gamma", gamma)))
         self._keep = (layers, emb, lm_head, dense)
         self.model = L.make_model(desc, entries, vocab, emb, lm_head, dense, dense_inter,
-                                  dense_wdtype, eps)
+                                  dense_wdtype, eps, draft_topr)
         rc = L.de_check_model(self.model)
         if rc != 0:
             L._check("de_check_model", rc)
