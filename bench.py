@@ -81,6 +81,8 @@ def parse():
     p.add_argument("--offload-steps", type=int, default=3)
     p.add_argument("--no-verify-side", action="store_true",
                    help="skip the truncation / prefetch comparison on the offload stack")
+    p.add_argument("--no-draft-side", action="store_true",
+                   help="skip the drafter comparison (top-r against DraftExpert) on the offload stack")
     return p.parse_args()
 
 
@@ -472,6 +474,8 @@ def offload_step(args, de, configs, gen, wgpu, torch, np):
     }
     if not args.no_verify_side:
         res["verify_side"] = verify_side(args, de, model, dm, cache, gen, torch, np)
+    if not args.no_draft_side:
+        res["draft_side"] = draft_side(args, de, model, dm, layers, t, cache, gen, torch, np)
     cache.close()
     del dm, t, host
     torch.cuda.empty_cache()
@@ -551,6 +555,67 @@ def verify_side(args, de, model, dm, cache, gen, torch, np):
     ar = rows["ar"]["verify_ms_per_step"]
     for r in rows.values():
         r["verify_cost_vs_ar"] = round(r["verify_ms_per_step"] / ar, 2) if ar > 0 else None
+    return rows
+
+
+def draft_side(args, de, model, dm, layers, t, cache, gen, torch, np):
+    """Draft-side cost on the offload stack: the shared + top-r self-drafters
+    (r = 1, 2, 3, no draft expert) against DraftExpert's shared + top-1 +
+    draft-expert path, K = 4 drafts per step, no verifier prefetch.  Reported:
+    the drafter's MoE-layer time per draft token (copy waits included)
+    relative to top-1, the unique layer-experts the drafter itself requests
+    per block, and the verify pass's cost relative to one-token decoding."""
+    K, L, k, V = 4, model.n_moe_layers, model.moe.top_k, model.vocab
+    S = args.offload_steps
+    dev = "cuda"
+    m = model.moe
+    drafters = [("top1", 1, False), ("top2", 2, False), ("top3", 3, False),
+                ("draftexpert", 1, True)]
+    rows = {}
+    for name, r, with_draft in drafters:
+        ls = layers if with_draft else [dict(l, draft=None, gamma=0.0) for l in layers]
+        dmr = de.DeviceModel(dm.desc, ls, V, t["emb"], t["lm"], t["dense"], model.dense_inter,
+                             de.DE_BF16, model.eps, m.gamma, K + 1, dev, draft_topr=r)
+        cache.reset()
+        block = torch.zeros(K + 1, dtype=torch.int32, device=dev)
+        amax = torch.empty(K + 1, dtype=torch.int32, device=dev)
+        outv = torch.empty(2, dtype=torch.int32, device=dev)
+        pred = torch.empty(K, L, k, dtype=torch.int32, device=dev)
+        q = torch.empty(K, dtype=torch.float32, device=dev)
+        block[0] = gen.start_token(model)
+        uniq = []
+
+        def one():
+            dmr.spec_step_trunc(block, amax, outv, pred, q, 0.0, 0, 0, cache=cache,
+                                prefetch=False)
+            p = pred.cpu().numpy()
+            uniq.append(len({(l, int(e)) for i in range(K) for l in range(L)
+                             for e in p[i, l, :r]}))
+            block[0] = int(outv[1].item())
+
+        one()
+        uniq.clear()
+        base = cache.stats()
+        t0 = time.perf_counter()
+        for _ in range(S):
+            one()
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        st = cache.stats()
+        d = {key: st[key] - base[key] for key in st}
+        rows[name] = {
+            "routed_experts_per_layer": r, "draft_expert": with_draft,
+            "draft_ms_per_token": round(d["draft_layer_us"] / (S * K) / 1e3, 3),
+            "drafter_layer_experts_per_block": round(float(np.mean(uniq)), 1),
+            "draft_hit_rate": round(d["draft_hits"] / max(1, d["draft_needed"]), 4),
+            "verify_ms_per_step": round(d["verify_layer_us"] / S / 1e3, 2),
+            "ms_per_step": round(1e3 * wall / S, 2),
+            "host_to_hbm_gb_per_step": round(d["bytes_copied"] / S / 1e9, 3),
+        }
+        del dmr
+    top1 = rows["top1"]["draft_ms_per_token"]
+    for r in rows.values():
+        r["draft_cost_vs_top1"] = round(r["draft_ms_per_token"] / top1, 3) if top1 > 0 else None
     return rows
 
 
