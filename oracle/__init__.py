@@ -14,9 +14,10 @@ Modules
                (Section 3.5, Algorithm 1)
     truncation confidence-expansion truncation of the draft loop
                (Section 3.4, Eqs. 12-14, Algorithm 1)
+    q4      dequantisation of Q4_0 expert weights (Section 4.1's 4.5-bit format)
 
 Pins (tests/test_oracle_*.py) tie every function to the paper or to
 mathematics independent of this code; functions without such a pin say
 "parity unpinned" in their docstring.
 """
-from . import cache_sim, decode, moe, truncation  # noqa: F401
+from . import cache_sim, decode, moe, q4, truncation  # noqa: F401

@@ -23,6 +23,8 @@ from __future__ import annotations
 
 import numpy as np
 
+from . import q4
+
 SOFTMAX = 0
 SIGMOID = 1
 
@@ -36,7 +38,10 @@ def to_f64(w: np.ndarray) -> np.ndarray:
 
 
 def split_expert(block: np.ndarray, inter: int, hidden: int):
-    """fp64 (G [I,H], U [I,H], D [H,I]) from a flat ``[G|U|D]`` expert block."""
+    """fp64 (G [I,H], U [I,H], D [H,I]) from a flat ``[G|U|D]`` expert block
+    (uint8 blocks are Q4_0, dequantised by ``oracle.q4``)."""
+    if np.asarray(block).dtype == np.uint8:
+        return q4.split_expert(block, inter, hidden)
     w = to_f64(block)
     n = inter * hidden
     return (w[:n].reshape(inter, hidden), w[n:2 * n].reshape(inter, hidden),

@@ -14,6 +14,7 @@ SOFTMAX = 0
 SIGMOID = 1
 F32 = 0
 BF16 = 1
+Q4_0 = 2    # blocks of 32 weights: 4-bit codes and an fp16 scale (18 bytes per block)
 
 
 @dataclass(frozen=True)
@@ -31,7 +32,7 @@ class MoECfg:
     draft_inter: int        # intermediate size of the draft expert
     score_func: int         # SOFTMAX or SIGMOID
     norm_topk: bool         # renormalise the top-k gates to sum to one
-    wdtype: int             # F32 or BF16 expert weights
+    wdtype: int             # F32, BF16 or Q4_0 expert weights
     weight_std: float       # routed / shared / draft expert weights
     router_std: float       # fp32 router weights
     bias_std: float = 0.0   # per-expert router bias (0 = no bias)
@@ -52,8 +53,15 @@ class MoECfg:
         i = self.inter if inter is None else inter
         return 3 * i * self.hidden
 
+    def mat_bytes(self, rows: int, cols: int) -> int:
+        """Bytes of one [rows, cols] weight matrix in this layer's format."""
+        if self.wdtype == Q4_0:
+            return rows * cols * 9 // 16   # cols / 32 blocks of 16 code bytes + a 2-byte scale
+        return rows * cols * self.welem
+
     def expert_bytes(self, inter: int | None = None) -> int:
-        return self.expert_elems(inter) * self.welem
+        i = self.inter if inter is None else inter
+        return 2 * self.mat_bytes(i, self.hidden) + self.mat_bytes(self.hidden, i)
 
 
 @dataclass(frozen=True)
@@ -129,5 +137,9 @@ def scaled_model(base: ModelCfg, *, n_moe_layers: int | None = None, vocab: int 
         moe=base.moe if moe is None else moe,
     )
 
+
+# The V2-Lite layer with Q4_0 expert weights (the mobile platform's format,
+# Section 4.1): routed, shared and draft experts 4.5 bits per weight.
+CFG2_Q4 = replace(CFG2, name="v2lite-q4", cfg_id=6, wdtype=Q4_0)
 
 ALL_LAYER_CFGS = {"cfg1": CFG1, "cfg2": CFG2, "cfg3": CFG3}

@@ -37,7 +37,48 @@ __global__ void fill_normal_kernel(void* out, int64_t n, int bf16, uint64_t key,
   }
 }
 
+// Raw bytes: byte i is byte (i % 8), little-endian, of output start_word + i / 8.
+__global__ void fill_bytes_kernel(uint8_t* out, int64_t n, uint64_t key, uint64_t start_word) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
+    const uint64_t z = mix64(key + (start_word + (uint64_t)(i >> 3) + 1ull) * kGamma);
+    out[i] = (uint8_t)(z >> (8 * (i & 7)));
+  }
+}
+
+// Q4_0 scale bits: exponent field 7, mantissa the low 10 bits of output i.
+__global__ void fill_q4scale_kernel(uint16_t* out, int64_t n, uint64_t key, uint64_t start) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
+    const uint64_t z = mix64(key + (start + (uint64_t)i + 1ull) * kGamma);
+    out[i] = (uint16_t)((7u << 10) | (uint32_t)(z & 0x3FFu));
+  }
+}
+
+unsigned grid_for(int64_t n) {
+  int64_t blocks = (n + 255) / 256;
+  return (unsigned)(blocks > 65536 ? 65536 : blocks);
+}
+
 }  // namespace
+
+extern "C" int synth_fill_bytes(void* out, int64_t n, uint64_t key, uint64_t start_word,
+                                hipStream_t stream) {
+  if (out == nullptr || n < 0) return -1;
+  if (n == 0) return 0;
+  hipLaunchKernelGGL(fill_bytes_kernel, dim3(grid_for(n)), dim3(256), 0, stream,
+                     static_cast<uint8_t*>(out), n, key, start_word);
+  return hipGetLastError() == hipSuccess ? 0 : -3;
+}
+
+extern "C" int synth_fill_q4scale(void* out, int64_t n, uint64_t key, uint64_t start,
+                                  hipStream_t stream) {
+  if (out == nullptr || n < 0) return -1;
+  if (n == 0) return 0;
+  hipLaunchKernelGGL(fill_q4scale_kernel, dim3(grid_for(n)), dim3(256), 0, stream,
+                     static_cast<uint16_t*>(out), n, key, start);
+  return hipGetLastError() == hipSuccess ? 0 : -3;
+}
 
 extern "C" int synth_fill_normal(void* out, int64_t n, int bf16, uint64_t key, uint64_t start,
                                  double scale, hipStream_t stream) {

@@ -19,7 +19,7 @@ from __future__ import annotations
 import numpy as np
 
 from . import rng
-from .configs import BF16, F32, MoECfg, ModelCfg
+from .configs import BF16, F32, Q4_0, MoECfg, ModelCfg
 
 
 def _weights(cfg_id: int, redraw: int, tag: str, layer: int, index: int, n: int,
@@ -30,20 +30,48 @@ def _weights(cfg_id: int, redraw: int, tag: str, layer: int, index: int, n: int,
     return rng.normal_f32(key, n, std)
 
 
-def routed_block(cfg: MoECfg, layer: int, e: int, redraw: int = 0) -> np.ndarray:
-    """Flat ``[G|U|D]`` block of routed expert ``e`` (uint16 bf16 bits or fp32)."""
-    return _weights(cfg.cfg_id, redraw, "routed", layer, e, cfg.expert_elems(),
+def q4_keys(cfg_id: int, redraw: int, tag: str, layer: int, index: int, part: int):
+    """Stream keys of the codes and the scales of matrix `part` (G 0, U 1, D 2)."""
+    base = (cfg_id, redraw, rng.TAGS[tag], layer, index, 100 + part)
+    return rng.stream_key(*base, 0), rng.stream_key(*base, 1)
+
+
+def q4_matrix(kc: int, ks: int, rows: int, cols: int) -> np.ndarray:
+    """One Q4_0 matrix as bytes: every row's codes (cols / 2 bytes per row,
+    block b of a row at byte 16 b: element j of the block in the low nibble of
+    byte j, element j + 16 in its high nibble), then every row's fp16 scales
+    (cols / 32 per row)."""
+    codes = rng.bytes_u8(kc, rows * cols // 2)
+    scales = rng.q4_scale_bits(ks, rows * cols // 32).view(np.uint8)
+    return np.concatenate([codes, scales])
+
+
+def _q4_block(cfg_id: int, redraw: int, tag: str, layer: int, index: int, inter: int,
+              hidden: int) -> np.ndarray:
+    shapes = ((inter, hidden), (inter, hidden), (hidden, inter))
+    return np.concatenate([q4_matrix(*q4_keys(cfg_id, redraw, tag, layer, index, p), r, c)
+                           for p, (r, c) in enumerate(shapes)])
+
+
+def _block(cfg: MoECfg, tag: str, layer: int, index: int, inter: int, redraw: int):
+    if cfg.wdtype == Q4_0:
+        return _q4_block(cfg.cfg_id, redraw, tag, layer, index, inter, cfg.hidden)
+    return _weights(cfg.cfg_id, redraw, tag, layer, index, cfg.expert_elems(inter),
                     cfg.weight_std, cfg.wdtype)
+
+
+def routed_block(cfg: MoECfg, layer: int, e: int, redraw: int = 0) -> np.ndarray:
+    """Flat ``[G|U|D]`` block of routed expert ``e`` (uint16 bf16 bits, fp32, or
+    Q4_0 bytes: the three matrices one after the other, each as q4_matrix)."""
+    return _block(cfg, "routed", layer, e, cfg.inter, redraw)
 
 
 def shared_block(cfg: MoECfg, layer: int, redraw: int = 0) -> np.ndarray:
-    return _weights(cfg.cfg_id, redraw, "shared", layer, 0, cfg.expert_elems(cfg.shared_inter),
-                    cfg.weight_std, cfg.wdtype)
+    return _block(cfg, "shared", layer, 0, cfg.shared_inter, redraw)
 
 
 def draft_block(cfg: MoECfg, layer: int, redraw: int = 0) -> np.ndarray:
-    return _weights(cfg.cfg_id, redraw, "draft", layer, 0, cfg.expert_elems(cfg.draft_inter),
-                    cfg.weight_std, cfg.wdtype)
+    return _block(cfg, "draft", layer, 0, cfg.draft_inter, redraw)
 
 
 def dense_block(model: ModelCfg, redraw: int = 0) -> np.ndarray:

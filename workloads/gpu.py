@@ -14,7 +14,7 @@ import numpy as np
 import torch
 
 from . import gen, rng
-from .configs import BF16, MoECfg, ModelCfg
+from .configs import BF16, Q4_0, MoECfg, ModelCfg
 
 _LIB = None
 
@@ -30,6 +30,11 @@ def _lib():
         lib.synth_fill_normal.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int,
                                           ctypes.c_uint64, ctypes.c_uint64, ctypes.c_double,
                                           ctypes.c_void_p]
+        for name in ("synth_fill_bytes", "synth_fill_q4scale"):
+            fn = getattr(lib, name)
+            fn.restype = ctypes.c_int
+            fn.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_uint64, ctypes.c_uint64,
+                           ctypes.c_void_p]
         _LIB = lib
     return _LIB
 
@@ -50,10 +55,44 @@ def _wtensor(n: int, wdtype: int, device) -> torch.Tensor:
     return torch.empty(n, dtype=torch.int16 if wdtype == BF16 else torch.float32, device=device)
 
 
+def _call(name, *args):
+    rc = getattr(_lib(), name)(*args, torch.cuda.current_stream().cuda_stream)
+    if rc != 0:
+        raise RuntimeError(f"{name} failed ({rc})")
+
+
+def fill_q4_block(out: torch.Tensor, cfg: MoECfg, tag: str, layer: int, index: int, inter: int,
+                  redraw: int = 0) -> torch.Tensor:
+    """A Q4_0 [G|U|D] block (uint8 device tensor), bit-identical to gen's."""
+    assert out.is_cuda and out.is_contiguous() and out.dtype == torch.uint8
+    H = cfg.hidden
+    off = 0
+    for part, (r, c) in enumerate(((inter, H), (inter, H), (H, inter))):
+        kc, ks = gen.q4_keys(cfg.cfg_id, redraw, tag, layer, index, part)
+        nc, ns = r * c // 2, r * c // 32
+        _call("synth_fill_bytes", out[off:].data_ptr(), nc, kc, 0)
+        _call("synth_fill_q4scale", out[off + nc:].data_ptr(), ns, ks, 0)
+        off += nc + 2 * ns
+    return out
+
+
+def _block(cfg: MoECfg, tag: str, layer: int, index: int, inter: int, device, redraw: int):
+    if cfg.wdtype == Q4_0:
+        out = torch.empty(cfg.expert_bytes(inter), dtype=torch.uint8, device=device)
+        return fill_q4_block(out, cfg, tag, layer, index, inter, redraw)
+    out = _wtensor(cfg.expert_elems(inter), cfg.wdtype, device)
+    return fill_normal(out, rng.key_for(cfg.cfg_id, redraw, tag, layer, index), cfg.weight_std)
+
+
 def routed_experts(cfg: MoECfg, layer: int, device="cuda", redraw: int = 0,
                    n_experts: int | None = None) -> torch.Tensor:
-    """[N, 3*I*H] expert blocks, expert e in row e (the resident layout)."""
+    """[N, block] expert blocks, expert e in row e (the resident layout)."""
     n = cfg.n_experts if n_experts is None else n_experts
+    if cfg.wdtype == Q4_0:
+        out = torch.empty(n, cfg.expert_bytes(), dtype=torch.uint8, device=device)
+        for e in range(n):
+            fill_q4_block(out[e], cfg, "routed", layer, e, cfg.inter, redraw)
+        return out
     out = _wtensor(n * cfg.expert_elems(), cfg.wdtype, device).view(n, -1)
     for e in range(n):
         fill_normal(out[e], rng.key_for(cfg.cfg_id, redraw, "routed", layer, e), cfg.weight_std)
@@ -61,13 +100,11 @@ def routed_experts(cfg: MoECfg, layer: int, device="cuda", redraw: int = 0,
 
 
 def shared_block(cfg: MoECfg, layer: int, device="cuda", redraw: int = 0) -> torch.Tensor:
-    out = _wtensor(cfg.expert_elems(cfg.shared_inter), cfg.wdtype, device)
-    return fill_normal(out, rng.key_for(cfg.cfg_id, redraw, "shared", layer, 0), cfg.weight_std)
+    return _block(cfg, "shared", layer, 0, cfg.shared_inter, device, redraw)
 
 
 def draft_block(cfg: MoECfg, layer: int, device="cuda", redraw: int = 0) -> torch.Tensor:
-    out = _wtensor(cfg.expert_elems(cfg.draft_inter), cfg.wdtype, device)
-    return fill_normal(out, rng.key_for(cfg.cfg_id, redraw, "draft", layer, 0), cfg.weight_std)
+    return _block(cfg, "draft", layer, 0, cfg.draft_inter, device, redraw)
 
 
 def dense_block(model: ModelCfg, device="cuda", redraw: int = 0) -> torch.Tensor:

@@ -178,6 +178,23 @@ def normal_bf16(key: int, n: int, std: float, start: int = 0) -> np.ndarray:
     return _fill_c(lib.synth_normal_bf16, np.empty(n, dtype=np.uint16), key, std, start)
 
 
+def bytes_u8(key: int, n: int, start_word: int = 0) -> np.ndarray:
+    """n raw bytes: the little-endian bytes of outputs start_word, start_word+1, ..."""
+    return raw_bits(key, start_word, (n + 7) // 8).view(np.uint8)[:n].copy()
+
+
+# Q4_0 scales: fp16 2^-8 * (1 + m / 1024) with m 10 random bits (exponent field
+# 7), so that d * (q - 8) over uniform 4-bit codes has a spread like the other
+# synthetic weights (about 0.027).
+Q4_SCALE_EXP = 7
+
+
+def q4_scale_bits(key: int, n: int, start: int = 0) -> np.ndarray:
+    """n fp16 bit patterns of positive Q4_0 block scales."""
+    m = (raw_bits(key, start, n) & np.uint64(0x3FF)).astype(np.uint16)
+    return (np.uint16(Q4_SCALE_EXP << 10) | m).astype(np.uint16)
+
+
 def uniform_int(key: int, n: int, high: int, start: int = 0) -> np.ndarray:
     """n integers in [0, high) (modulo reduction; the bias is < 2^-40 for our ranges)."""
     return (raw_bits(key, start, n) % np.uint64(high)).astype(np.int64)
