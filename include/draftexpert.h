@@ -54,9 +54,22 @@ extern "C" {
 #define DE_SOFTMAX 0 /* scores softmax(z + b); selection key z + b */
 #define DE_SIGMOID 1 /* scores sigmoid(z); selection key sigmoid(z) + b */
 
-/* Expert weight element types. */
+/* Expert weight element types.  An expert block is [G][U][D], G and U
+ * [I, H], D [H, I], each matrix row-major [out, in]:
+ *   DE_F32 / DE_BF16: rows * cols elements of 4 / 2 bytes;
+ *   DE_Q4_0: the 4.5-bit block format of the paper's mobile platform
+ *     (Section 4.1): each row in blocks of 32 weights, a block being 16 bytes
+ *     of 4-bit codes q (byte j: weight j in the low nibble, weight j + 16 in
+ *     the high nibble) and an fp16 scale d, weight = d (q - 8).  A matrix
+ *     stores every row's codes first (cols / 2 bytes per row, block b of a row
+ *     at byte 16 b), then every row's scales (cols / 16 bytes per row): 18
+ *     bytes per 32 weights, rows * cols * 9 / 16 bytes per matrix.  H, I and
+ *     the shared and draft I must be multiples of 32.  Applies to the routed,
+ *     shared and draft experts of a layer; embedding, LM head and the dense
+ *     layer stay bf16. */
 #define DE_F32 0
 #define DE_BF16 1
+#define DE_Q4_0 2
 
 /* Shape and options of one MoE layer. */
 typedef struct de_moe_desc {
@@ -69,7 +82,7 @@ typedef struct de_moe_desc {
   int32_t score_func;   /* DE_SOFTMAX or DE_SIGMOID */
   int32_t norm_topk;    /* 1: divide the k gates by their sum */
   float routed_scale;   /* multiplies every routed gate */
-  int32_t wdtype;       /* DE_F32 or DE_BF16 expert weights */
+  int32_t wdtype;       /* DE_F32, DE_BF16 or DE_Q4_0 expert weights */
 } de_moe_desc;
 
 /* Where routed expert e lives: base + slot_of_expert[e] * slot_stride_bytes.

@@ -23,6 +23,14 @@ DE_SOFTMAX = 0
 DE_SIGMOID = 1
 DE_F32 = 0
 DE_BF16 = 1
+DE_Q4_0 = 2
+
+
+def expert_bytes(wdtype: int, inter: int, hidden: int) -> int:
+    """Bytes of one [G|U|D] expert block in the given weight format."""
+    if wdtype == DE_Q4_0:
+        return 3 * inter * hidden * 9 // 16
+    return 3 * inter * hidden * (2 if wdtype == DE_BF16 else 4)
 
 C_FUNCS = [
     "de_abi_version", "de_error_string", "de_hip_error_detail", "de_check_desc", "de_workspace_bytes",

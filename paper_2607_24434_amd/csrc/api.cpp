@@ -25,12 +25,22 @@ const DevInfo& dev_info() {
   return info[dev];
 }
 
+// Bytes of a [rows, cols] weight matrix and of a [G|U|D] expert block.
+size_t mat_bytes(int wdtype, int rows, int cols) {
+  if (wdtype == DE_Q4_0) return (size_t)rows * cols * 9 / 16;
+  return (size_t)rows * cols * (wdtype == DE_BF16 ? 2 : 4);
+}
+
+size_t expert_bytes(int wdtype, int inter, int hidden) {
+  return 2 * mat_bytes(wdtype, inter, hidden) + mat_bytes(wdtype, hidden, inter);
+}
+
 // Host checks of an expert table against a layer shape (also used by the
 // model calls before they enqueue anything).
 int check_table(const de_moe_desc& d, const de_expert_table* t) {
   if (t == nullptr || t->base == nullptr || (reinterpret_cast<uintptr_t>(t->base) & 15u) != 0)
     return DE_ERR_INVALID;
-  const int64_t need = 3ll * d.inter * d.hidden * (d.wdtype == DE_BF16 ? 2 : 4);
+  const int64_t need = (int64_t)expert_bytes(d.wdtype, d.inter, d.hidden);
   if (t->slot_stride_bytes < need || (t->slot_stride_bytes & 15) != 0) return DE_ERR_INVALID;
   if (t->n_slots < 1) return DE_ERR_INVALID;
   if (t->slot_of_expert == nullptr && t->n_slots < d.n_experts) return DE_ERR_INVALID;
@@ -55,7 +65,8 @@ constexpr int kMaxN = 256;
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 size_t up256(size_t v) { return (v + 255) & ~size_t(255); }
 int elem_bytes(int wdtype) { return wdtype == DE_BF16 ? 2 : 4; }
-int elem_align(int wdtype) { return wdtype == DE_BF16 ? 8 : 4; }
+// Element alignment of every row length (16-byte rows; Q4_0: whole blocks).
+int elem_align(int wdtype) { return wdtype == DE_Q4_0 ? 32 : (wdtype == DE_BF16 ? 8 : 4); }
 
 // The shared path's down projection runs as up to this many dense sources
 // (intermediate chunks), each with its own [T, H] partial.
@@ -197,7 +208,8 @@ int run_grouped(const de_moe_desc& d, int T, const float* x, const de::RoutedSrc
                 float gamma, float* y, const de_epilogue* epi, const Layout& L, void* ws,
                 const de::TopkUnionArgs* fused_sel, hipStream_t s, bool dense_on = true,
                 bool combine_on = true, bool fuse_select = false) {
-  const size_t esz = elem_bytes(d.wdtype);
+  const bool q4 = d.wdtype == DE_Q4_0;
+  const size_t esz = q4 ? 0 : elem_bytes(d.wdtype);
   de::GroupedArgs g{};
   if (fused_sel != nullptr) {
     g.fuse_route = 1;
@@ -238,11 +250,15 @@ int run_grouped(const de_moe_desc& d, int T, const float* x, const de::RoutedSrc
     const int max_chunks = kMaxSharedChunks - ((draft_w != nullptr && d.draft_inter > 0) ? 1 : 0);
     const int chunks = shared_chunks(d.shared_inter, T, max_chunks, elem_align(d.wdtype));
     const int cl = d.shared_inter / chunks;
+    const char* D = static_cast<const char*>(shared_w) +
+                    2 * de::mat_bytes(d.wdtype, d.shared_inter, d.hidden);
     c.n_dense = 0;
     for (int i = 0; i < chunks; ++i) {
       de::DenseSrc& ds = g.dense[nd++];
-      ds.w = static_cast<const char*>(shared_w) + 2 * (size_t)d.shared_inter * d.hidden * esz +
-             (size_t)i * cl * esz;
+      // Columns [i cl, (i+1) cl) of D; Q4_0: their codes, and their scales
+      // after the matrix's codes.
+      ds.w = D + (q4 ? (size_t)i * cl / 2 : (size_t)i * cl * esz);
+      ds.ws = q4 ? D + (size_t)d.hidden * d.shared_inter / 2 + (size_t)i * cl / 16 : nullptr;
       ds.inter = cl;
       ds.ld = d.shared_inter;
       ds.rows = d.hidden;
@@ -256,7 +272,8 @@ int run_grouped(const de_moe_desc& d, int T, const float* x, const de::RoutedSrc
   }
   if (draft_w != nullptr && d.draft_inter > 0) {
     de::DenseSrc& ds = g.dense[nd++];
-    ds.w = static_cast<const char*>(draft_w) + 2 * (size_t)d.draft_inter * d.hidden * esz;
+    ds.w = static_cast<const char*>(draft_w) + 2 * de::mat_bytes(d.wdtype, d.draft_inter, d.hidden);
+    ds.ws = q4 ? static_cast<const char*>(ds.w) + (size_t)d.hidden * d.draft_inter / 2 : nullptr;
     ds.inter = d.draft_inter;
     ds.ld = d.draft_inter;
     ds.rows = d.hidden;
@@ -360,7 +377,8 @@ const char* de_error_string(int code) {
 
 int de_check_desc(const de_moe_desc* d) {
   if (d == nullptr) return DE_ERR_INVALID;
-  if (d->wdtype != DE_F32 && d->wdtype != DE_BF16) return DE_ERR_UNSUPPORTED;
+  if (d->wdtype != DE_F32 && d->wdtype != DE_BF16 && d->wdtype != DE_Q4_0)
+    return DE_ERR_UNSUPPORTED;
   if (d->score_func != DE_SOFTMAX && d->score_func != DE_SIGMOID) return DE_ERR_UNSUPPORTED;
   if (d->norm_topk != 0 && d->norm_topk != 1) return DE_ERR_INVALID;
   if (d->n_experts < 1 || d->n_experts > kMaxN) return DE_ERR_INVALID;

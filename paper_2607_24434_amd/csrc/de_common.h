@@ -95,6 +95,7 @@ struct DenseSrc {
   int vin_stride;
   float* out;        // gate/up: A [T, inter]; down: P [T, out_stride]
   int out_stride;
+  const void* ws;    // down, Q4_0 weights: the scales of the matrix's first row
 };
 
 // The routed part of a grouped launch: the union members and their lists.

@@ -29,9 +29,11 @@
 //    steps inside 16 lanes and two cross-row shuffles, identical in every
 //    lane.  No float atomics: results are bitwise reproducible.
 #include "de_common.h"
+#include "draftexpert.h"
 #include "topk_union.h"
 
 #include <mutex>
+#include <type_traits>
 #include <utility>
 #include <vector>
 
@@ -77,6 +79,48 @@ struct WTr<float> {
   static constexpr int EPU = 4;
 };
 
+// Q4_0 weights: blocks of 32 weights of a row, 16 bytes of 4-bit codes q
+// (byte j: weight j in the low nibble, weight j + 16 in the high one) and an
+// fp16 scale d; weight = d (q - 8).  A [rows, cols] matrix holds every row's
+// codes (cols / 2 bytes per row), then every row's scales (cols / 16 bytes).
+struct q4_t {};
+template <>
+struct WTr<q4_t> {
+  static constexpr int EPU = 32;
+};
+
+template <typename WT>
+constexpr bool kQ4 = std::is_same_v<WT, q4_t>;
+
+// Positions per pass and ring depth.  Q4_0 units carry four times the
+// weights of a bf16 unit (and its arithmetic): fewer positions per pass and a
+// shallower ring keep the unrolled stream in registers, and the 16-byte loads
+// in flight per wave (2 x 4 KB) still cover the memory latency.
+template <typename WT>
+constexpr int kDenseNTOf = kQ4<WT> ? 5 : kDenseNT;
+template <typename WT>
+constexpr int kRoutedNTOf = kQ4<WT> ? 2 : kRoutedNT;
+template <typename WT>
+constexpr int kRingOf = kQ4<WT> ? 2 : kRing;
+
+// Bytes per row of a matrix's codes (or plain values).
+template <typename WT>
+__host__ __device__ __forceinline__ size_t qrow_bytes(int cols) {
+  if constexpr (kQ4<WT>)
+    return (size_t)cols / 2;
+  else
+    return (size_t)cols * sizeof(WT);
+}
+
+// Bytes of a [rows, cols] matrix.
+template <typename WT>
+__host__ __device__ __forceinline__ size_t mat_bytes(int rows, int cols) {
+  if constexpr (kQ4<WT>)
+    return (size_t)rows * cols * 9 / 16;
+  else
+    return (size_t)rows * cols * sizeof(WT);
+}
+
 __device__ __forceinline__ u32x4 load_w16(const void* p) {
 #if DE_NT_LOADS
   return load_stream16(p);
@@ -112,24 +156,43 @@ __device__ __forceinline__ int perm_index(int u, int half) {
   return (((u >> 4) * 2 + half) * 16 + (u & 15)) * 4;
 }
 
+// Q4_0 weights (32 per unit): a unit's 32 floats are contiguous and units
+// are 36 floats apart, so that 16 lanes reading 16 bytes each at the same
+// offset within their units hit 64 distinct banks.
 template <int EPU>
 __host__ __device__ __forceinline__ int staged_stride(int len) {
+  if (EPU == 32) return (len / 32) * 36;
   return EPU == 8 ? ((len + 127) / 128) * 128 : len;
+}
+
+// LDS float offset of float4 h4 of a staged row.
+template <int EPU>
+__device__ __forceinline__ int staged_f4(int h4) {
+  if constexpr (EPU == 8) return perm_index(h4 >> 1, h4 & 1);
+  if constexpr (EPU == 32) return (h4 >> 3) * 36 + (h4 & 7) * 4;
+  return h4 * 4;
 }
 
 // The EPU activations that meet weight unit u of one row: from LDS (staged
 // layout, row at float offset `off`) when g is null, else from global memory
 // (natural layout).
+// Staged offsets are multiples of 4 floats; indexing LDS as float4 lets the
+// compiler use 16-byte reads (a float pointer plus an offset it cannot prove
+// aligned is read as pairs of dwords).
+__device__ __forceinline__ float4 lds4(int off_floats) {
+  return reinterpret_cast<const float4*>(s_dyn)[off_floats >> 2];
+}
+
 template <int EPU>
 __device__ __forceinline__ void act_frag(const float* g, int off, int u, float (&v)[EPU]) {
   if (g == nullptr) {
     if constexpr (EPU == 8) {
-      const float4 a = *reinterpret_cast<const float4*>(&s_dyn[off + perm_index(u, 0)]);
-      const float4 b = *reinterpret_cast<const float4*>(&s_dyn[off + perm_index(u, 1)]);
+      const float4 a = lds4(off + perm_index(u, 0));
+      const float4 b = lds4(off + perm_index(u, 1));
       v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
       v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
     } else {
-      const float4 a = *reinterpret_cast<const float4*>(&s_dyn[off + u * 4]);
+      const float4 a = lds4(off + u * 4);
       v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
     }
   } else {
@@ -145,6 +208,27 @@ __device__ __forceinline__ void act_frag(const float* g, int off, int u, float (
   }
 }
 
+// Half h (weights 16 h .. 16 h + 15) of the 32 activations that meet Q4_0
+// unit u: from LDS (staged layout, units 36 floats apart) when g is null,
+// else from global memory.
+__device__ __forceinline__ void act_half_q4(const float* g, int off, int u, int h,
+                                            float (&v)[16]) {
+  if (g == nullptr) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float4 a = lds4(off + u * 36 + 16 * h + 4 * i);
+      v[4 * i + 0] = a.x; v[4 * i + 1] = a.y; v[4 * i + 2] = a.z; v[4 * i + 3] = a.w;
+    }
+  } else {
+    const DE_GLOBAL f32x4* q = gptr<f32x4>(g + off + u * 32 + 16 * h);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const f32x4 t = q[i];
+      v[4 * i + 0] = t.x; v[4 * i + 1] = t.y; v[4 * i + 2] = t.z; v[4 * i + 3] = t.w;
+    }
+  }
+}
+
 // Copies `rows` activation rows of length len (fp32, row stride gstride) into
 // LDS in the staged layout (row stride staged_stride(len)).  All threads; the
 // caller synchronises before the rows are read.
@@ -155,7 +239,7 @@ __device__ __forceinline__ void stage_rows(const float* g, int gstride, int rows
   for (int i = threadIdx.x; i < rows * l4; i += kBlock) {
     const int t = i / l4, h4 = i - t * l4;
     const f32x4 v = gptr<f32x4>(g + (size_t)t * gstride)[h4];
-    const int dst = t * sst + (EPU == 8 ? perm_index(h4 >> 1, h4 & 1) : h4 * 4);
+    const int dst = t * sst + staged_f4<EPU>(h4);
     *reinterpret_cast<f32x4*>(&s_dyn[dst]) = v;
   }
 }
@@ -169,7 +253,7 @@ __device__ __forceinline__ void stage_rows_at(float* dst, const float* g, int gs
   for (int i = threadIdx.x; i < rows * l4; i += kBlock) {
     const int t = i / l4, h4 = i - t * l4;
     const f32x4 v = gptr<f32x4>(g + (size_t)t * gstride)[h4];
-    const int o = t * sst + (EPU == 8 ? perm_index(h4 >> 1, h4 & 1) : h4 * 4);
+    const int o = t * sst + staged_f4<EPU>(h4);
     *reinterpret_cast<f32x4*>(dst + o) = v;
   }
 }
@@ -272,6 +356,7 @@ __device__ __forceinline__ DenseSrc dense_at(const Tables& tb, int s) {
   d.vin_stride = uni(g.vin_stride);
   d.out = uni(g.out);
   d.out_stride = uni(g.out_stride);
+  d.ws = uni(g.ws);
   return d;
 }
 
@@ -321,6 +406,7 @@ __device__ __forceinline__ int routed_count(const GroupedArgs& a) {
 template <int NT>
 struct Pass {
   const char* row[kNS];
+  const char* srow[kNS];  // Q4_0: the rows' scales
   int L;               // 16-byte units per row
   int nit;             // wave iterations: ceil(L / 64)
   int nt;              // positions
@@ -398,7 +484,6 @@ struct Walker {
   // Fills p for tile c.tile at position c.m0; c.ntok receives the tile's
   // position count.  False when the tile's member is not resident.
   __device__ __forceinline__ bool make(const GroupedArgs& a, Cursor& c, Pass<NT>& p) const {
-    constexpr size_t esz = sizeof(WT);
     constexpr int EPU = WTr<WT>::EPU;
     const int H = a.H;
     if (c.tile >= ly.ndt) {
@@ -413,8 +498,8 @@ struct Walker {
       p.nt = min(NT, c.ntok - c.m0);
       p.orow0 = off + c.m0;
       if constexpr (GATEUP) {
-        const size_t rb = (size_t)H * esz;
-        const char* U = blk + (size_t)I * rb;
+        const size_t rb = qrow_bytes<WT>(H);
+        const char* U = blk + mat_bytes<WT>(I, H);
         p.r0 = rg * (RT / 2);
         p.rows = I;
 #pragma unroll
@@ -422,6 +507,10 @@ struct Walker {
           const size_t rc = (size_t)min(p.r0 + q, I - 1);
           p.row[2 * q] = blk + rc * rb;
           p.row[2 * q + 1] = U + rc * rb;
+          if constexpr (kQ4<WT>) {
+            p.srow[2 * q] = blk + (size_t)I * rb + rc * (H / 16);
+            p.srow[2 * q + 1] = U + (size_t)I * rb + rc * (H / 16);
+          }
         }
         p.L = (int)(rb / 16);
         p.act = xlds ? nullptr : a.x;
@@ -431,12 +520,16 @@ struct Walker {
         p.ostride = I;
         p.goff = -1;
       } else {
-        const size_t rb = (size_t)I * esz;
-        const char* D = blk + 2 * (size_t)I * H * esz;
+        const size_t rb = qrow_bytes<WT>(I);
+        const char* D = blk + 2 * mat_bytes<WT>(I, H);
         p.r0 = rg * RT;
         p.rows = H;
 #pragma unroll
-        for (int k = 0; k < RT; ++k) p.row[k] = D + (size_t)min(p.r0 + k, H - 1) * rb;
+        for (int k = 0; k < RT; ++k) {
+          const size_t r = (size_t)min(p.r0 + k, H - 1);
+          p.row[k] = D + r * rb;
+          if constexpr (kQ4<WT>) p.srow[k] = D + (size_t)H * rb + r * (I / 16);
+        }
         p.L = (int)(rb / 16);
         const int act = uni(mb.act);
         if (act >= 0) {
@@ -464,8 +557,8 @@ struct Walker {
       p.orow0 = c.m0;
       const char* W = static_cast<const char*>(d.w);
       if constexpr (GATEUP) {
-        const size_t rb = (size_t)H * esz;
-        const char* U = W + (size_t)d.inter * rb;
+        const size_t rb = qrow_bytes<WT>(H);
+        const char* U = W + mat_bytes<WT>(d.inter, H);
         p.r0 = rg * (RT / 2);
         p.rows = d.inter;
 #pragma unroll
@@ -473,6 +566,10 @@ struct Walker {
           const size_t rc = (size_t)min(p.r0 + q, d.inter - 1);
           p.row[2 * q] = W + rc * rb;
           p.row[2 * q + 1] = U + rc * rb;
+          if constexpr (kQ4<WT>) {
+            p.srow[2 * q] = W + (size_t)d.inter * rb + rc * (H / 16);
+            p.srow[2 * q + 1] = U + (size_t)d.inter * rb + rc * (H / 16);
+          }
         }
         p.L = (int)(rb / 16);
         p.act = xlds ? nullptr : a.x;
@@ -481,12 +578,17 @@ struct Walker {
         p.out = d.out;
         p.ostride = d.inter;
       } else {
-        const size_t rb = (size_t)(d.ld > 0 ? d.ld : d.inter) * esz;
+        const int ldc = d.ld > 0 ? d.ld : d.inter;
+        const size_t rb = qrow_bytes<WT>(ldc);
         p.r0 = rg * RT;
         p.rows = d.rows;
 #pragma unroll
-        for (int k = 0; k < RT; ++k) p.row[k] = W + (size_t)min(p.r0 + k, d.rows - 1) * rb;
-        p.L = (int)((size_t)d.inter * esz / 16);
+        for (int k = 0; k < RT; ++k) {
+          const size_t r = (size_t)min(p.r0 + k, d.rows - 1);
+          p.row[k] = W + r * rb;
+          if constexpr (kQ4<WT>) p.srow[k] = static_cast<const char*>(d.ws) + r * (ldc / 16);
+        }
+        p.L = (int)(qrow_bytes<WT>(d.inter) / 16);
         const int act = dact;
         if (act >= 0) {
           const int sst = staged_stride<EPU>(d.inter);
@@ -527,18 +629,28 @@ struct Walker {
   }
 };
 
-// Loads iteration `it` of pass p (RT rows) into r.  Past a row's end the lane
-// re-reads the last unit (always in bounds); consume() zeroes it.
-template <int NT, int RT>
-__device__ __forceinline__ void issue(const Pass<NT>& p, int it, u32x4 (&r)[RT], int lane) {
-  const uint32_t uc = (uint32_t)min(it * kWave + lane, p.L - 1) * 16u;
+// Loads iteration `it` of pass p (RT rows) into r (Q4_0: the units' scales
+// into sc).  Past a row's end the lane re-reads the last unit (always in
+// bounds); consume() zeroes it.
+template <typename WT, int NT, int RT>
+__device__ __forceinline__ void issue(const Pass<NT>& p, int it, u32x4 (&r)[RT],
+                                      uint32_t (&sc)[RT], int lane) {
+  const uint32_t u = (uint32_t)min(it * kWave + lane, p.L - 1);
 #pragma unroll
-  for (int k = 0; k < RT; ++k) r[k] = load_w16(p.row[k] + uc);
+  for (int k = 0; k < RT; ++k) {
+    r[k] = load_w16(p.row[k] + u * 16u);
+    if constexpr (kQ4<WT>) sc[k] = *gptr<uint16_t>(p.srow[k] + u * 2u);
+  }
+}
+
+__device__ __forceinline__ float half_bits_to_float(uint32_t h) {
+  return (float)__builtin_bit_cast(_Float16, (unsigned short)h);
 }
 
 // Accumulates iteration `it` of pass p.
 template <typename WT, int NT, int RT>
-__device__ __forceinline__ void consume(const Pass<NT>& p, int it, const u32x4 (&r)[RT], int lane,
+__device__ __forceinline__ void consume(const Pass<NT>& p, int it, const u32x4 (&r)[RT],
+                                        const uint32_t (&sc)[RT], int lane,
                                         float (&acc)[RT][NT]) {
   constexpr int EPU = WTr<WT>::EPU;
   const int u = it * kWave + lane;
@@ -547,15 +659,52 @@ __device__ __forceinline__ void consume(const Pass<NT>& p, int it, const u32x4 (
 #pragma unroll
   for (int m = 0; m < NT; ++m) {
     if (m < p.nt) {
-      float xv[EPU];
-      act_frag<EPU>(p.act, p.vo[m], uc, xv);
+      if constexpr (kQ4<WT>) {
+        // sum_e d (q_e - 8) x_e = d (sum_e q_e x_e - 8 sum_e x_e), in two
+        // halves: weights 0..15 of the unit are the low nibbles of its 16
+        // bytes, weights 16..31 the high nibbles.
+        float qx[RT], xs = 0.f;
 #pragma unroll
-      for (int k = 0; k < RT; ++k) {
-        const u32x4 rr = ok ? r[k] : u32x4{0u, 0u, 0u, 0u};
-        float w[EPU];
-        unpack(rr, w);
+        for (int k = 0; k < RT; ++k) qx[k] = 0.f;
 #pragma unroll
-        for (int v = 0; v < EPU; ++v) acc[k][m] = fmaf(w[v], xv[v], acc[k][m]);
+        for (int h = 0; h < 2; ++h) {
+          float xv[16];
+          act_half_q4(p.act, p.vo[m], uc, h, xv);
+#pragma unroll
+          for (int v = 0; v < 16; ++v) xs += xv[v];
+#pragma unroll
+          for (int k = 0; k < RT; ++k) {
+            uint32_t wd[4] = {r[k].x, r[k].y, r[k].z, r[k].w};
+            // Converted codes are not kept across positions (4 x 32 floats
+            // would not fit in registers): each position converts again.
+            asm volatile("" : "+v"(wd[0]), "+v"(wd[1]), "+v"(wd[2]), "+v"(wd[3]));
+#pragma unroll
+            for (int w = 0; w < 4; ++w) {
+              const uint32_t nib = (h ? wd[w] >> 4 : wd[w]) & 0x0F0F0F0Fu;
+#pragma unroll
+              for (int b = 0; b < 4; ++b)
+                qx[k] = fmaf((float)((nib >> (8 * b)) & 0xFFu), xv[4 * w + b], qx[k]);
+            }
+          }
+        }
+#pragma unroll
+        for (int k = 0; k < RT; ++k) {
+          // A lane past the row's end re-read the last unit: scale 0.
+          const float d = ok ? half_bits_to_float(sc[k]) : 0.f;
+          acc[k][m] = fmaf(d, fmaf(-8.f, xs, qx[k]), acc[k][m]);
+        }
+
+      } else {
+        float xv[EPU];
+        act_frag<EPU>(p.act, p.vo[m], uc, xv);
+#pragma unroll
+        for (int k = 0; k < RT; ++k) {
+          const u32x4 rr = ok ? r[k] : u32x4{0u, 0u, 0u, 0u};
+          float w[EPU];
+          unpack(rr, w);
+#pragma unroll
+          for (int v = 0; v < EPU; ++v) acc[k][m] = fmaf(w[v], xv[v], acc[k][m]);
+        }
       }
     }
     // Keeps the next position's activation loads from being hoisted above
@@ -612,10 +761,11 @@ __device__ __forceinline__ void run_stream(const GroupedArgs& a,
   bool c_ok = wk.seek(a, cc, cp);
   int l_it = 0, c_it = 0;
   u32x4 raw[RING][RT];
+  uint32_t sraw[RING][RT];
 #pragma unroll
   for (int q = 0; q < RING; ++q) {
     if (l_ok) {
-      issue(lp, l_it, raw[q], lane);
+      issue<WT>(lp, l_it, raw[q], sraw[q], lane);
       if (++l_it == lp.nit) {
         l_ok = wk.next(a, lc, lp);
         l_it = 0;
@@ -631,7 +781,7 @@ __device__ __forceinline__ void run_stream(const GroupedArgs& a,
 #pragma unroll
     for (int q = 0; q < RING; ++q) {
       if (c_ok) {
-        consume<WT, NT, RT>(cp, c_it, raw[q], lane, acc);
+        consume<WT, NT, RT>(cp, c_it, raw[q], sraw[q], lane, acc);
         if (++c_it == cp.nit) {
           finish<GATEUP, NT, RT>(cp, wk.tb, lane, acc);
           const int prev_tile = cc.tile;
@@ -640,7 +790,7 @@ __device__ __forceinline__ void run_stream(const GroupedArgs& a,
           // Dense sources over many positions are arithmetic-heavy: a wave
           // with more tiles left gets a higher issue priority, so the waves
           // of a CU finish together instead of the oldest first.
-          if (NT == kDenseNT && a.T >= 8 && c_ok && cc.tile != prev_tile) {
+          if (NT == kDenseNTOf<WT> && a.T >= 8 && c_ok && cc.tile != prev_tile) {
             const int rem = (wk.hi - 1 - cc.tile) / wk.step;
             if (rem >= 3)
               __builtin_amdgcn_s_setprio(3);
@@ -653,7 +803,7 @@ __device__ __forceinline__ void run_stream(const GroupedArgs& a,
           }
         }
         if (l_ok) {
-          issue(lp, l_it, raw[q], lane);
+          issue<WT>(lp, l_it, raw[q], sraw[q], lane);
           if (++l_it == lp.nit) {
             l_ok = wk.next(a, lc, lp);
             l_it = 0;
@@ -672,14 +822,16 @@ __device__ __forceinline__ void run_tiles(const GroupedArgs& a, const Layout ly,
   const int step = (int)gridDim.x * kWavesPB;
   const int first = (int)blockIdx.x * kWavesPB + wave;
   if (first < ly.ndt) {
-    const Walker<WT, GATEUP, kDenseNT, RT> wd{ly, tb, step, 0, ly.ndt, xstride, xlds};
-    run_stream<WT, GATEUP, kDenseNT, kDenseRing, RT>(a, wd, first, lane);
+    constexpr int DNT = kDenseNTOf<WT>;
+    const Walker<WT, GATEUP, DNT, RT> wd{ly, tb, step, 0, ly.ndt, xstride, xlds};
+    run_stream<WT, GATEUP, DNT, kDenseRing, RT>(a, wd, first, lane);
   }
   __builtin_amdgcn_s_setprio(0);
   if (ly.nr > 0) {
     const int f2 = first >= ly.ndt ? first : first + cdiv(ly.ndt - first, step) * step;
-    const Walker<WT, GATEUP, kRoutedNT, RT> wr{ly, tb, step, ly.ndt, ly.total, xstride, xlds};
-    run_stream<WT, GATEUP, kRoutedNT, kRing, RT>(a, wr, f2, lane);
+    constexpr int RNT = kRoutedNTOf<WT>;
+    const Walker<WT, GATEUP, RNT, RT> wr{ly, tb, step, ly.ndt, ly.total, xstride, xlds};
+    run_stream<WT, GATEUP, RNT, kRingOf<WT>, RT>(a, wr, f2, lane);
   }
 }
 
@@ -1037,11 +1189,13 @@ hipError_t allow_lds(const void* fn, size_t lds) {
 }
 
 hipError_t launch_gateup(const GroupedArgs& a, int wdtype, hipStream_t s) {
-  return wdtype == 1 ? gateup_typed<uint16_t>(a, s) : gateup_typed<float>(a, s);
+  if (wdtype == DE_Q4_0) return gateup_typed<q4_t>(a, s);
+  return wdtype == DE_BF16 ? gateup_typed<uint16_t>(a, s) : gateup_typed<float>(a, s);
 }
 
 hipError_t launch_down(const GroupedArgs& a, int wdtype, hipStream_t s) {
-  return wdtype == 1 ? down_typed<uint16_t>(a, s) : down_typed<float>(a, s);
+  if (wdtype == DE_Q4_0) return down_typed<q4_t>(a, s);
+  return wdtype == DE_BF16 ? down_typed<uint16_t>(a, s) : down_typed<float>(a, s);
 }
 
 hipError_t launch_combine(const CombineArgs& a, hipStream_t s) {

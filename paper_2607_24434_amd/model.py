@@ -27,7 +27,7 @@ class DeviceModel:
         self.desc = desc
         self.vocab = int(vocab)
         self.n_layers = len(layers)
-        stride = 3 * desc.inter * desc.hidden * (2 if desc.wdtype == L.DE_BF16 else 4)
+        stride = L.expert_bytes(desc.wdtype, desc.inter, desc.hidden)
         entries = []
         for l in layers:
             table = l.get("table")

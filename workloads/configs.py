@@ -138,8 +138,9 @@ def scaled_model(base: ModelCfg, *, n_moe_layers: int | None = None, vocab: int 
     )
 
 
-# The V2-Lite layer with Q4_0 expert weights (the mobile platform's format,
+# The tiny layer and the V2-Lite layer with Q4_0 expert weights (the mobile platform's format,
 # Section 4.1): routed, shared and draft experts 4.5 bits per weight.
+CFG1_Q4 = replace(CFG1, name="tiny-q4", cfg_id=7, wdtype=Q4_0)
 CFG2_Q4 = replace(CFG2, name="v2lite-q4", cfg_id=6, wdtype=Q4_0)
 
 ALL_LAYER_CFGS = {"cfg1": CFG1, "cfg2": CFG2, "cfg3": CFG3}
