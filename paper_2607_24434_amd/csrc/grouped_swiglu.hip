@@ -97,7 +97,7 @@ constexpr bool kQ4 = std::is_same_v<WT, q4_t>;
 // shallower ring keep the unrolled stream in registers, and the 16-byte loads
 // in flight per wave (2 x 4 KB) still cover the memory latency.
 template <typename WT>
-constexpr int kDenseNTOf = kQ4<WT> ? 5 : kDenseNT;
+constexpr int kDenseNTOf = kQ4<WT> ? 3 : kDenseNT;
 template <typename WT>
 constexpr int kRoutedNTOf = kQ4<WT> ? 2 : kRoutedNT;
 template <typename WT>
@@ -156,20 +156,22 @@ __device__ __forceinline__ int perm_index(int u, int half) {
   return (((u >> 4) * 2 + half) * 16 + (u & 15)) * 4;
 }
 
-// Q4_0 weights (32 per unit): a unit's 32 floats are contiguous and units
-// are 36 floats apart, so that 16 lanes reading 16 bytes each at the same
-// offset within their units hit 64 distinct banks.
+// Q4_0 weights (32 per unit): unit u's 32 floats stay in its own 128 bytes,
+// its float4 j stored at slot (j + u / 2) mod 8, so that 16 lanes reading
+// float4 j of 16 consecutive units hit 64 distinct banks (no padding: the
+// rows of a 9-position block still fit two blocks per CU).
 template <int EPU>
 __host__ __device__ __forceinline__ int staged_stride(int len) {
-  if (EPU == 32) return (len / 32) * 36;
   return EPU == 8 ? ((len + 127) / 128) * 128 : len;
 }
+
+__device__ __forceinline__ int q4_slot(int u, int j) { return u * 32 + 4 * ((j + (u >> 1)) & 7); }
 
 // LDS float offset of float4 h4 of a staged row.
 template <int EPU>
 __device__ __forceinline__ int staged_f4(int h4) {
   if constexpr (EPU == 8) return perm_index(h4 >> 1, h4 & 1);
-  if constexpr (EPU == 32) return (h4 >> 3) * 36 + (h4 & 7) * 4;
+  if constexpr (EPU == 32) return q4_slot(h4 >> 3, h4 & 7);
   return h4 * 4;
 }
 
@@ -209,14 +211,13 @@ __device__ __forceinline__ void act_frag(const float* g, int off, int u, float (
 }
 
 // Half h (weights 16 h .. 16 h + 15) of the 32 activations that meet Q4_0
-// unit u: from LDS (staged layout, units 36 floats apart) when g is null,
-// else from global memory.
+// unit u: from LDS (staged layout) when g is null, else from global memory.
 __device__ __forceinline__ void act_half_q4(const float* g, int off, int u, int h,
                                             float (&v)[16]) {
   if (g == nullptr) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const float4 a = lds4(off + u * 36 + 16 * h + 4 * i);
+      const float4 a = lds4(off + q4_slot(u, 4 * h + i));
       v[4 * i + 0] = a.x; v[4 * i + 1] = a.y; v[4 * i + 2] = a.z; v[4 * i + 3] = a.w;
     }
   } else {
@@ -674,16 +675,20 @@ __device__ __forceinline__ void consume(const Pass<NT>& p, int it, const u32x4 (
           for (int v = 0; v < 16; ++v) xs += xv[v];
 #pragma unroll
           for (int k = 0; k < RT; ++k) {
-            uint32_t wd[4] = {r[k].x, r[k].y, r[k].z, r[k].w};
-            // Converted codes are not kept across positions (4 x 32 floats
-            // would not fit in registers): each position converts again.
-            asm volatile("" : "+v"(wd[0]), "+v"(wd[1]), "+v"(wd[2]), "+v"(wd[3]));
+            const uint32_t wd[4] = {r[k].x, r[k].y, r[k].z, r[k].w};
+            uint32_t nib[4];
+#pragma unroll
+            for (int w = 0; w < 4; ++w) nib[w] = (h ? wd[w] >> 4 : wd[w]) & 0x0F0F0F0Fu;
+            // Opaque to the compiler: the codes are converted again for every
+            // position (4 x 32 converted floats would not fit in registers),
+            // and each byte is converted by one byte-select conversion
+            // instead of a bit-field extract and a conversion.
+            asm volatile("" : "+v"(nib[0]), "+v"(nib[1]), "+v"(nib[2]), "+v"(nib[3]));
 #pragma unroll
             for (int w = 0; w < 4; ++w) {
-              const uint32_t nib = (h ? wd[w] >> 4 : wd[w]) & 0x0F0F0F0Fu;
 #pragma unroll
               for (int b = 0; b < 4; ++b)
-                qx[k] = fmaf((float)((nib >> (8 * b)) & 0xFFu), xv[4 * w + b], qx[k]);
+                qx[k] = fmaf((float)((nib[w] >> (8 * b)) & 0xFFu), xv[4 * w + b], qx[k]);
             }
           }
         }
