@@ -15,9 +15,10 @@ Modules
     truncation confidence-expansion truncation of the draft loop
                (Section 3.4, Eqs. 12-14, Algorithm 1)
     q4      dequantisation of Q4_0 expert weights (Section 4.1's 4.5-bit format)
+    distill the self-distillation signals of Eqs. 6-10 from teacher-forced passes
 
 Pins (tests/test_oracle_*.py) tie every function to the paper or to
 mathematics independent of this code; functions without such a pin say
 "parity unpinned" in their docstring.
 """
-from . import cache_sim, decode, moe, q4, truncation  # noqa: F401
+from . import cache_sim, decode, distill, moe, q4, truncation  # noqa: F401
