@@ -487,6 +487,52 @@ int de_spec_step_trunc(const de_model* m, de_cache* cache, int k_max, const de_t
                        int32_t* n_union, int32_t* pred_idx, float* q, int32_t* trace, void* ws,
                        size_t ws_bytes, hipStream_t stream);
 
+/* ---- Self-distillation signals (Section 3.3, Eqs. 6-10) ----
+ *
+ * Training the draft experts is outside this library; these calls emit what
+ * it consumes, from passes the runtime already makes. */
+
+/* The residual target of Eq. 6 for the last de_verify_layer (or
+ * de_grouped_swiglu) call made with the same desc, T and workspace on
+ * `stream`: m_star [T, H] fp32 (device) = y* - S(x) - g_e1 E_e1(x), i.e. the
+ * sum of each position's routed partials ranked 2..k, in list order. */
+int de_residual_target(const de_moe_desc* d, int T, const void* ws, size_t ws_bytes,
+                       float* m_star, hipStream_t stream);
+
+/* The router logits z = W_r x [T, N] fp32 of the last layer call made with
+ * the same desc, T and workspace (device copy on `stream`). */
+int de_layer_router_logits(const de_moe_desc* d, int T, const void* ws, size_t ws_bytes,
+                           float* z, hipStream_t stream);
+
+/* Row divergences (one launch; all pointers device): for each row r of a
+ * (target) [rows, lda] and b (draft) [rows, ldb], first n values:
+ *   sigmoid = 0: p = softmax((a_r + bias) / tau), q = softmax((b_r + bias) / tau),
+ *     kl[r] = tau^2 KL(p || q) (Eq. 8 with temperature tau; Eq. 10 with tau 1
+ *     and the router bias), and, when ce is not NULL, ce[r] =
+ *     -log softmax(b_r + bias)[argmax (a_r + bias)] (Eq. 9; ties to the lowest
+ *     index, NaN as -infinity);
+ *   sigmoid = 1 (sigmoid routers, Eq. 10): p and q the sigmoid scores
+ *     normalised to sum one, kl[r] = KL(p || q); bias and ce must be NULL and
+ *     tau 1.
+ * bias [n] may be NULL. */
+int de_row_kl(int rows, int n, const float* a, int lda, const float* b, int ldb,
+              const float* bias, int sigmoid, float tau, float* kl, float* ce,
+              hipStream_t stream);
+
+/* The self-distillation signals of T teacher-forced positions (tokens [T],
+ * device), from one target pass and one draft pass over them (without
+ * attention a position depends only on its token):
+ *   m_star [n_layers, T, H]: the residual target of Eq. 6 at every MoE layer;
+ *   router_kl [n_layers, T]: Eq. 10, KL from the target's router distribution
+ *     at the target's layer input to the router distribution at the draft
+ *     path's layer input (softmax(z + b); sigmoid routers: normalised scores);
+ *   logit_kl [T]: Eq. 8 at temperature tau; token_ce [T]: Eq. 9.
+ * m_star and router_kl are both given or both NULL, likewise logit_kl and
+ * token_ce.  All device fp32.  Scratch: de_model_workspace_bytes(m, T). */
+int de_distill_signals(const de_model* m, int T, const int32_t* tokens, float tau,
+                       float* m_star, float* router_kl, float* logit_kl, float* token_ce,
+                       void* ws, size_t ws_bytes, hipStream_t stream);
+
 /* Pure streaming read of `bytes` (multiple of 16) from buf: the measured HBM
  * read ceiling.  sink [1] receives a value that depends on every byte. */
 int de_stream_probe(const void* buf, size_t bytes, float* sink, hipStream_t stream);

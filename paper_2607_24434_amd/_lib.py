@@ -43,6 +43,7 @@ C_FUNCS = [
     "de_cache_begin_block", "de_cache_prefetch", "de_cache_ensure", "de_cache_release",
     "de_cache_table", "de_cache_stats", "de_cache_slots", "de_spec_step_cached",
     "de_confidence", "de_expansion", "de_spec_step_trunc", "de_draft_layer_topr",
+    "de_residual_target", "de_layer_router_logits", "de_row_kl", "de_distill_signals",
 ]
 DE_PHASE_GATEUP = 0
 DE_PHASE_DOWN = 1
@@ -149,6 +150,10 @@ def _load(path: str = LIB_PATH, strict: bool = True):
         "de_grouped_swiglu": (I, [DP, I, P, TP, P, P, P, P, P, P, P, P, EP, P, SZ, P]),
         "de_draft_layer": (I, [DP, I, P, P, P, TP, P, P, F, P, P, P, EP, P, SZ, P]),
         "de_draft_layer_topr": (I, [DP, I, P, P, P, TP, P, P, F, I, P, P, P, EP, P, SZ, P]),
+        "de_residual_target": (I, [DP, I, P, SZ, P, P]),
+        "de_layer_router_logits": (I, [DP, I, P, SZ, P, P]),
+        "de_row_kl": (I, [I, I, P, I, P, I, P, I, F, P, P, P]),
+        "de_distill_signals": (I, [MP, I, P, F, P, P, P, P, P, SZ, P]),
         "de_verify_layer": (I, [DP, I, P, P, P, TP, P, P, P, P, P, P, P, P, P, P, EP, P, SZ, P]),
         "de_accept_workspace_bytes": (SZ, [I, I]),
         "de_accept_len": (I, [I, I, P, P, P, P, P, SZ, P]),
@@ -524,3 +529,27 @@ def de_spec_step_trunc(model, cache, k_max, tau, budget, slots, block, target_ar
         _ptr(n_union), _ptr(pred_idx), _ptr(q), _ptr(trace), _ptr(ws),
         ws.numel() if ws is not None else 0, _stream(stream)))
     return int(nd.value)
+
+
+def de_residual_target(desc, T, ws, m_star, stream=None):
+    _check("de_residual_target", LIB.de_residual_target(
+        ctypes.byref(desc), int(T), _ptr(ws), ws.numel(), _ptr(m_star), _stream(stream)))
+
+
+def de_layer_router_logits(desc, T, ws, z, stream=None):
+    _check("de_layer_router_logits", LIB.de_layer_router_logits(
+        ctypes.byref(desc), int(T), _ptr(ws), ws.numel(), _ptr(z), _stream(stream)))
+
+
+def de_row_kl(rows, n, a, lda, b, ldb, bias, sigmoid, tau, kl, ce=None, stream=None):
+    _check("de_row_kl", LIB.de_row_kl(int(rows), int(n), _ptr(a), int(lda), _ptr(b), int(ldb),
+                                      _ptr(bias), int(bool(sigmoid)), float(tau), _ptr(kl),
+                                      _ptr(ce), _stream(stream)))
+
+
+def de_distill_signals(model, T, tokens, tau, m_star, router_kl, logit_kl, token_ce, ws=None,
+                       stream=None):
+    _check("de_distill_signals", LIB.de_distill_signals(
+        ctypes.byref(model), int(T), _ptr(tokens), float(tau), _ptr(m_star), _ptr(router_kl),
+        _ptr(logit_kl), _ptr(token_ce), _ptr(ws), ws.numel() if ws is not None else 0,
+        _stream(stream)))

@@ -723,6 +723,59 @@ int de_expansion(int L, int k, int N, const int32_t* pred_idx, uint64_t* uhat, i
   return hip_status(de::launch_expansion(a, stream));
 }
 
+int de_residual_target(const de_moe_desc* d, int T, const void* ws, size_t ws_bytes,
+                       float* m_star, hipStream_t stream) {
+  int rc = de_check_desc(d);
+  if (rc != DE_OK) return rc;
+  if ((rc = check_T(T)) != DE_OK) return rc;
+  if (m_star == nullptr) return DE_ERR_INVALID;
+  if ((rc = check_ws(*d, T, ws, ws_bytes)) != DE_OK) return rc;
+  const Layout L = layout(*d, T);
+  de::ResidualArgs a{};
+  a.T = T;
+  a.H = d->hidden;
+  a.kk = d->top_k;
+  a.pairs_max = T * d->top_k;
+  a.p_r = at<float>(const_cast<void*>(ws), L.p_r);
+  a.pair_pos = at<int32_t>(const_cast<void*>(ws), L.ppos);
+  a.out = m_star;
+  return hip_status(de::launch_residual(a, stream));
+}
+
+int de_layer_router_logits(const de_moe_desc* d, int T, const void* ws, size_t ws_bytes,
+                           float* z, hipStream_t stream) {
+  int rc = de_check_desc(d);
+  if (rc != DE_OK) return rc;
+  if ((rc = check_T(T)) != DE_OK) return rc;
+  if (z == nullptr) return DE_ERR_INVALID;
+  if ((rc = check_ws(*d, T, ws, ws_bytes)) != DE_OK) return rc;
+  const Layout L = layout(*d, T);
+  return hip_status(hipMemcpyAsync(z, static_cast<const char*>(ws) + L.z,
+                                   (size_t)T * d->n_experts * 4, hipMemcpyDeviceToDevice,
+                                   stream));
+}
+
+int de_row_kl(int rows, int n, const float* a, int lda, const float* b, int ldb,
+              const float* bias, int sigmoid, float tau, float* kl, float* ce,
+              hipStream_t stream) {
+  if (rows < 1 || rows > (1 << 20) || n < 1 || lda < n || ldb < n) return DE_ERR_INVALID;
+  if (!a || !b || !kl || !(tau > 0.f) || !std::isfinite(tau)) return DE_ERR_INVALID;
+  if (sigmoid != 0 && (bias != nullptr || ce != nullptr || tau != 1.f)) return DE_ERR_INVALID;
+  de::RowKlArgs r{};
+  r.rows = rows;
+  r.n = n;
+  r.a = a;
+  r.lda = lda;
+  r.b = b;
+  r.ldb = ldb;
+  r.bias = bias;
+  r.sigmoid = sigmoid != 0;
+  r.tau = tau;
+  r.kl = kl;
+  r.ce = ce;
+  return hip_status(de::launch_rowkl(r, stream));
+}
+
 int de_stream_probe(const void* buf, size_t bytes, float* sink, hipStream_t stream) {
   if (!buf || !sink || bytes == 0 || bytes % 16 || !aligned16(buf)) return DE_ERR_INVALID;
   return hip_status(de::launch_stream_probe(buf, bytes, sink, stream));

@@ -234,6 +234,28 @@ struct ExpansionArgs {
   int32_t* out;                // [5]
 };
 hipError_t launch_confidence(int T, int V, const float* logits, float* q, hipStream_t s);
+
+// Self-distillation signals.
+struct ResidualArgs {
+  int T, H, kk, pairs_max;
+  const float* p_r;            // [pairs, H] routed partials (gates applied)
+  const int32_t* pair_pos;     // [T, kk]
+  float* out;                  // [T, H]
+};
+struct RowKlArgs {
+  int rows, n;
+  const float* a;              // target rows [rows, lda]
+  int lda;
+  const float* b;              // draft rows [rows, ldb]
+  int ldb;
+  const float* bias;           // [n] or NULL (softmax mode)
+  int sigmoid;
+  float tau;
+  float* kl;                   // [rows]
+  float* ce;                   // [rows] or NULL (softmax mode only)
+};
+hipError_t launch_residual(const ResidualArgs& a, hipStream_t s);
+hipError_t launch_rowkl(const RowKlArgs& a, hipStream_t s);
 hipError_t launch_expansion(const ExpansionArgs& a, hipStream_t s);
 
 }  // namespace de

@@ -50,6 +50,7 @@ struct ModelLayout {
   size_t ridx, rgate;         // top-k lists of the cached step's routing [64, k]
   size_t h, n0, n1, logits;   // residual stream, two normed buffers, logits
   size_t uhat, tctl;          // truncation: predicted verifier set [L, words], decision [5]
+  size_t zt, zd, logits2;     // distillation: router logits of both passes [L, T, N], draft logits
   size_t total;
 };
 
@@ -77,6 +78,9 @@ ModelLayout model_layout(const de_model& m, int T) {
   L.logits = take((size_t)T * m.vocab * 4);
   L.uhat = take((size_t)m.n_layers * ((m.moe.n_experts + 63) / 64) * 8);
   L.tctl = take(5 * 4);
+  L.zt = take((size_t)m.n_layers * T * m.moe.n_experts * 4);
+  L.zd = take((size_t)m.n_layers * T * m.moe.n_experts * 4);
+  L.logits2 = take((size_t)T * m.vocab * 4);
   L.total = o;
   return L;
 }
@@ -174,13 +178,20 @@ int cached_layer(const de_model& m, de_cache* c, int l, int T, bool draft, const
   return de::cache_span(c, true, purpose, s);
 }
 
+// Per-layer outputs a forward may copy out after each MoE layer: its router
+// logits [L, T, N], and (target mode) its residual target [L, T, H].
+struct Capture {
+  float* z = nullptr;
+  float* m = nullptr;
+};
+
 // Logits of T positions through the whole stack; the last MoE layer's fused
 // epilogue leaves RMSNorm(h) in the normed buffer, which the LM head reads.
 // With a cache the routed experts come through it (cached_layer).
 int forward(const de_model& m, int T, const int32_t* tokens, int mode, float* logits,
             const ArgmaxOut& am, int32_t* n_union, int32_t* pred_idx, size_t pred_stride,
             void* ws, const ModelLayout& L, hipStream_t s, de_cache* cache = nullptr,
-            std::vector<int32_t>* deferred = nullptr) {
+            std::vector<int32_t>* deferred = nullptr, const Capture& cap = Capture{}) {
   const int H = m.moe.hidden;
   float* h = at<float>(ws, L.h);
   float* ncur = at<float>(ws, L.n0);
@@ -213,6 +224,14 @@ int forward(const de_model& m, int T, const int32_t* tokens, int mode, float* lo
                                L.layer_bytes, s);
     }
     if (rc != DE_OK) return rc;
+    if (cap.z != nullptr &&
+        (rc = de_layer_router_logits(&m.moe, T, lws, L.layer_bytes,
+                                     cap.z + (size_t)l * T * m.moe.n_experts, s)) != DE_OK)
+      return rc;
+    if (cap.m != nullptr && mode == DE_TARGET &&
+        (rc = de_residual_target(&m.moe, T, lws, L.layer_bytes, cap.m + (size_t)l * T * H, s)) !=
+            DE_OK)
+      return rc;
     std::swap(ncur, nnext);
   }
   rc = de_lm_head(T, H, m.vocab, ncur, m.lm_head, logits, s);
@@ -413,6 +432,52 @@ int de_spec_step_trunc(const de_model* m, de_cache* cache, int k_max, const de_t
   const ArgmaxOut am{target_argmax, out, kept > 0 ? block + 1 : nullptr};
   return forward(*m, kept + 1, block, DE_TARGET, logits, am, n_union, nullptr, 0, ws, L, stream,
                  cache);
+}
+
+int de_distill_signals(const de_model* m, int T, const int32_t* tokens, float tau,
+                       float* m_star, float* router_kl, float* logit_kl, float* token_ce,
+                       void* ws, size_t ws_bytes, hipStream_t stream) {
+  int rc = de_check_model(m);
+  if (rc != DE_OK) return rc;
+  if (tokens == nullptr || !(tau > 0.f) || !std::isfinite(tau)) return DE_ERR_INVALID;
+  if (m->n_layers > 0 && (m_star == nullptr) != (router_kl == nullptr)) return DE_ERR_INVALID;
+  if ((logit_kl == nullptr) != (token_ce == nullptr)) return DE_ERR_INVALID;
+  if ((rc = check_block(*m, T, ws, ws_bytes)) != DE_OK) return rc;
+  const ModelLayout L = model_layout(*m, T);
+  const int N = m->moe.n_experts, NL = m->n_layers;
+  float* zt = at<float>(ws, L.zt);
+  float* zd = at<float>(ws, L.zd);
+  float* lt = at<float>(ws, L.logits);
+  float* ld = at<float>(ws, L.logits2);
+  const ArgmaxOut none{nullptr, nullptr, nullptr};
+  // Teacher-forced passes over the same positions: the target (capturing each
+  // layer's router logits and residual target), then the drafter.
+  Capture ct;
+  ct.z = zt;
+  ct.m = m_star;
+  rc = forward(*m, T, tokens, DE_TARGET, lt, none, nullptr, nullptr, 0, ws, L, stream, nullptr,
+               nullptr, ct);
+  if (rc != DE_OK) return rc;
+  Capture cd;
+  cd.z = zd;
+  rc = forward(*m, T, tokens, DE_DRAFT, ld, none, nullptr, nullptr, 0, ws, L, stream, nullptr,
+               nullptr, cd);
+  if (rc != DE_OK) return rc;
+  const bool sig = m->moe.score_func == DE_SIGMOID;
+  if (router_kl != nullptr) {
+    for (int l = 0; l < NL; ++l) {
+      const size_t o = (size_t)l * T * N;
+      rc = de_row_kl(T, N, zt + o, N, zd + o, N, sig ? nullptr : m->layers[l].bias, sig ? 1 : 0,
+                     1.f, router_kl + (size_t)l * T, nullptr, stream);
+      if (rc != DE_OK) return rc;
+    }
+  }
+  if (logit_kl != nullptr) {
+    rc = de_row_kl(T, m->vocab, lt, m->vocab, ld, m->vocab, nullptr, 0, tau, logit_kl, token_ce,
+                   stream);
+    if (rc != DE_OK) return rc;
+  }
+  return DE_OK;
 }
 
 }  // extern "C"

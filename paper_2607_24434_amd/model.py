@@ -59,6 +59,11 @@ class DeviceModel:
                                     target_argmax, out, pred_idx, q, n_union, trace, self.ws,
                                     stream, prefetch)
 
+    def distill(self, tokens, tau, m_star, router_kl, logit_kl, token_ce, stream=None):
+        """The self-distillation signals (Eqs. 6-10) of teacher-forced positions."""
+        L.de_distill_signals(self.model, tokens.numel(), tokens, tau, m_star, router_kl,
+                             logit_kl, token_ce, self.ws, stream)
+
     def forward(self, tokens, mode, logits, argmax=None, n_union=None, stream=None):
         L.de_model_forward(self.model, tokens.numel(), tokens, mode, logits, argmax, n_union,
                            self.ws, stream)
