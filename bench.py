@@ -81,6 +81,8 @@ def parse():
     p.add_argument("--offload-steps", type=int, default=3)
     p.add_argument("--no-verify-side", action="store_true",
                    help="skip the truncation / prefetch comparison on the offload stack")
+    p.add_argument("--no-q4", action="store_true",
+                   help="skip the Q4_0-weight layer measurement")
     p.add_argument("--no-draft-side", action="store_true",
                    help="skip the drafter comparison (top-r against DraftExpert) on the offload stack")
     return p.parse_args()
@@ -219,6 +221,11 @@ def main():
                 + (T * cfg.top_k * cfg.inter + T * cfg.shared_inter) * 4 + (T * cfg.top_k + T) * H * 4)
     dn_gbs = float(dn_bytes.sum() / (sum(dn_ms) * 1e-3) / 1e9)
 
+    q4 = None
+    if not args.no_q4:
+        del copies
+        torch.cuda.empty_cache()
+        q4 = q4_layer(args, de, configs, gen, wgpu, torch, np, 1e3 * statistics.median(ver_ms))
     full = None if args.no_full_step else full_step(args, de, configs, gen, wgpu, torch, np)
     offload = None if args.no_offload else offload_step(args, de, configs, gen, wgpu, torch, np)
 
@@ -290,11 +297,110 @@ def main():
             "traffic_vs_algorithmic": PMC_TRAFFIC["vs_algorithmic"] if pmc_traffic() else None,
             "algorithmic_bytes_per_launch": int(round(float(gu_bytes.mean()))),
         },
+        "q4_layer": q4,
         "full_step": full,
         "offload_step": offload,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
+
+
+def q4_layer(args, de, configs, gen, wgpu, torch, np, bf16_verify_us):
+    """The V2-Lite layer with Q4_0 expert weights (routed, shared and draft;
+    4,866,048 bytes per expert instead of 17,301,504): the 9-position verify
+    layer and a draft layer, on rotated weight copies, with the grouped
+    kernels timed by HIP events in separate steps."""
+    cfg = configs.CFG2_Q4
+    dev = "cuda"
+    H, T, R = cfg.hidden, 9, args.copies
+    desc = de.make_desc(H, cfg.n_experts, cfg.top_k, cfg.inter, cfg.shared_inter,
+                        cfg.draft_inter, cfg.score_func, cfg.norm_topk, cfg.routed_scale,
+                        cfg.wdtype)
+    eb = cfg.expert_bytes()
+    copies = []
+    for c in range(R):
+        routed = wgpu.routed_experts(cfg, 0, dev, redraw=c)
+        copies.append(dict(routed=routed, table=de.make_table(routed, eb, None, cfg.n_experts),
+                           shared=wgpu.shared_block(cfg, 0, dev, redraw=c),
+                           draft=wgpu.draft_block(cfg, 0, dev, redraw=c),
+                           router=wgpu.router(cfg, 0, dev, redraw=c)))
+    x = wgpu.to_device(gen.x_rows(cfg, T, block=0), dev)
+    ws = de.workspace(desc, T, dev)
+    y = torch.empty(T, H, dtype=torch.float32, device=dev)
+    steps = args.warmup + args.steps
+    nu = torch.zeros(steps, dtype=torch.int32, device=dev)
+
+    def ev():
+        # Recorded once here so that torch accepts them; the library records
+        # the phase events again around its launches.
+        e = torch.cuda.Event(enable_timing=True)
+        e.record()
+        return e
+
+    def verify(i, e=None):
+        cp = copies[i % R]
+        if e is not None:
+            de.de_time_next_phase(de.DE_PHASE_GATEUP, e[0], e[1])
+            de.de_time_next_phase(de.DE_PHASE_DOWN, e[2], e[3])
+        de.de_verify_layer(desc, T, x, cp["router"], None, cp["table"], cp["shared"], y,
+                           n_union=nu[i:i + 1], ws=ws)
+
+    def draft(i):
+        cp = copies[i % R]
+        de.de_draft_layer(desc, 1, x[:1], cp["router"], None, cp["table"], cp["shared"],
+                          cp["draft"], cfg.gamma, y[:1], None, None, ws)
+
+    for i in range(args.warmup):
+        verify(i)
+        draft(i)
+    torch.cuda.synchronize()
+    vt, dt, ph = [], [], []
+    for i in range(args.warmup, steps):
+        a, b, c, d = ev(), ev(), ev(), ev()
+        a.record()
+        verify(i)
+        b.record()
+        draft(i)
+        c.record()
+        vt.append((a, b))
+        dt.append((b, c))
+    for i in range(args.warmup, steps):
+        e = [ev() for _ in range(4)]
+        verify(i, e)
+        ph.append(e)
+    torch.cuda.synchronize()
+    med = statistics.median
+    ver_ms = [a.elapsed_time(b) for a, b in vt]
+    n = nu[args.warmup:].cpu().numpy().astype(np.int64)
+    gu_ms = [e[0].elapsed_time(e[1]) for e in ph]
+    dn_ms = [e[2].elapsed_time(e[3]) for e in ph]
+    mb = cfg.mat_bytes
+    gu_bytes = (n * 2 * mb(cfg.inter, H) + 2 * mb(cfg.shared_inter, H) + T * H * 4
+                + (T * cfg.top_k * cfg.inter + T * cfg.shared_inter) * 4)
+    dn_bytes = (n * mb(H, cfg.inter) + mb(H, cfg.shared_inter)
+                + (T * cfg.top_k * cfg.inter + T * cfg.shared_inter) * 4 + (T * cfg.top_k + T) * H * 4)
+    gu_gbs = float(gu_bytes.sum() / (sum(gu_ms) * 1e-3) / 1e9)
+    value = float((n * eb).sum() / (sum(ver_ms) * 1e-3) / 1e9)
+    res = {
+        "workload": "v2lite-moe-layer-q4_0: the V2-Lite layer (H=2048, 64 routed + 2 shared "
+                    "experts of I=1408, top-6, draft expert I=1408) with Q4_0 expert weights "
+                    "(18-byte blocks of 32 weights), 9-position verify block, fp32 activations",
+        "expert_bytes": eb,
+        "verify_layer_us": round(1e3 * med(ver_ms), 2),
+        "draft_layer_us": round(1e3 * med([a.elapsed_time(b) for a, b in dt]), 2),
+        "gateup_us": round(1e3 * med(gu_ms), 2),
+        "down_us": round(1e3 * med(dn_ms), 2),
+        "union_mean": round(float(n.mean()), 2),
+        "union_gbs": round(value, 1),
+        "union_frac_of_peak": round(value / PEAK_HBM_GBS, 4),
+        "gateup_gbs": round(gu_gbs, 1),
+        "gateup_frac_of_peak": round(gu_gbs / PEAK_HBM_GBS, 4),
+        "down_gbs": round(float(dn_bytes.sum() / (sum(dn_ms) * 1e-3) / 1e9), 1),
+        "verify_speedup_vs_bf16": round(bf16_verify_us / (1e3 * med(ver_ms)), 3),
+    }
+    del copies
+    torch.cuda.empty_cache()
+    return res
 
 
 def full_step(args, de, configs, gen, wgpu, torch, np):
