@@ -91,8 +91,8 @@ def parse():
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py measures one GPU: --gpus {args.gpus} is not supported (this build has no "
-              f"multi-GPU path; see the sharding notes in DESIGN.md)", file=sys.stderr)
+        print(f"bench.py measures one GPU: --gpus {args.gpus} is not supported (the library "
+              f"has no multi-GPU path)", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np

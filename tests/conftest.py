@@ -9,5 +9,5 @@ if ROOT not in sys.path:
 
 
 def pytest_configure(config):
-    config.addinivalue_line("markers", "gpu: needs a HIP device (MI355X); runs on the GPU box")
+    config.addinivalue_line("markers", "gpu: needs a HIP device (MI355X)")
     config.addinivalue_line("markers", "slow: CPU test that takes more than a few seconds")
