@@ -25,6 +25,18 @@ const DevInfo& dev_info() {
   return info[dev];
 }
 
+int draft_layer_chain(const de_moe_desc* d, int T, const float* x, const float* w_router,
+                      const float* bias, const de_expert_table* routed, const void* shared_w,
+                      const void* draft_w, float gamma, int r, float* y, int32_t* pred_idx,
+                      float* pred_gate, const de_epilogue* epi, void* ws, size_t ws_bytes,
+                      hipStream_t stream, bool logits_ready, const float* next_router);
+int verify_layer_chain(const de_moe_desc* d, int T, const float* x, const float* w_router,
+                       const float* bias, const de_expert_table* routed, const void* shared_w,
+                       float* y, int32_t* topk_idx, float* topk_gate, int32_t* n_union,
+                       int32_t* union_ids, int32_t* offsets, int32_t* tok_list, float* gate_list,
+                       int32_t* pair_pos, const de_epilogue* epi, void* ws, size_t ws_bytes,
+                       hipStream_t stream, bool logits_ready, const float* next_router);
+
 // Bytes of a [rows, cols] weight matrix and of a [G|U|D] expert block.
 size_t mat_bytes(int wdtype, int rows, int cols) {
   if (wdtype == DE_Q4_0) return (size_t)rows * cols * 9 / 16;
@@ -207,7 +219,8 @@ int run_grouped(const de_moe_desc& d, int T, const float* x, const de::RoutedSrc
                 const int32_t* pair_pos, int kk, const void* shared_w, const void* draft_w,
                 float gamma, float* y, const de_epilogue* epi, const Layout& L, void* ws,
                 const de::TopkUnionArgs* fused_sel, hipStream_t s, bool dense_on = true,
-                bool combine_on = true, bool fuse_select = false) {
+                bool combine_on = true, bool fuse_select = false,
+                const float* next_router = nullptr) {
   const bool q4 = d.wdtype == DE_Q4_0;
   const size_t esz = q4 ? 0 : elem_bytes(d.wdtype);
   de::GroupedArgs g{};
@@ -297,6 +310,17 @@ int run_grouped(const de_moe_desc& d, int T, const float* x, const de::RoutedSrc
   e = timed_phase(DE_PHASE_DOWN, s, [&] { return de::launch_down(g, d.wdtype, s); });
   if (e != hipSuccess) return DE_ERR_HIP;
   if (!combine_on) return DE_OK;
+  if (next_router != nullptr) {
+    // The next layer's router logits go to this workspace's logit rows, where
+    // the next layer call (same shape, T and workspace) reads them.
+    de::RouteArgs nr{};
+    nr.sel.T = T;
+    nr.sel.N = d.n_experts;
+    nr.w = next_router;
+    nr.H = d.hidden;
+    nr.z = at<float>(ws, L.z);
+    return hip_status(de::launch_combine_route(c, nr, s));
+  }
   return hip_status(de::launch_combine(c, s));
 }
 
@@ -481,6 +505,43 @@ int de_draft_layer_topr(const de_moe_desc* d, int T, const float* x, const float
                         const void* draft_w, float gamma, int r, float* y, int32_t* pred_idx,
                         float* pred_gate, const de_epilogue* epi, void* ws, size_t ws_bytes,
                         hipStream_t stream) {
+  return de::draft_layer_chain(d, T, x, w_router, bias, routed, shared_w, draft_w, gamma, r, y,
+                               pred_idx, pred_gate, epi, ws, ws_bytes, stream, false, nullptr);
+}
+
+int de_draft_layer(const de_moe_desc* d, int T, const float* x, const float* w_router,
+                   const float* bias, const de_expert_table* routed, const void* shared_w,
+                   const void* draft_w, float gamma, float* y, int32_t* pred_idx,
+                   float* pred_gate, const de_epilogue* epi, void* ws, size_t ws_bytes,
+                   hipStream_t stream) {
+  return de_draft_layer_topr(d, T, x, w_router, bias, routed, shared_w, draft_w, gamma, 1, y,
+                             pred_idx, pred_gate, epi, ws, ws_bytes, stream);
+}
+
+int de_verify_layer(const de_moe_desc* d, int T, const float* x, const float* w_router,
+                    const float* bias, const de_expert_table* routed, const void* shared_w,
+                    float* y, int32_t* topk_idx, float* topk_gate, int32_t* n_union,
+                    int32_t* union_ids, int32_t* offsets, int32_t* tok_list, float* gate_list,
+                    int32_t* pair_pos, const de_epilogue* epi, void* ws, size_t ws_bytes,
+                    hipStream_t stream) {
+  return de::verify_layer_chain(d, T, x, w_router, bias, routed, shared_w, y, topk_idx,
+                                topk_gate, n_union, union_ids, offsets, tok_list, gate_list,
+                                pair_pos, epi, ws, ws_bytes, stream, false, nullptr);
+}
+
+}  // extern "C"
+
+namespace de {
+
+// The layer calls of a chain of MoE layers (the stacked model): with
+// logits_ready the router logits were already written to the workspace by the
+// previous layer's combine; with next_router this layer's combine also writes
+// the next layer's logits (which needs epi->normed).
+int draft_layer_chain(const de_moe_desc* d, int T, const float* x, const float* w_router,
+                      const float* bias, const de_expert_table* routed, const void* shared_w,
+                      const void* draft_w, float gamma, int r, float* y, int32_t* pred_idx,
+                      float* pred_gate, const de_epilogue* epi, void* ws, size_t ws_bytes,
+                      hipStream_t stream, bool logits_ready, const float* next_router) {
   int rc = de_check_desc(d);
   if (rc != DE_OK) return rc;
   if ((rc = check_T(T)) != DE_OK) return rc;
@@ -513,29 +574,22 @@ int de_draft_layer_topr(const de_moe_desc* d, int T, const float* x, const float
   a.pair_pos = at<int32_t>(ws, L.ppos);
   a.z = at<float>(ws, L.z);
   // Logits only; the gate/up prologue selects the top-k in every block.
-  if (route(*d, T, x, w_router, L, ws, a, stream, false) != hipSuccess) return DE_ERR_HIP;
+  if (next_router != nullptr && (epi == nullptr || epi->normed == nullptr)) return DE_ERR_INVALID;
+  if (!logits_ready && route(*d, T, x, w_router, L, ws, a, stream, false) != hipSuccess)
+    return DE_ERR_HIP;
   const de::RoutedSrc rs = routed_src(*d, T, r, routed, a.n_union, a.union_ids, a.offsets,
                                       a.tok_list, a.gate_list, at<float>(ws, L.a_r),
                                       at<float>(ws, L.p_r));
   return run_grouped(*d, T, x, rs, a.pair_pos, r, shared_w, draft_w, gamma, y, epi, L, ws, &a,
-                     stream, true, true, true);
+                     stream, true, true, true, next_router);
 }
 
-int de_draft_layer(const de_moe_desc* d, int T, const float* x, const float* w_router,
-                   const float* bias, const de_expert_table* routed, const void* shared_w,
-                   const void* draft_w, float gamma, float* y, int32_t* pred_idx,
-                   float* pred_gate, const de_epilogue* epi, void* ws, size_t ws_bytes,
-                   hipStream_t stream) {
-  return de_draft_layer_topr(d, T, x, w_router, bias, routed, shared_w, draft_w, gamma, 1, y,
-                             pred_idx, pred_gate, epi, ws, ws_bytes, stream);
-}
-
-int de_verify_layer(const de_moe_desc* d, int T, const float* x, const float* w_router,
-                    const float* bias, const de_expert_table* routed, const void* shared_w,
-                    float* y, int32_t* topk_idx, float* topk_gate, int32_t* n_union,
-                    int32_t* union_ids, int32_t* offsets, int32_t* tok_list, float* gate_list,
-                    int32_t* pair_pos, const de_epilogue* epi, void* ws, size_t ws_bytes,
-                    hipStream_t stream) {
+int verify_layer_chain(const de_moe_desc* d, int T, const float* x, const float* w_router,
+                       const float* bias, const de_expert_table* routed, const void* shared_w,
+                       float* y, int32_t* topk_idx, float* topk_gate, int32_t* n_union,
+                       int32_t* union_ids, int32_t* offsets, int32_t* tok_list, float* gate_list,
+                       int32_t* pair_pos, const de_epilogue* epi, void* ws, size_t ws_bytes,
+                       hipStream_t stream, bool logits_ready, const float* next_router) {
   int rc = de_check_desc(d);
   if (rc != DE_OK) return rc;
   if ((rc = check_T(T)) != DE_OK) return rc;
@@ -565,13 +619,19 @@ int de_verify_layer(const de_moe_desc* d, int T, const float* x, const float* w_
   a.pair_pos = pair_pos ? pair_pos : at<int32_t>(ws, L.ppos);
   a.z = at<float>(ws, L.z);
   // Logits only; the gate/up prologue selects the top-k in every block.
-  if (route(*d, T, x, w_router, L, ws, a, stream, false) != hipSuccess) return DE_ERR_HIP;
+  if (next_router != nullptr && (epi == nullptr || epi->normed == nullptr)) return DE_ERR_INVALID;
+  if (!logits_ready && route(*d, T, x, w_router, L, ws, a, stream, false) != hipSuccess)
+    return DE_ERR_HIP;
   const de::RoutedSrc r = routed_src(*d, T, d->top_k, routed, a.n_union, a.union_ids,
                                      a.offsets, a.tok_list, a.gate_list, at<float>(ws, L.a_r),
                                      at<float>(ws, L.p_r));
   return run_grouped(*d, T, x, r, a.pair_pos, d->top_k, shared_w, nullptr, 0.f, y, epi, L, ws, &a,
-                     stream, true, true, true);
+                     stream, true, true, true, next_router);
 }
+
+}  // namespace de
+
+extern "C" {
 
 size_t de_accept_workspace_bytes(int K, int V) {
   if (K < 0 || K > 1024 || V < 1) return 0;

@@ -192,6 +192,7 @@ struct RouteArgs {
   int select;              // 0: logits only (the gate/up prologue selects)
 };
 hipError_t launch_route(const RouteArgs& r, hipStream_t s);
+hipError_t launch_combine_route(const CombineArgs& a, const RouteArgs& r, hipStream_t s);
 // Union only, from caller-supplied lists (sel.idx_in / sel.gate_in).
 hipError_t launch_union(const TopkUnionArgs& a, hipStream_t s);
 
@@ -202,6 +203,9 @@ hipError_t launch_down(const GroupedArgs& a, int wdtype, hipStream_t s);
 
 
 hipError_t launch_combine(const CombineArgs& a, hipStream_t s);
+// The combine (with RMSNorm) fused with the next layer's router logits:
+// r.w, r.H, r.z, r.sel.N are read.  Needs a.normed and combine_route_fits(H).
+bool combine_route_fits(int H);
 
 struct AcceptArgs {
   int K, V;

@@ -1016,9 +1016,12 @@ constexpr int kCombPer = 4;
 // in that fixed order; optionally also RMSNorm(y).  One block of NTH threads
 // per position; each thread's kCombPer elements are loaded independently and,
 // for a row of at most NTH * kCombPer elements, stay in registers for the
-// normalisation.
+// normalisation.  xs (LDS, may be null) also receives the normalised row;
+// without `write` (only with a row of at most NTH * kCombPer elements and
+// xs) nothing is written to global memory.
 template <int NTH>
-__device__ __forceinline__ void combine_row(const CombineArgs& a, int t, float* red) {
+__device__ __forceinline__ void combine_row(const CombineArgs& a, int t, float* red,
+                                            float* xs = nullptr, bool write = true) {
   const size_t rowoff = (size_t)t * a.H;
   int pp[8];
   const int kk = a.p_r ? min(a.kk, 8) : 0;
@@ -1065,7 +1068,7 @@ __device__ __forceinline__ void combine_row(const CombineArgs& a, int t, float* 
     for (int i = 0; i < kCombPer; ++i) {
       const int h = h0 + i * NTH;
       if (h < a.H) {
-        a.y[rowoff + h] = v[i];
+        if (write) a.y[rowoff + h] = v[i];
         ss = fmaf(v[i], v[i], ss);
       }
     }
@@ -1081,7 +1084,11 @@ __device__ __forceinline__ void combine_row(const CombineArgs& a, int t, float* 
 #pragma unroll
       for (int i = 0; i < kCombPer; ++i) {
         const int h = threadIdx.x + i * NTH;
-        if (h < a.H) a.normed[rowoff + h] = v[i] * r;
+        if (h < a.H) {
+          const float n = v[i] * r;
+          if (write) a.normed[rowoff + h] = n;
+          if (xs != nullptr) xs[h] = n;
+        }
       }
     } else {
       for (int h = threadIdx.x; h < a.H; h += NTH) a.normed[rowoff + h] = a.y[rowoff + h] * r;
@@ -1093,6 +1100,27 @@ __device__ __forceinline__ void combine_row(const CombineArgs& a, int t, float* 
 __global__ __launch_bounds__(kCombThreads) void combine_kernel(CombineArgs a) {
   __shared__ float red[kCombThreads / 64];
   combine_row<kCombThreads>(a, blockIdx.x, red);
+}
+
+// The combine of one layer and the router logits of the next (Eq. 1) in one
+// launch.  Block (t, g) combines position t (the g = 0 blocks write y and
+// RMSNorm(y); every block keeps the normalised row in LDS) and computes the
+// next layer's logits of experts 16 g .. 16 g + 15, one per wave, with the
+// same arithmetic as the routing launch.
+__global__ __launch_bounds__(kCombThreads) void combine_route_kernel(CombineArgs a, RouteArgs r) {
+  __shared__ float red[kCombThreads / 64];
+  const int t = blockIdx.x;
+  combine_row<kCombThreads>(a, t, red, s_dyn, blockIdx.y == 0);
+  __syncthreads();
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int e = blockIdx.y * (kCombThreads / kWave) + wave;
+  if (e < r.sel.N) {
+    const int H4 = r.H >> 2;
+    const float4* xs4 = reinterpret_cast<const float4*>(s_dyn);
+    const float acc = router_dot(reinterpret_cast<const float4*>(r.w) + (size_t)e * H4, H4, lane,
+                                 [&](int h) { return xs4[h]; });
+    if (lane == 0) r.z[(size_t)t * r.sel.N + e] = acc;
+  }
 }
 
 // ------------------------------------------------------------------ launch
@@ -1201,6 +1229,14 @@ hipError_t launch_gateup(const GroupedArgs& a, int wdtype, hipStream_t s) {
 hipError_t launch_down(const GroupedArgs& a, int wdtype, hipStream_t s) {
   if (wdtype == DE_Q4_0) return down_typed<q4_t>(a, s);
   return wdtype == DE_BF16 ? down_typed<uint16_t>(a, s) : down_typed<float>(a, s);
+}
+
+bool combine_route_fits(int H) { return H <= kCombThreads * kCombPer && H % 4 == 0; }
+
+hipError_t launch_combine_route(const CombineArgs& a, const RouteArgs& r, hipStream_t s) {
+  const dim3 grid(a.T, (r.sel.N + kCombThreads / kWave - 1) / (kCombThreads / kWave));
+  hipLaunchKernelGGL(combine_route_kernel, grid, dim3(kCombThreads), (size_t)a.H * 4, s, a, r);
+  return note_hip(hipGetLastError());
 }
 
 hipError_t launch_combine(const CombineArgs& a, hipStream_t s) {

@@ -25,6 +25,18 @@ int cache_experts(const de_cache* c);
 int cache_layers(const de_cache* c);
 bool cache_resident(const de_cache* c, int layer, int e);
 int cache_span(de_cache* c, bool end, int purpose, hipStream_t s);
+int draft_layer_chain(const de_moe_desc* d, int T, const float* x, const float* w_router,
+                      const float* bias, const de_expert_table* routed, const void* shared_w,
+                      const void* draft_w, float gamma, int r, float* y, int32_t* pred_idx,
+                      float* pred_gate, const de_epilogue* epi, void* ws, size_t ws_bytes,
+                      hipStream_t stream, bool logits_ready, const float* next_router);
+int verify_layer_chain(const de_moe_desc* d, int T, const float* x, const float* w_router,
+                       const float* bias, const de_expert_table* routed, const void* shared_w,
+                       float* y, int32_t* topk_idx, float* topk_gate, int32_t* n_union,
+                       int32_t* union_ids, int32_t* offsets, int32_t* tok_list, float* gate_list,
+                       int32_t* pair_pos, const de_epilogue* epi, void* ws, size_t ws_bytes,
+                       hipStream_t stream, bool logits_ready, const float* next_router);
+bool combine_route_fits(int H);
 }
 
 namespace {
@@ -206,22 +218,29 @@ int forward(const de_model& m, int T, const int32_t* tokens, int mode, float* lo
     std::swap(ncur, nnext);
   }
   void* lws = at<void>(ws, L.layer_ws);
+  // Resident layers are chained: each layer's combine also computes the next
+  // layer's router logits, so only the first layer launches its routing.
+  // (Not with per-layer captures, which read each layer's own logits.)
+  const bool chain = cache == nullptr && cap.z == nullptr && de::combine_route_fits(H);
   for (int l = 0; l < m.n_layers; ++l) {
     const de_layer_weights& w = m.layers[l];
     const de_epilogue epi{h, nnext, m.eps};
+    const bool ready = chain && l > 0;
+    const float* next = chain && l + 1 < m.n_layers ? m.layers[l + 1].w_router : nullptr;
     if (cache != nullptr) {
       rc = cached_layer(m, cache, l, T, mode == DE_DRAFT, ncur, h, nnext,
                         mode == DE_TARGET ? n_union : nullptr,
                         pred_idx ? pred_idx + l * pred_stride : nullptr, ws, L, s, deferred);
     } else if (mode == DE_TARGET) {
-      rc = de_verify_layer(&m.moe, T, ncur, w.w_router, w.bias, &w.routed, w.shared_w, h, nullptr,
-                           nullptr, n_union ? n_union + l : nullptr, nullptr, nullptr, nullptr,
-                           nullptr, nullptr, &epi, lws, L.layer_bytes, s);
+      rc = de::verify_layer_chain(&m.moe, T, ncur, w.w_router, w.bias, &w.routed, w.shared_w, h,
+                                  nullptr, nullptr, n_union ? n_union + l : nullptr, nullptr,
+                                  nullptr, nullptr, nullptr, nullptr, &epi, lws, L.layer_bytes, s,
+                                  ready, next);
     } else {
-      rc = de_draft_layer_topr(&m.moe, T, ncur, w.w_router, w.bias, &w.routed, w.shared_w,
-                               w.draft_w, w.gamma, draft_r(m), h,
-                               pred_idx ? pred_idx + l * pred_stride : nullptr, nullptr, &epi, lws,
-                               L.layer_bytes, s);
+      rc = de::draft_layer_chain(&m.moe, T, ncur, w.w_router, w.bias, &w.routed, w.shared_w,
+                                 w.draft_w, w.gamma, draft_r(m), h,
+                                 pred_idx ? pred_idx + l * pred_stride : nullptr, nullptr, &epi,
+                                 lws, L.layer_bytes, s, ready, next);
     }
     if (rc != DE_OK) return rc;
     if (cap.z != nullptr &&

@@ -55,27 +55,7 @@ __global__ __launch_bounds__(kRsThreads) void route_split_kernel(RouteArgs r) {
   const float4* w4 = reinterpret_cast<const float4*>(r.w);
   const int e = blockIdx.y * kRsWaves + wave;
   if (e < N) {
-    // Router row and activation loads of a 2048-element chunk issued together.
-    float acc = 0.f;
-    for (int h0 = 0; h0 < H4; h0 += kWave * 8) {
-      float4 v0[8], xv[8];
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const int h = min(h0 + lane + j * kWave, H4 - 1);  // clamped: in bounds, skipped below
-        v0[j] = w4[(size_t)e * H4 + h];
-        xv[j] = xg[h];
-      }
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        if (h0 + lane + j * kWave < H4) {
-          acc = fmaf(v0[j].x, xv[j].x, acc);
-          acc = fmaf(v0[j].y, xv[j].y, acc);
-          acc = fmaf(v0[j].z, xv[j].z, acc);
-          acc = fmaf(v0[j].w, xv[j].w, acc);
-        }
-      }
-    }
-    acc = wave_sum(acc);
+    const float acc = router_dot(w4 + (size_t)e * H4, H4, lane, [&](int h) { return xg[h]; });
     if (lane == 0) r.z[(size_t)t * N + e] = acc;
   }
   if (!r.select) return;

@@ -381,4 +381,33 @@ __device__ inline void build_union_wave(const TopkUnionArgs& a, const SelView& s
   }
 }
 
+// Router logit of one expert (Eq. 1) by one wave: the dot product of the
+// expert's fp32 router row w (H4 float4s) with x (xf(h) returns float4 h of
+// the position's input), lane-strided in chunks of 8 float4 per lane whose
+// loads are in flight together, then summed over the wave.  Every lane
+// receives the same bits, whichever memory xf reads.
+template <typename XF>
+__device__ __forceinline__ float router_dot(const float4* w, int H4, int lane, XF xf) {
+  float acc = 0.f;
+  for (int h0 = 0; h0 < H4; h0 += kWave * 8) {
+    float4 v0[8], xv[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int h = min(h0 + lane + j * kWave, H4 - 1);  // clamped: in bounds, skipped below
+      v0[j] = w[h];
+      xv[j] = xf(h);
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      if (h0 + lane + j * kWave < H4) {
+        acc = fmaf(v0[j].x, xv[j].x, acc);
+        acc = fmaf(v0[j].y, xv[j].y, acc);
+        acc = fmaf(v0[j].z, xv[j].z, acc);
+        acc = fmaf(v0[j].w, xv[j].w, acc);
+      }
+    }
+  }
+  return wave_sum(acc);
+}
+
 }  // namespace de
