@@ -46,7 +46,7 @@ PMC_TRAFFIC = {
     "sources": ["paper_2607_24434_amd/csrc/grouped_swiglu.hip",
                 "paper_2607_24434_amd/csrc/topk_union.h",
                 "paper_2607_24434_amd/csrc/de_common.h"],
-    "sha256": "a9bb991f37da60d11c9b98fd4bb261069d306de60a8d7e51c5b33c91674587a8",
+    "sha256": "b0a8bffe75e91d88262c65eb1e18fb1a0a12fe8e3df5b1be4afb5ad8df587f71",
 }
 
 

@@ -1110,15 +1110,22 @@ __global__ __launch_bounds__(kCombThreads) void combine_kernel(CombineArgs a) {
 __global__ __launch_bounds__(kCombThreads) void combine_route_kernel(CombineArgs a, RouteArgs r) {
   __shared__ float red[kCombThreads / 64];
   const int t = blockIdx.x;
-  combine_row<kCombThreads>(a, t, red, s_dyn, blockIdx.y == 0);
-  __syncthreads();
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int e = blockIdx.y * (kCombThreads / kWave) + wave;
+  const int H4 = r.H >> 2;
+  const float4* w4 = reinterpret_cast<const float4*>(r.w) + (size_t)min(e, r.sel.N - 1) * H4;
+  // A router row of at most 2048 floats is loaded before the combine (it does
+  // not depend on it), so its latency overlaps the combine's.
+  const bool pre = H4 <= kWave * 8;
+  float4 wp[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) wp[j] = pre ? w4[min(lane + j * kWave, H4 - 1)] : float4{};
+  combine_row<kCombThreads>(a, t, red, s_dyn, blockIdx.y == 0);
+  __syncthreads();
   if (e < r.sel.N) {
-    const int H4 = r.H >> 2;
     const float4* xs4 = reinterpret_cast<const float4*>(s_dyn);
-    const float acc = router_dot(reinterpret_cast<const float4*>(r.w) + (size_t)e * H4, H4, lane,
-                                 [&](int h) { return xs4[h]; });
+    const auto xf = [&](int h) { return xs4[h]; };
+    const float acc = pre ? router_dot_pre(wp, H4, lane, xf) : router_dot(w4, H4, lane, xf);
     if (lane == 0) r.z[(size_t)t * r.sel.N + e] = acc;
   }
 }

@@ -410,4 +410,25 @@ __device__ __forceinline__ float router_dot(const float4* w, int H4, int lane, X
   return wave_sum(acc);
 }
 
+// router_dot for rows of at most kWave * 8 float4 (H <= 2048) with the row
+// already loaded (w[j] = float4 lane + j * kWave, clamped as in router_dot):
+// the same arithmetic, so the same bits.
+template <typename XF>
+__device__ __forceinline__ float router_dot_pre(const float4 (&w)[8], int H4, int lane, XF xf) {
+  float acc = 0.f;
+  float4 xv[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) xv[j] = xf(min(lane + j * kWave, H4 - 1));
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    if (lane + j * kWave < H4) {
+      acc = fmaf(w[j].x, xv[j].x, acc);
+      acc = fmaf(w[j].y, xv[j].y, acc);
+      acc = fmaf(w[j].z, xv[j].z, acc);
+      acc = fmaf(w[j].w, xv[j].w, acc);
+    }
+  }
+  return wave_sum(acc);
+}
+
 }  // namespace de
