@@ -83,6 +83,45 @@ def test_route_topk(name, cfg, T):
     gate_close(gate.cpu().numpy(), gate_o)
 
 
+def _planted_keys(r, N, k):
+    """Distinct logits in [-2, 2) on a 4/N grid (exact in fp32), then equal
+    pairs planted at the top, across the k-th place and at random."""
+    v = (r.permutation(N) - N // 2) * (4.0 / N)
+    order = np.argsort(-v, kind="stable")
+    j = int(r.integers(N))
+    if j != order[0]:
+        v[j] = v[order[0]]
+    if k < N:
+        order = np.argsort(-v, kind="stable")
+        v[order[k]] = v[order[k - 1]]
+    a, b = r.choice(N, 2, replace=False)
+    v[b] = v[a]
+    return v
+
+
+@pytest.mark.parametrize("N,k,score", [(33, 6, 0), (64, 6, 0), (64, 8, 1), (65, 6, 0),
+                                       (128, 16, 1), (256, 8, 0), (256, 1, 1), (8, 8, 0)])
+def test_route_topk_planted_ties(N, k, score):
+    """Selection order with exactly equal keys: larger key first, ties to the
+    lower expert id, against the oracle's stable sort.  Position t's input is
+    the unit vector e_t, so its logits are router column t exactly on both
+    sides.  Covers one candidate per lane (N <= 64) and more (N > 64)."""
+    T, H = 5, 256
+    r = np.random.default_rng(1000 * N + 10 * k + score)
+    w = np.zeros((N, H), np.float32)
+    for t in range(T):
+        w[:, t] = _planted_keys(r, N, k)
+    x = np.zeros((T, H), np.float32)
+    x[np.arange(T), np.arange(T)] = 1.0
+    idx_o, gate_o, _ = moe.route_topk(x, w, None, k, score, False)
+    desc = de.make_desc(H, N, k, 64, 64, 64, score, 0, 1.0, de.DE_BF16)
+    idx = torch.empty(T, k, dtype=torch.int32, device="cuda")
+    gate = torch.empty(T, k, dtype=torch.float32, device="cuda")
+    de.de_route_topk(desc, T, f32(x), f32(w), None, idx, gate, de.workspace(desc, T))
+    np.testing.assert_array_equal(idx.cpu().numpy(), idx_o)
+    gate_close(gate.cpu().numpy(), gate_o)
+
+
 # ------------------------------------------------------------------ union
 
 def union_case(T, k, N, seed):
