@@ -225,7 +225,9 @@ int de_embed_gather(int T, int H, int V, const int32_t* tokens, const void* emb,
                     float* normed, float eps, hipStream_t stream);
 
 /* Dense SwiGLU layer y = E(x) of intermediate I (layer 0 of the stack), with
- * the optional epilogue.  Scratch: de_dense_workspace_bytes(T, I). */
+ * the optional epilogue.  Scratch: de_dense_workspace_bytes(T, H, I).  The
+ * down projection runs in up to three intermediate chunks whose partials are
+ * summed in chunk order. */
 size_t de_dense_workspace_bytes(int T, int H, int I);
 int de_dense_swiglu(int T, int H, int I, int wdtype, const float* x, const void* w, float* y,
                     const de_epilogue* epi, void* ws, size_t ws_bytes, hipStream_t stream);

@@ -36,6 +36,9 @@ int verify_layer_chain(const de_moe_desc* d, int T, const float* x, const float*
                        int32_t* union_ids, int32_t* offsets, int32_t* tok_list, float* gate_list,
                        int32_t* pair_pos, const de_epilogue* epi, void* ws, size_t ws_bytes,
                        hipStream_t stream, bool logits_ready, const float* next_router);
+int dense_swiglu_chain(int T, int H, int I, int wdtype, const float* x, const void* w, float* y,
+                       const de_epilogue* epi, void* ws, size_t ws_bytes, hipStream_t stream,
+                       const de_moe_desc* next_desc, void* next_ws, const float* next_router);
 
 // Bytes of a [rows, cols] weight matrix and of a [G|U|D] expert block.
 size_t mat_bytes(int wdtype, int rows, int cols) {
@@ -698,11 +701,34 @@ int de_embed_gather(int T, int H, int V, const int32_t* tokens, const void* emb,
 
 size_t de_dense_workspace_bytes(int T, int H, int I) {
   if (check_T(T) != DE_OK || H < 1 || I < 1) return 0;
-  return up256((size_t)T * I * 4) + up256((size_t)T * H * 4);
+  return up256((size_t)T * I * 4) + (size_t)kMaxSharedChunks * up256((size_t)T * H * 4);
+}
+
+// Intermediate chunks of a dense layer's down pass: as many as there are
+// dense sources (each a whole number of 16-byte units), so that its few
+// output rows are streamed by three times the waves.
+int dense_chunks(int I, int align) {
+  for (int c = kMaxSharedChunks; c > 1; --c)
+    if (I % c == 0 && (I / c) % align == 0) return c;
+  return 1;
 }
 
 int de_dense_swiglu(int T, int H, int I, int wdtype, const float* x, const void* w, float* y,
                     const de_epilogue* epi, void* ws, size_t ws_bytes, hipStream_t stream) {
+  return de::dense_swiglu_chain(T, H, I, wdtype, x, w, y, epi, ws, ws_bytes, stream, nullptr,
+                                nullptr, nullptr);
+}
+
+}  // extern "C"
+
+namespace de {
+
+// The dense layer in a chain: with next_router, its combine also writes the
+// following MoE layer's router logits (next_desc's shape) to that layer's
+// workspace next_ws, where its call with the logits ready reads them.
+int dense_swiglu_chain(int T, int H, int I, int wdtype, const float* x, const void* w, float* y,
+                       const de_epilogue* epi, void* ws, size_t ws_bytes, hipStream_t stream,
+                       const de_moe_desc* next_desc, void* next_ws, const float* next_router) {
   if (wdtype != DE_F32 && wdtype != DE_BF16) return DE_ERR_UNSUPPORTED;
   const int al = elem_align(wdtype);
   if (check_T(T) != DE_OK || H < al || H % al || I < al || I % al || I > (1 << 17))
@@ -714,6 +740,7 @@ int de_dense_swiglu(int T, int H, int I, int wdtype, const float* x, const void*
     return DE_ERR_WORKSPACE;
   float* A = static_cast<float*>(ws);
   float* P = at<float>(ws, up256((size_t)T * I * 4));
+  const size_t pstride = up256((size_t)T * H * 4) / 4;
   de::GroupedArgs g{};
   g.T = T;
   g.H = H;
@@ -726,27 +753,53 @@ int de_dense_swiglu(int T, int H, int I, int wdtype, const float* x, const void*
   if (timed_phase(DE_PHASE_GATEUP, stream, [&] { return de::launch_gateup(g, wdtype, stream); }) !=
       hipSuccess)
     return DE_ERR_HIP;
-  g.dense[0].w = static_cast<const char*>(w) + 2 * (size_t)I * H * elem_bytes(wdtype);
-  g.dense[0].rows = H;
-  g.dense[0].gate = 1.0f;
-  g.dense[0].vin = A;
-  g.dense[0].vin_stride = I;
-  g.dense[0].out = P;
-  g.dense[0].out_stride = H;
+  // Down: D [H, I] in column chunks, each a dense source with its own partial.
+  const int nc = dense_chunks(I, al);
+  const int cw = I / nc;
+  const char* D = static_cast<const char*>(w) + 2 * (size_t)I * H * elem_bytes(wdtype);
+  g.n_dense = nc;
+  for (int i = 0; i < nc; ++i) {
+    g.dense[i] = de::DenseSrc{};
+    g.dense[i].w = D + (size_t)i * cw * elem_bytes(wdtype);
+    g.dense[i].inter = cw;
+    g.dense[i].ld = I;
+    g.dense[i].rows = H;
+    g.dense[i].gate = 1.0f;
+    g.dense[i].vin = A + (size_t)i * cw;
+    g.dense[i].vin_stride = I;
+    g.dense[i].out = P + (size_t)i * pstride;
+    g.dense[i].out_stride = H;
+  }
   if (timed_phase(DE_PHASE_DOWN, stream, [&] { return de::launch_down(g, wdtype, stream); }) !=
       hipSuccess)
     return DE_ERR_HIP;
   de::CombineArgs c{};
   c.T = T;
   c.H = H;
-  c.n_dense = 1;
-  c.dense_p[0] = P;
+  c.n_dense = nc;
+  for (int i = 0; i < nc; ++i) c.dense_p[i] = P + (size_t)i * pstride;
   c.y = y;
   c.residual = epi ? epi->residual : nullptr;
   c.normed = epi ? epi->normed : nullptr;
   c.eps = epi ? epi->eps : 0.f;
+  if (next_router != nullptr) {
+    if (next_desc == nullptr || next_ws == nullptr || c.normed == nullptr ||
+        next_desc->hidden != H || !de::combine_route_fits(H) || !aligned16(next_router))
+      return DE_ERR_INVALID;
+    de::RouteArgs nr{};
+    nr.sel.T = T;
+    nr.sel.N = next_desc->n_experts;
+    nr.w = next_router;
+    nr.H = H;
+    nr.z = at<float>(next_ws, layout(*next_desc, T).z);
+    return hip_status(de::launch_combine_route(c, nr, stream));
+  }
   return hip_status(de::launch_combine(c, stream));
 }
+
+}  // namespace de
+
+extern "C" {
 
 int de_time_next_phase(int phase, hipEvent_t start, hipEvent_t stop) {
   if (phase != DE_PHASE_GATEUP && phase != DE_PHASE_DOWN) return DE_ERR_INVALID;

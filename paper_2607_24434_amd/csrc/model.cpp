@@ -36,6 +36,9 @@ int verify_layer_chain(const de_moe_desc* d, int T, const float* x, const float*
                        int32_t* union_ids, int32_t* offsets, int32_t* tok_list, float* gate_list,
                        int32_t* pair_pos, const de_epilogue* epi, void* ws, size_t ws_bytes,
                        hipStream_t stream, bool logits_ready, const float* next_router);
+int dense_swiglu_chain(int T, int H, int I, int wdtype, const float* x, const void* w, float* y,
+                       const de_epilogue* epi, void* ws, size_t ws_bytes, hipStream_t stream,
+                       const de_moe_desc* next_desc, void* next_ws, const float* next_router);
 bool combine_route_fits(int H);
 }
 
@@ -210,22 +213,25 @@ int forward(const de_model& m, int T, const int32_t* tokens, int mode, float* lo
   float* nnext = at<float>(ws, L.n1);
   int rc = de_embed_gather(T, H, m.vocab, tokens, m.emb, h, ncur, m.eps, s);
   if (rc != DE_OK) return rc;
+  void* lws = at<void>(ws, L.layer_ws);
+  // Resident layers are chained: each layer's combine (and the dense layer's)
+  // also computes the next layer's router logits, so no MoE layer launches its
+  // own routing.  (Not with per-layer captures, which read each layer's own
+  // logits.)
+  const bool chain = cache == nullptr && cap.z == nullptr && de::combine_route_fits(H);
+  const bool dense_chained = chain && m.dense_inter > 0 && m.n_layers > 0;
   if (m.dense_inter > 0) {
     const de_epilogue epi{h, nnext, m.eps};
-    rc = de_dense_swiglu(T, H, m.dense_inter, m.dense_wdtype, ncur, m.dense_w, h, &epi,
-                         at<void>(ws, L.dense_ws), L.dense_bytes, s);
+    rc = de::dense_swiglu_chain(T, H, m.dense_inter, m.dense_wdtype, ncur, m.dense_w, h, &epi,
+                                at<void>(ws, L.dense_ws), L.dense_bytes, s, &m.moe, lws,
+                                dense_chained ? m.layers[0].w_router : nullptr);
     if (rc != DE_OK) return rc;
     std::swap(ncur, nnext);
   }
-  void* lws = at<void>(ws, L.layer_ws);
-  // Resident layers are chained: each layer's combine also computes the next
-  // layer's router logits, so only the first layer launches its routing.
-  // (Not with per-layer captures, which read each layer's own logits.)
-  const bool chain = cache == nullptr && cap.z == nullptr && de::combine_route_fits(H);
   for (int l = 0; l < m.n_layers; ++l) {
     const de_layer_weights& w = m.layers[l];
     const de_epilogue epi{h, nnext, m.eps};
-    const bool ready = chain && l > 0;
+    const bool ready = chain && (l > 0 || dense_chained);
     const float* next = chain && l + 1 < m.n_layers ? m.layers[l + 1].w_router : nullptr;
     if (cache != nullptr) {
       rc = cached_layer(m, cache, l, T, mode == DE_DRAFT, ncur, h, nnext,
