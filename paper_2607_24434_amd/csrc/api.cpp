@@ -569,6 +569,9 @@ int draft_layer_chain(const de_moe_desc* d, int T, const float* x, const float* 
   a.idx_out = pred_idx ? pred_idx : at<int32_t>(ws, L.idx);
   a.gate_out = pred_gate ? pred_gate : at<float>(ws, L.gate);
   a.ucols = r;  // the drafter reads only the r leading experts of each position
+  // Without the predicted lists and the top-k renormalisation nothing reads
+  // past the r leading entries: the prologue selects only those.
+  a.rounds = (pred_idx == nullptr && pred_gate == nullptr && !d->norm_topk) ? r : 0;
   a.n_union = at<int32_t>(ws, L.nu);
   a.union_ids = at<int32_t>(ws, L.uids);
   a.offsets = at<int32_t>(ws, L.offs);

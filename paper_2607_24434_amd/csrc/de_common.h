@@ -128,6 +128,8 @@ struct TopkUnionArgs {
   int32_t* idx_out;        // [T, k] (may be NULL in union-only mode)
   float* gate_out;
   int ucols;               // union over the first ucols columns of each row (k or 1)
+  int rounds;              // fused selection: leading entries selected per row
+                           // (0: all k; fewer only when nothing reads the rest)
   int32_t* n_union;        // NULL: skip the union
   int32_t* union_ids;
   int32_t* offsets;

@@ -892,9 +892,10 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
           for (int q = 0; q < 4; ++q) z1[0][q] = z0[0][q];
           topk_regs<1>(a.sel, z1, v.idx + t * k, v.sc + t * k);
         }
+        const int kr = a.sel.rounds > 0 ? min(a.sel.rounds, k) : k;
         for (int r = 0; r < 2; ++r) {
           const int tt = t + r * kWavesPB;
-          if (tt < a.T && lane < k) {
+          if (tt < a.T && lane < kr) {
             const float g = topk_gate(a.sel, v.sc + tt * k, lane);
             v.gate[tt * k + lane] = g;
             if (blockIdx.x == 0) {

@@ -68,7 +68,8 @@ __device__ __forceinline__ void topk_load(const TopkUnionArgs& a, const float* z
 // takes the largest remaining key, ties to the lower id: every lane offers
 // its best remaining candidate, a wave max finds the key, a wave min the
 // lowest id offering it, and the owning lane records and retires it.  A NaN
-// key counts as -inf; a candidate id >= N never competes.  One wave.
+// key counts as -inf; a candidate id >= N never competes.  With a.rounds
+// set, only that many leading entries are selected.  One wave.
 template <int R>
 __device__ __forceinline__ void topk_regs(const TopkUnionArgs& a, const float (&z)[R][4],
                                           int32_t* idx0, float* sc0, int32_t* idx1 = nullptr,
@@ -125,7 +126,8 @@ __device__ __forceinline__ void topk_regs(const TopkUnionArgs& a, const float (&
 #pragma unroll
       for (int q = 0; q < 4; ++q) sc[r][q] = ex[r][q] / sum[r];
   }
-  for (int j = 0; j < k; ++j) {
+  const int kr = a.rounds > 0 ? min(a.rounds, k) : k;
+  for (int j = 0; j < kr; ++j) {
     float bk[R];
     int bid[R];
 #pragma unroll

@@ -286,6 +286,27 @@ def test_draft_layer(name, cfg, T, variant):
     assert rel_err(y.cpu().numpy(), y_o) <= y_tol(cfg)
 
 
+@pytest.mark.parametrize("name,cfg,T", DRAFT_CASES + [("cfg2-T5", configs.CFG2, 5)],
+                         ids=[c[0] for c in DRAFT_CASES] + ["cfg2-T5"])
+def test_draft_layer_without_predictions(name, cfg, T):
+    """Without the predicted lists the layer may select only the leading
+    expert (when no top-k renormalisation needs the rest): the output equals
+    the oracle's and, bit for bit, that of the call with the lists."""
+    orc, dev = layer_pair(cfg)
+    x, _ = gapped_x(orc, T, block=1)
+    y_o, _, _ = orc.draft_out(x)
+    ws = dev.ws(T)
+    y0 = torch.empty(T, cfg.hidden, dtype=torch.float32, device="cuda")
+    y1 = torch.empty_like(y0)
+    pidx = torch.empty(T, cfg.top_k, dtype=torch.int32, device="cuda")
+    de.de_draft_layer(dev.desc, T, f32(x), dev.router, dev.bias, dev.table, dev.shared, dev.draft,
+                      cfg.gamma, y0, None, None, ws)
+    de.de_draft_layer(dev.desc, T, f32(x), dev.router, dev.bias, dev.table, dev.shared, dev.draft,
+                      cfg.gamma, y1, pidx, None, ws)
+    assert rel_err(y0.cpu().numpy(), y_o) <= y_tol(cfg)
+    assert torch.equal(y0, y1)
+
+
 def test_draft_layer_zero_draft_expert_equals_no_draft():
     cfg = configs.CFG2
     orc, dev = layer_pair(cfg)
