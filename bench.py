@@ -46,7 +46,7 @@ PMC_TRAFFIC = {
     "sources": ["paper_2607_24434_amd/csrc/grouped_swiglu.hip",
                 "paper_2607_24434_amd/csrc/topk_union.h",
                 "paper_2607_24434_amd/csrc/de_common.h"],
-    "sha256": "b0a8bffe75e91d88262c65eb1e18fb1a0a12fe8e3df5b1be4afb5ad8df587f71",
+    "sha256": "f4d6d92782289d62baef1fc133b3ca93c6555778da9878c162d8b2d5cdbe31c7",
 }
 
 
