@@ -88,13 +88,16 @@ int elem_align(int wdtype) { return wdtype == DE_Q4_0 ? 32 : (wdtype == DE_BF16 
 constexpr int kMaxSharedChunks = 3;
 
 // Chunks of the shared intermediate for the down pass: the fewest (up to
-// max_chunks) whose T input rows fit 64 KB, each a whole number of 16-byte
-// weight units; when none fits, the valid split with the smallest chunk.
-int shared_chunks(int inter, int T, int max_chunks, int align) {
+// max_chunks) whose T input rows fit 64 KB and that are no wider than
+// `width` (the routed experts' intermediate, so that every down tile of the
+// launch streams rows of about the same length), each a whole number of
+// 16-byte weight units; when none qualifies, the valid split with the
+// smallest chunk.
+int shared_chunks(int inter, int T, int max_chunks, int align, int width) {
   int best = 1;
   for (int c = 1; c <= max_chunks; ++c) {
     if (inter % c != 0 || (inter / c) % align != 0) continue;
-    if ((size_t)T * (inter / c) * 4 <= 64 * 1024) return c;
+    if ((size_t)T * (inter / c) * 4 <= 64 * 1024 && inter / c <= width) return c;
     best = c;
   }
   return best;
@@ -264,7 +267,8 @@ int run_grouped(const de_moe_desc& d, int T, const float* x, const de::RoutedSrc
   int nd = 0;
   if (shared_w != nullptr && d.shared_inter > 0) {
     const int max_chunks = kMaxSharedChunks - ((draft_w != nullptr && d.draft_inter > 0) ? 1 : 0);
-    const int chunks = shared_chunks(d.shared_inter, T, max_chunks, elem_align(d.wdtype));
+    const int chunks =
+        shared_chunks(d.shared_inter, T, max_chunks, elem_align(d.wdtype), d.inter);
     const int cl = d.shared_inter / chunks;
     const char* D = static_cast<const char*>(shared_w) +
                     2 * de::mat_bytes(d.wdtype, d.shared_inter, d.hidden);
