@@ -762,13 +762,41 @@ def cpu_baseline(cfg, x, budget_s):
         if time.perf_counter() > t_end or len(times) >= 50:
             break
     t = statistics.median(times)
+    # The same layer on one thread (a quarter of the budget, at least one run).
+    single = []
+    try:
+        from threadpoolctl import threadpool_limits
+        t_end = time.perf_counter() + budget_s / 4
+        with threadpool_limits(limits=1):
+            while True:
+                t0 = time.perf_counter()
+                run()
+                single.append(time.perf_counter() - t0)
+                if time.perf_counter() > t_end or len(single) >= 10:
+                    break
+    except Exception:  # noqa: BLE001
+        single = []
+    host = "unknown CPU"
+    try:
+        with open("/proc/cpuinfo") as f:
+            host = next(l.split(":", 1)[1].strip() for l in f if l.startswith("model name"))
+    except (OSError, StopIteration):
+        pass
+    try:
+        from threadpoolctl import threadpool_info
+        blas = ",".join(sorted({i.get("internal_api", "?") for i in threadpool_info()})) or "none"
+    except Exception:  # noqa: BLE001
+        blas = "unknown"
+    one = (f"; one thread: median {statistics.median(single) * 1e3:.1f} ms over {len(single)} runs"
+           if single else "")
     return {
         "value": round(len(members) * cfg.expert_bytes() / t / 1e9, 4),
         "unit": "GB/s",
         "cores": int(cores),
         "kind": "oracle",
         "sample": f"fp64 oracle verify layer (T={x.shape[0]}, |U|={len(members)}) on the V2-Lite "
-                  f"shape, bf16 weights in host memory, {len(times)} runs, median {t * 1e3:.1f} ms",
+                  f"shape, bf16 weights in host memory, {len(times)} runs, median {t * 1e3:.1f} ms"
+                  f"{one}; {host}, NumPy {np.__version__}, BLAS {blas}",
     }
 
 
