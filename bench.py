@@ -46,7 +46,7 @@ PMC_TRAFFIC = {
     "sources": ["paper_2607_24434_amd/csrc/grouped_swiglu.hip",
                 "paper_2607_24434_amd/csrc/topk_union.h",
                 "paper_2607_24434_amd/csrc/de_common.h"],
-    "sha256": "f4d6d92782289d62baef1fc133b3ca93c6555778da9878c162d8b2d5cdbe31c7",
+    "sha256": "71145a090e007f3f67d92e9bbc5d8c7b6db5ed74706d5f43d4f33cc737aa3765",
 }
 
 

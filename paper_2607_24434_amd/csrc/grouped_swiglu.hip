@@ -949,7 +949,9 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
   __shared__ int s_nlist;
   if (threadIdx.x == 0) {
     const int step = (int)gridDim.x * kWavesPB;
-    int used = 0, n = 0;
+    // A single position's inputs are read from global memory (their loads
+    // overlap the weight loads; staging them first measured slower).
+    int used = a.T == 1 ? a.lds_floats + 1 : 0, n = 0;
     // Dense sources whose tiles this block visits.
     for (int s = 0; s < 3; ++s) s_dact[s] = -1;
     for (int t = blockIdx.x * kWavesPB; t < ly.ndt; t += step) {
@@ -1171,7 +1173,8 @@ size_t staged_bytes(int rows, int len) {
   return (size_t)rows * staged_stride<WTr<WT>::EPU>(len) * sizeof(float);
 }
 
-// The whole block of positions is staged in LDS when it fits the budget.
+// The whole block of positions is staged in LDS when it fits the budget and
+// holds more than one position.
 // Small launches (fewer full tiles than the device has waves) use tiles of
 // one (G, U) pair or two rows, so that more waves share the rows (one row per
 // down tile measured slower: every block then stages every source's input).
@@ -1191,7 +1194,9 @@ hipError_t gateup_typed(const GroupedArgs& a, hipStream_t s) {
   if (max_tiles(a, true, kNS) == 0) return hipSuccess;
   const size_t tabs = tables_bytes(a);
   const size_t lds = staged_bytes<WT>(a.T, a.H);
-  if (lds + tabs <= (size_t)kLdsBudget) return gateup_tiles<WT, true>(a, lds + tabs, s);
+  // Staged unless a single position (read from global memory alongside the
+  // weights, as in the down pass).
+  if (lds + tabs <= (size_t)kLdsBudget && a.T > 1) return gateup_tiles<WT, true>(a, lds + tabs, s);
   return gateup_tiles<WT, false>(a, tabs, s);
 }
 
