@@ -32,6 +32,10 @@ CASES = [
     ("cfg3-T5", configs.CFG3, 5),
     ("cfg3-T9", configs.CFG3, 9),
     ("cfg3-T17", configs.CFG3, 17),
+    # The largest block the ABI takes: 64-bit position masks up to bit 63,
+    # positions read from global memory, eight positions per selecting wave.
+    ("cfg1-T64", configs.CFG1, 64),
+    ("cfg2-T64", configs.CFG2, 64),
 ]
 IDS = [c[0] for c in CASES]
 
