@@ -46,7 +46,7 @@ PMC_TRAFFIC = {
     "sources": ["paper_2607_24434_amd/csrc/grouped_swiglu.hip",
                 "paper_2607_24434_amd/csrc/topk_union.h",
                 "paper_2607_24434_amd/csrc/de_common.h"],
-    "sha256": "71145a090e007f3f67d92e9bbc5d8c7b6db5ed74706d5f43d4f33cc737aa3765",
+    "sha256": "1e15e8d28d6fd0fbbd06f91dd29ef84356f151f74836aa6d7e876f0193ff415a",
 }
 
 

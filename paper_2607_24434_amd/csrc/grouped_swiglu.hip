@@ -7,8 +7,8 @@
 // HBM bandwidth, not arithmetic.  The design keeps the memory system busy
 // without pause and touches each weight byte once:
 //
-//  * Persistent 512-thread blocks over a tile list: the union members' row
-//    tiles, then each dense source's.  Wave w of block b takes the tiles
+//  * Persistent 512-thread blocks over a tile list: each dense source's row
+//    tiles, then the union members'.  Wave w of block b takes the tiles
 //    b*8 + w, then every (grid*8)-th one, so at any moment the whole grid
 //    streams a narrow window of consecutive rows.  The union size stays in
 //    device memory; the member table (weight block, first pair, positions)
@@ -22,9 +22,10 @@
 //    runs kRing iterations ahead of the consumer across pass and tile
 //    boundaries, so the next tile's first loads are in flight while the
 //    current one finishes and its sums are reduced.
-//  * Activations come from LDS (the block of positions staged once, in a
-//    bank-conflict-free order) or, for the grouped down, from the small
-//    L2-resident A rows.
+//  * Activations come from LDS: gate/up stages the block of positions once,
+//    in a bank-conflict-free order; down stages the input rows of the
+//    sources a block visits, as far as they fit.  A single position, and
+//    rows that do not fit, are read from global memory.
 //  * bf16 -> fp32 by a shift or mask, fp32 accumulation; a row sum is four DPP
 //    steps inside 16 lanes and two cross-row shuffles, identical in every
 //    lane.  No float atomics: results are bitwise reproducible.
