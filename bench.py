@@ -46,7 +46,7 @@ PMC_TRAFFIC = {
     "sources": ["paper_2607_24434_amd/csrc/grouped_swiglu.hip",
                 "paper_2607_24434_amd/csrc/topk_union.h",
                 "paper_2607_24434_amd/csrc/de_common.h"],
-    "sha256": "1e15e8d28d6fd0fbbd06f91dd29ef84356f151f74836aa6d7e876f0193ff415a",
+    "sha256": "568db70214a5b68cc041ccdef9a97080abaa2ef520f23030270f05b255933f7a",
 }
 
 

@@ -742,6 +742,10 @@ int dense_swiglu_chain(int T, int H, int I, int wdtype, const float* x, const vo
     return DE_ERR_INVALID;
   if (!x || !w || !y || !aligned16(x) || !aligned16(w)) return DE_ERR_INVALID;
   if (check_epi(epi) != DE_OK) return DE_ERR_INVALID;
+  if (next_router != nullptr &&
+      (next_desc == nullptr || next_ws == nullptr || epi == nullptr || epi->normed == nullptr ||
+       next_desc->hidden != H || !de::combine_route_fits(H) || !aligned16(next_router)))
+    return DE_ERR_INVALID;
   if (ws == nullptr || (reinterpret_cast<uintptr_t>(ws) & 255u) != 0 ||
       ws_bytes < de_dense_workspace_bytes(T, H, I))
     return DE_ERR_WORKSPACE;
@@ -790,9 +794,6 @@ int dense_swiglu_chain(int T, int H, int I, int wdtype, const float* x, const vo
   c.normed = epi ? epi->normed : nullptr;
   c.eps = epi ? epi->eps : 0.f;
   if (next_router != nullptr) {
-    if (next_desc == nullptr || next_ws == nullptr || c.normed == nullptr ||
-        next_desc->hidden != H || !de::combine_route_fits(H) || !aligned16(next_router))
-      return DE_ERR_INVALID;
     de::RouteArgs nr{};
     nr.sel.T = T;
     nr.sel.N = next_desc->n_experts;

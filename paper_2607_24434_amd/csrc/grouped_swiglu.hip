@@ -1248,6 +1248,8 @@ hipError_t launch_down(const GroupedArgs& a, int wdtype, hipStream_t s) {
 bool combine_route_fits(int H) { return H <= kCombThreads * kCombPer && H % 4 == 0; }
 
 hipError_t launch_combine_route(const CombineArgs& a, const RouteArgs& r, hipStream_t s) {
+  // The normalised row is held in LDS: a row that does not fit is an error.
+  if (!combine_route_fits(a.H) || r.H != a.H) return note_hip(hipErrorInvalidValue);
   const dim3 grid(a.T, (r.sel.N + kCombThreads / kWave - 1) / (kCombThreads / kWave));
   hipLaunchKernelGGL(combine_route_kernel, grid, dim3(kCombThreads), (size_t)a.H * 4, s, a, r);
   return note_hip(hipGetLastError());
