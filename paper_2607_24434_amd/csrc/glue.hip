@@ -19,6 +19,65 @@ __device__ __forceinline__ bool am_better(float va, int ia, float vb, int ib) {
   return va > vb || (va == vb && ia < ib);
 }
 
+constexpr int kRowThreads = 1024;
+
+// K = 0: the argmax of the single row by one block (each thread scans a
+// strided slice in 16-byte loads when the row allows), with no cross-block
+// step; out = (0, argmax).
+__global__ __launch_bounds__(kRowThreads) void argmax_row_kernel(AcceptArgs a) {
+  __shared__ float sv[kRowThreads / 64];
+  __shared__ int si[kRowThreads / 64];
+  const float* p = a.logits;
+  float bv = -INFINITY;
+  int bi = INT_MAX;
+  const auto offer = [&](float xv, int v) {
+    if (!(xv == xv)) xv = -INFINITY;
+    if (am_better(xv, v, bv, bi)) {
+      bv = xv;
+      bi = v;
+    }
+  };
+  if ((a.V & 3) == 0 && (reinterpret_cast<uintptr_t>(p) & 15u) == 0) {
+    const float4* p4 = reinterpret_cast<const float4*>(p);
+    const int n4 = a.V >> 2;
+#pragma unroll 4
+    for (int j = threadIdx.x; j < n4; j += kRowThreads) {
+      const float4 q = p4[j];
+      offer(q.x, 4 * j);
+      offer(q.y, 4 * j + 1);
+      offer(q.z, 4 * j + 2);
+      offer(q.w, 4 * j + 3);
+    }
+  } else {
+    for (int v = threadIdx.x; v < a.V; v += kRowThreads) offer(p[v], v);
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const float ov = __shfl_xor(bv, o, kWave);
+    const int oi = __shfl_xor(bi, o, kWave);
+    if (am_better(ov, oi, bv, bi)) {
+      bv = ov;
+      bi = oi;
+    }
+  }
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  if (lane == 0) {
+    sv[wave] = bv;
+    si[wave] = bi;
+  }
+  __syncthreads();
+  if (threadIdx.x != 0) return;
+  for (int w = 1; w < kRowThreads / 64; ++w)
+    if (am_better(sv[w], si[w], sv[0], si[0])) {
+      sv[0] = sv[w];
+      si[0] = si[w];
+    }
+  const int t = si[0] == INT_MAX ? 0 : si[0];
+  a.amax[0] = t;
+  a.out[0] = 0;
+  a.out[1] = t;
+}
+
 // Grid (chunks, K+1).  Each block finds the argmax of one 4096-logit chunk of
 // one row; the last block of a row (device-scope counter) reduces the row's
 // chunk results in chunk order, and the last row to finish applies the greedy
@@ -164,6 +223,10 @@ __global__ __launch_bounds__(256) void stream_probe_kernel(const u32x4* __restri
 int accept_chunks(int V) { return (V + kAmChunk - 1) / kAmChunk; }
 
 hipError_t launch_argmax_accept(const AcceptArgs& a, hipStream_t s) {
+  if (a.K == 0) {
+    hipLaunchKernelGGL(argmax_row_kernel, dim3(1), dim3(kRowThreads), 0, s, a);
+    return note_hip(hipGetLastError());
+  }
   hipLaunchKernelGGL(argmax_accept_kernel, dim3(accept_chunks(a.V), a.K + 1), dim3(kAmThreads), 0,
                      s, a);
   return note_hip(hipGetLastError());

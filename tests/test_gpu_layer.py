@@ -386,7 +386,7 @@ def test_lm_head_and_argmax(V, H, T):
 
 
 @pytest.mark.parametrize("K", [0, 1, 4, 8, 16])
-@pytest.mark.parametrize("V", [1000, 102400])
+@pytest.mark.parametrize("V", [1000, 1003, 102400])
 def test_accept_len_planted_prefix(K, V):
     r = np.random.default_rng(1000 * K + V)
     logits = r.standard_normal((K + 1, V)).astype(np.float32)
@@ -417,3 +417,21 @@ def test_argmax_ties_go_to_lowest_index():
     de.de_accept_len(2, V, f32(logits), i32([17, 0]), amax, out, de.accept_workspace(2, V))
     np.testing.assert_array_equal(amax.cpu().numpy(), [17, 0, V - 1])
     assert out.cpu().tolist() == [2, V - 1]
+
+
+@pytest.mark.parametrize("V", [4096, 4099])
+def test_single_row_argmax_ties_and_nan(V):
+    """K = 0 (one row, the draft loop's case): ties go to the lowest index and
+    a NaN counts as -infinity, in 16-byte loads (V = 4096) and element loads
+    (V = 4099); an all-NaN row gives index 0."""
+    logits = np.zeros((1, V), np.float32)
+    logits[0, 3] = np.nan
+    logits[0, [11, 4000, V - 1]] = 7.0
+    amax = torch.empty(1, dtype=torch.int32, device="cuda")
+    out = torch.empty(2, dtype=torch.int32, device="cuda")
+    ws = de.accept_workspace(0, V)
+    de.de_accept_len(0, V, f32(logits), None, amax, out, ws)
+    assert int(amax.item()) == 11 and out.cpu().tolist() == [0, 11]
+    nan_row = np.full((1, V), np.nan, np.float32)
+    de.de_accept_len(0, V, f32(nan_row), None, amax, out, ws)
+    assert int(amax.item()) == 0 and out.cpu().tolist() == [0, 0]
