@@ -87,6 +87,26 @@ def test_cached_step_equals_resident_and_bookkeeping_equals_oracle():
     cache.close()
 
 
+def test_q4_cached_step_equals_resident():
+    """Q4_0 experts through the cache: the cached step (slot copies of 4.87 MB
+    blocks, chunked verification when the union exceeds the slots) equals the
+    resident step bit for bit."""
+    model = replace(SMALL, moe=configs.CFG5_Q4.moe, name="v2lite-offload-q4-small")
+    K = model.k_draft
+    dm, cache = build(model)
+    for r in range(2):
+        c = gen.start_token(model, redraw=r)
+        res = run_step(dm, model, c)
+        got = run_step(dm, model, c, cached=cache)
+        for a, b, name in zip(got, res, ("block", "argmax", "out", "n_union", "pred")):
+            assert np.array_equal(a, b), name
+    st = cache.stats()
+    print(f"q4 cached: stats {st}", flush=True)
+    assert st["bytes_copied"] == (st["prefetch_issued"] + st["demand_loads"]) * model.moe.expert_bytes()
+    assert st["draft_needed"] == 2 * K * model.n_moe_layers
+    cache.close()
+
+
 def test_full_offload_stack_cached_equals_resident():
     model = configs.CFG5
     K, L = model.k_draft, model.n_moe_layers

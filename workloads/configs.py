@@ -142,5 +142,8 @@ def scaled_model(base: ModelCfg, *, n_moe_layers: int | None = None, vocab: int 
 # Section 4.1): routed, shared and draft experts 4.5 bits per weight.
 CFG1_Q4 = replace(CFG1, name="tiny-q4", cfg_id=7, wdtype=Q4_0)
 CFG2_Q4 = replace(CFG2, name="v2lite-q4", cfg_id=6, wdtype=Q4_0)
+# The offload stack with Q4_0 experts (the paper's mobile pairing of the 4.5-bit
+# format with offloaded experts); same seeds, routers and Zipf biases as CFG5.
+CFG5_Q4 = replace(CFG5, name="v2lite-offload-q4", moe=replace(CFG5.moe, wdtype=Q4_0))
 
 ALL_LAYER_CFGS = {"cfg1": CFG1, "cfg2": CFG2, "cfg3": CFG3}
