@@ -40,7 +40,7 @@ PEAK_HBM_GBS = 8000.0
 # factors in profiles/verify_layer_v2lite_T9.md).  Valid only for the kernel
 # sources they were measured on: reported as null once those change.
 PMC_TRAFFIC = {
-    "bytes_per_launch": 463.50e6,
+    "bytes_per_launch": 463.49e6,
     "vs_algorithmic": 1.004,
     "union_mean": 38.0,
     "sources": ["paper_2607_24434_amd/csrc/grouped_swiglu.hip",
