@@ -40,7 +40,7 @@
 extern "C" {
 #endif
 
-#define DE_ABI_VERSION 1
+#define DE_ABI_VERSION 2
 
 /* Return codes. */
 #define DE_OK 0
@@ -48,7 +48,8 @@ extern "C" {
 #define DE_ERR_UNSUPPORTED (-2)  /* dtype or option combination not implemented */
 #define DE_ERR_HIP (-3)          /* a HIP launch or runtime call failed */
 #define DE_ERR_WORKSPACE (-4)    /* ws NULL or smaller than de_workspace_bytes() */
-#define DE_ERR_NOT_RESIDENT (-5) /* expert cache: a needed expert has no slot */
+#define DE_ERR_NOT_RESIDENT (-5) /* a needed routed expert had no valid slot (Section 3.5:
+                                    a missed expert must be loaded, never dropped) */
 
 /* Router score functions (the router distribution R_l of Section 3.2). */
 #define DE_SOFTMAX 0 /* scores softmax(z + b); selection key z + b */
@@ -87,8 +88,14 @@ typedef struct de_moe_desc {
 
 /* Where routed expert e lives: base + slot_of_expert[e] * slot_stride_bytes.
  * slot_of_expert NULL means slot e (all experts resident, in order).
- * A slot < 0 or >= n_slots marks an expert that is not resident: its work is
- * skipped (the expert cache guarantees residency before it launches). */
+ * A slot < 0 or >= n_slots marks an expert that is not resident.  The paper's
+ * runtime loads a missed expert on demand and never drops it (Section 3.5,
+ * Algorithm 1); the expert cache below does so before it launches.  A layer
+ * call that meets a needed expert without a valid slot cannot load it: that
+ * expert's term is left out of y (its partials are zero, nothing stale is
+ * summed) and the workspace's status word records it, so that the next
+ * de_layer_status (de_model_status for the model calls) returns
+ * DE_ERR_NOT_RESIDENT. */
 typedef struct de_expert_table {
   const void* base;              /* device: slot 0 */
   int64_t slot_stride_bytes;     /* >= 3*I*H*elem, multiple of 16 */
@@ -99,7 +106,8 @@ typedef struct de_expert_table {
 /* Optional fused epilogue of a layer call.  With residual != NULL the layer
  * writes y = residual + layer(x) (the pre-norm residual stack); with
  * normed != NULL it also writes RMSNorm(y) = y / sqrt(mean(y^2) + eps), the
- * next layer's input.  residual may alias y. */
+ * next layer's input.  residual may alias y (one block per position writes
+ * each row after reading it); normed must not alias residual. */
 typedef struct de_epilogue {
   const float* residual; /* device [T, H] or NULL */
   float* normed;         /* device [T, H] or NULL */
@@ -121,9 +129,18 @@ size_t de_workspace_bytes(const de_moe_desc* d, int T);
 
 /* Zeroes the control words at the start of a freshly allocated workspace
  * (enqueued on `stream`).  Required once per allocation before its first use
- * by a layer call; every layer call leaves them zero again.  Calls that share
- * one workspace must not run concurrently. */
+ * by a layer call; every layer call leaves its counters zero again.  Calls
+ * that share one workspace must not run concurrently. */
 int de_workspace_init(void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Device-side conditions of the layer calls made on workspace ws (a
+ * de_workspace_bytes workspace), surfaced on the host: waits for `stream`,
+ * reads the workspace's status word and clears it.  Returns DE_OK,
+ * DE_ERR_NOT_RESIDENT when some call since the last check met a needed routed
+ * expert whose slot is outside [0, n_slots) (its term was dropped; see
+ * de_expert_table), DE_ERR_WORKSPACE for a bad ws, DE_ERR_HIP on a failed
+ * copy.  Host-synchronous by design; the layer calls themselves never wait. */
+int de_layer_status(void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* Router scoring and top-k selection (Eq. 1) with the gates of Eq. (4).
  *   x [T, H], w_router [N, H], bias [N] or NULL.
@@ -219,10 +236,11 @@ int de_lm_head(int T, int H, int V, const float* x, const void* w_lm, float* log
 int de_rmsnorm(int T, int H, const float* x, float eps, float* out, hipStream_t stream);
 
 /* h [T, H] = fp32(emb[tokens[t]]) with emb bf16 [V, H]; tokens is a device
- * int32 array (ids are clamped into [0, V)).  normed (may be NULL) receives
- * RMSNorm(h). */
+ * int32 array.  normed (may be NULL) receives RMSNorm(h).  A token id outside
+ * [0, V) reads nothing: its rows of h and normed are NaN, and status (a device
+ * int32, may be NULL) gets bit 2 set (OR-ed in, never cleared here). */
 int de_embed_gather(int T, int H, int V, const int32_t* tokens, const void* emb, float* h,
-                    float* normed, float eps, hipStream_t stream);
+                    float* normed, float eps, int32_t* status, hipStream_t stream);
 
 /* Dense SwiGLU layer y = E(x) of intermediate I (layer 0 of the stack), with
  * the optional epilogue.  Scratch: de_dense_workspace_bytes(T, H, I).  The
@@ -279,6 +297,13 @@ size_t de_model_workspace_bytes(const de_model* m, int T);
 /* Host-only validation of a model (DE_OK or an error code).  Checks the MoE
  * shape, every layer's pointers and table, and the glue's sizes. */
 int de_check_model(const de_model* m);
+
+/* Device-side conditions of the model calls made on workspace ws, as
+ * de_layer_status: DE_ERR_NOT_RESIDENT when a MoE layer met a needed routed
+ * expert without a valid slot (a table of m->layers marks it absent),
+ * DE_ERR_INVALID when a token id outside [0, vocab) reached the embedding.
+ * Waits for `stream` and clears the word. */
+int de_model_status(const de_model* m, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* Logits of T independent positions (each a token id, device int32 [T]):
  * logits [T, V] fp32; argmax [T] (may be NULL) the row argmax, ties to the

@@ -44,6 +44,7 @@ C_FUNCS = [
     "de_cache_table", "de_cache_stats", "de_cache_slots", "de_spec_step_cached",
     "de_confidence", "de_expansion", "de_spec_step_trunc", "de_draft_layer_topr",
     "de_residual_target", "de_layer_router_logits", "de_row_kl", "de_distill_signals",
+    "de_layer_status", "de_model_status",
 ]
 DE_PHASE_GATEUP = 0
 DE_PHASE_DOWN = 1
@@ -159,7 +160,9 @@ def _load(path: str = LIB_PATH, strict: bool = True):
         "de_accept_len": (I, [I, I, P, P, P, P, P, SZ, P]),
         "de_lm_head": (I, [I, I, I, P, P, P, P]),
         "de_rmsnorm": (I, [I, I, P, F, P, P]),
-        "de_embed_gather": (I, [I, I, I, P, P, P, P, F, P]),
+        "de_embed_gather": (I, [I, I, I, P, P, P, P, F, P, P]),
+        "de_layer_status": (I, [P, SZ, P]),
+        "de_model_status": (I, [MP, P, SZ, P]),
         "de_dense_workspace_bytes": (SZ, [I, I, I]),
         "de_dense_swiglu": (I, [I, I, I, I, P, P, P, EP, P, SZ, P]),
         "de_stream_probe": (I, [P, SZ, P, P]),
@@ -341,10 +344,19 @@ def de_rmsnorm(T, H, x, eps, out, stream=None):
                                         _stream(stream)))
 
 
-def de_embed_gather(T, H, V, tokens, emb, h, normed=None, eps=1e-6, stream=None):
+def de_embed_gather(T, H, V, tokens, emb, h, normed=None, eps=1e-6, status=None, stream=None):
     _check("de_embed_gather", LIB.de_embed_gather(int(T), int(H), int(V), _ptr(tokens), _ptr(emb),
                                                   _ptr(h), _ptr(normed), float(eps),
-                                                  _stream(stream)))
+                                                  _ptr(status), _stream(stream)))
+
+
+def de_layer_status(ws, stream=None) -> int:
+    """The workspace's device status as a return code (0, or -5 / -1); waits and clears."""
+    return LIB.de_layer_status(_ptr(ws), ws.numel(), _stream(stream))
+
+
+def de_model_status(model, ws, stream=None) -> int:
+    return LIB.de_model_status(ctypes.byref(model), _ptr(ws), ws.numel(), _stream(stream))
 
 
 def de_dense_workspace_bytes(T, H, I) -> int:

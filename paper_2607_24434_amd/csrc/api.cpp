@@ -103,6 +103,9 @@ int shared_chunks(int inter, int T, int max_chunks, int align, int width) {
   return best;
 }
 
+constexpr size_t kCtlBytes = 512;
+constexpr size_t kStatusOff = 256;
+
 struct Layout {
   size_t ctl, z, idx, gate, nu, uids, offs, tok, glist, ppos;
   size_t a_r, a_s, a_d, p_r, p_s, p_d;
@@ -118,7 +121,10 @@ Layout layout(const de_moe_desc& d, int T) {
     return r;
   };
   const size_t tk = (size_t)T * d.top_k;
-  L.ctl = take(256);  // counters: zero after de_workspace_init and after every call
+  // Control area: the routing launch's arrival counters [T] (zero after
+  // de_workspace_init and after every call), then the status word at byte 256
+  // (sticky until de_layer_status reads it).
+  L.ctl = take(kCtlBytes);
   L.z = take((size_t)T * d.n_experts * 4);
   L.idx = take(tk * 4);
   L.gate = take(tk * 4);
@@ -196,8 +202,11 @@ T* at(void* ws, size_t off) {
 // drafter's top-1), which bounds the union by T * kk.
 de::RoutedSrc routed_src(const de_moe_desc& d, int T, int kk, const de_expert_table* tab,
                          const int32_t* nu, const int32_t* uids, const int32_t* offs,
-                         const int32_t* tok, const float* glist, float* a_r, float* p_r) {
+                         const int32_t* tok, const float* glist, float* a_r, float* p_r,
+                         int32_t* status) {
   de::RoutedSrc r{};
+  r.status = status;
+  r.absent_ok = 0;
   r.base = static_cast<const char*>(tab->base);
   r.stride = tab->slot_stride_bytes;
   r.slot_of_expert = tab->slot_of_expert;
@@ -335,6 +344,20 @@ int run_grouped(const de_moe_desc& d, int T, const float* x, const de::RoutedSrc
 
 namespace de {
 
+int32_t* layer_status_word(void* ws) { return at<int32_t>(ws, kStatusOff); }
+
+// Reads the status word after the stream's work so far, clears it, and maps
+// its bits to a return code (a missing expert first).
+int take_status(int32_t* word, hipStream_t stream) {
+  int32_t v = 0;
+  if (hipMemcpyAsync(&v, word, sizeof(v), hipMemcpyDeviceToHost, stream) != hipSuccess ||
+      hipStreamSynchronize(stream) != hipSuccess)
+    return DE_ERR_HIP;
+  if (v == 0) return DE_OK;
+  if (hipMemsetAsync(word, 0, sizeof(v), stream) != hipSuccess) return DE_ERR_HIP;
+  return (v & kStatusNotResident) ? DE_ERR_NOT_RESIDENT : DE_ERR_INVALID;
+}
+
 // The grouped part of a layer whose routing already ran: the union of the
 // first `ucols` entries of each position's lists idx / gate [T, k] (device),
 // built in the gate/up prologue, then gate/up and down over the members the
@@ -377,9 +400,12 @@ int layer_after_route(const de_moe_desc& d, int T, const float* x, const de_expe
   a.gate_list = at<float>(ws, L.glist);
   a.pair_pos = at<int32_t>(ws, L.ppos);
   a.z = at<float>(ws, L.z);
-  const RoutedSrc r = routed_src(d, T, ucols, routed, a.n_union, a.union_ids, a.offsets,
-                                 a.tok_list, a.gate_list, at<float>(ws, L.a_r),
-                                 at<float>(ws, L.p_r));
+  RoutedSrc r = routed_src(d, T, ucols, routed, a.n_union, a.union_ids, a.offsets, a.tok_list,
+                           a.gate_list, at<float>(ws, L.a_r), at<float>(ws, L.p_r),
+                           at<int32_t>(ws, L.ctl + kStatusOff));
+  // The cache marks every member outside the requested chunk absent on
+  // purpose: their work is skipped, not reported.
+  r.absent_ok = 1;
   return run_grouped(d, T, x, r, a.pair_pos, ucols, shared_w, draft_w, gamma, y, epi, L, ws, &a,
                      stream, dense_on, combine_on);
 }
@@ -401,7 +427,7 @@ const char* de_error_string(int code) {
     case DE_ERR_UNSUPPORTED: return "unsupported dtype or option combination";
     case DE_ERR_HIP: return "HIP launch or runtime error";
     case DE_ERR_WORKSPACE: return "workspace missing, misaligned (256 B) or too small";
-    case DE_ERR_NOT_RESIDENT: return "a needed expert is not resident in the expert cache";
+    case DE_ERR_NOT_RESIDENT: return "a needed routed expert had no valid slot (its term was dropped)";
     default: return "unknown error code";
   }
 }
@@ -501,8 +527,8 @@ int de_grouped_swiglu(const de_moe_desc* d, int T, const float* x, const de_expe
   if ((rc = check_ws(*d, T, ws, ws_bytes)) != DE_OK) return rc;
   const Layout L = layout(*d, T);
   const de::RoutedSrc r = routed_src(*d, T, d->top_k, routed, n_union, union_ids, offsets,
-                                     tok_list, gate_list,
-                                     at<float>(ws, L.a_r), at<float>(ws, L.p_r));
+                                     tok_list, gate_list, at<float>(ws, L.a_r),
+                                     at<float>(ws, L.p_r), at<int32_t>(ws, L.ctl + kStatusOff));
   return run_grouped(*d, T, x, r, pair_pos, d->top_k, shared_w, nullptr, 0.f, y, epi, L, ws,
                      nullptr, stream);
 }
@@ -589,7 +615,7 @@ int draft_layer_chain(const de_moe_desc* d, int T, const float* x, const float* 
     return DE_ERR_HIP;
   const de::RoutedSrc rs = routed_src(*d, T, r, routed, a.n_union, a.union_ids, a.offsets,
                                       a.tok_list, a.gate_list, at<float>(ws, L.a_r),
-                                      at<float>(ws, L.p_r));
+                                      at<float>(ws, L.p_r), at<int32_t>(ws, L.ctl + kStatusOff));
   return run_grouped(*d, T, x, rs, a.pair_pos, r, shared_w, draft_w, gamma, y, epi, L, ws, &a,
                      stream, true, true, true, next_router);
 }
@@ -634,7 +660,7 @@ int verify_layer_chain(const de_moe_desc* d, int T, const float* x, const float*
     return DE_ERR_HIP;
   const de::RoutedSrc r = routed_src(*d, T, d->top_k, routed, a.n_union, a.union_ids,
                                      a.offsets, a.tok_list, a.gate_list, at<float>(ws, L.a_r),
-                                     at<float>(ws, L.p_r));
+                                     at<float>(ws, L.p_r), at<int32_t>(ws, L.ctl + kStatusOff));
   return run_grouped(*d, T, x, r, a.pair_pos, d->top_k, shared_w, nullptr, 0.f, y, epi, L, ws, &a,
                      stream, true, true, true, next_router);
 }
@@ -699,11 +725,17 @@ int de_rmsnorm(int T, int H, const float* x, float eps, float* out, hipStream_t 
 }
 
 int de_embed_gather(int T, int H, int V, const int32_t* tokens, const void* emb, float* h,
-                    float* normed, float eps, hipStream_t stream) {
+                    float* normed, float eps, int32_t* status, hipStream_t stream) {
   if (T < 1 || T > 65536 || H < 1 || V < 1 || !tokens || !emb || !h || !(eps >= 0.f))
     return DE_ERR_INVALID;
   return hip_status(de::launch_embed(T, H, V, tokens, static_cast<const uint16_t*>(emb), h, normed,
-                                     eps, stream));
+                                     eps, status, stream));
+}
+
+int de_layer_status(void* ws, size_t ws_bytes, hipStream_t stream) {
+  if (ws == nullptr || (reinterpret_cast<uintptr_t>(ws) & 255u) != 0 || ws_bytes < kCtlBytes)
+    return DE_ERR_WORKSPACE;
+  return de::take_status(de::layer_status_word(ws), stream);
 }
 
 size_t de_dense_workspace_bytes(int T, int H, int I) {

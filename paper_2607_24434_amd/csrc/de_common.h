@@ -115,7 +115,18 @@ struct RoutedSrc {
   int inter;                   // I
   float* a;                    // A_r [pairs, I]
   float* p;                    // P_r [pairs, H]
+  // A union member whose slot is outside [0, n_slots): with absent_ok (the
+  // expert cache's chunked calls, which mark the other chunks' members absent
+  // on purpose) its work is skipped; otherwise its partial rows are written as
+  // zeros (its term drops out of y) and block 0 of the gate/up launch stores
+  // kStatusNotResident into *status (when not NULL).
+  int absent_ok;
+  int32_t* status;
 };
+
+// Bits of the device status word of a workspace.
+constexpr int32_t kStatusNotResident = 1;
+constexpr int32_t kStatusBadToken = 2;
 
 struct TopkUnionArgs {
   int T, N, k;
@@ -224,7 +235,7 @@ int accept_chunks(int V);
 hipError_t launch_argmax_accept(const AcceptArgs& a, hipStream_t s);
 hipError_t launch_rmsnorm(int T, int H, const float* x, float eps, float* out, hipStream_t s);
 hipError_t launch_embed(int T, int H, int V, const int32_t* tokens, const uint16_t* emb, float* h,
-                        float* normed, float eps, hipStream_t s);
+                        float* normed, float eps, int32_t* status, hipStream_t s);
 hipError_t launch_stream_probe(const void* buf, size_t bytes, float* sink, hipStream_t s);
 
 // Truncation of the draft loop.

@@ -177,14 +177,25 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(int H, const float* __rest
   for (int h = threadIdx.x; h < H; h += 256) out[off + h] = x[off + h] * r;
 }
 
+// A token id outside [0, V) reads no embedding row: its h (and normed) row is
+// NaN, so nothing downstream passes for a real token, and *status (when not
+// NULL) receives kStatusBadToken.
 __global__ __launch_bounds__(256) void embed_kernel(int H, int V, const int32_t* __restrict__ tokens,
                                                     const uint16_t* __restrict__ emb, float* h,
-                                                    float* normed, float eps) {
+                                                    float* normed, float eps, int32_t* status) {
   __shared__ float red[4];
-  int tok = tokens[blockIdx.x];
-  tok = tok < 0 ? 0 : (tok >= V ? V - 1 : tok);
-  const uint16_t* row = emb + (size_t)tok * H;
+  const int tok = tokens[blockIdx.x];
   const size_t off = (size_t)blockIdx.x * H;
+  if (tok < 0 || tok >= V) {
+    for (int i = threadIdx.x; i < H; i += 256) {
+      h[off + i] = __builtin_nanf("");
+      if (normed) normed[off + i] = __builtin_nanf("");
+    }
+    if (threadIdx.x == 0 && status != nullptr)
+      __hip_atomic_fetch_or(status, kStatusBadToken, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    return;
+  }
+  const uint16_t* row = emb + (size_t)tok * H;
   float ss = 0.f;
   for (int i = threadIdx.x; i < H; i += 256) {
     const float v = __uint_as_float((uint32_t)row[i] << 16);
@@ -238,8 +249,9 @@ hipError_t launch_rmsnorm(int T, int H, const float* x, float eps, float* out, h
 }
 
 hipError_t launch_embed(int T, int H, int V, const int32_t* tokens, const uint16_t* emb, float* h,
-                        float* normed, float eps, hipStream_t s) {
-  hipLaunchKernelGGL(embed_kernel, dim3(T), dim3(256), 0, s, H, V, tokens, emb, h, normed, eps);
+                        float* normed, float eps, int32_t* status, hipStream_t s) {
+  hipLaunchKernelGGL(embed_kernel, dim3(T), dim3(256), 0, s, H, V, tokens, emb, h, normed, eps,
+                     status);
   return note_hip(hipGetLastError());
 }
 

@@ -321,14 +321,18 @@ __device__ __forceinline__ SelView sel_at(const GroupedArgs& a, const Tables& tb
 // The member table from a union built in LDS: member j = the expert with
 // union index j.  All threads; the caller synchronises.
 __device__ __forceinline__ void members_from_union(const GroupedArgs& a, const Tables& tb,
-                                                   const SelView& v, int first, int stride) {
+                                                   const SelView& v, int first, int stride,
+                                                   int* absent) {
   const RoutedSrc& r = a.r;
   for (int e = first; e < a.sel.N; e += stride) {
     const unsigned long long m = v.mask[e];
     if (m == 0ull) continue;
     const int slot = e < r.n_experts ? (r.slot_of_expert ? r.slot_of_expert[e] : e) : -1;
     Member mb{nullptr, v.off[e], (int)__popcll(m), -1, 0};
-    if (slot >= 0 && slot < r.n_slots) mb.blk = r.base + (size_t)slot * r.stride;
+    if (slot >= 0 && slot < r.n_slots)
+      mb.blk = r.base + (size_t)slot * r.stride;
+    else
+      *absent = 1;
     tb.mem[v.upos[e]] = mb;
   }
 }
@@ -372,9 +376,11 @@ __device__ __forceinline__ void fill_dense(const GroupedArgs& a, const Tables& t
 
 // Resolves the union members into LDS.  Lists built by the union kernel always
 // pass; caller-supplied ones are checked so that a bad list can only drop
-// work, never read or write out of bounds.  All threads; the caller
-// synchronises.
-__device__ __forceinline__ void fill_tables(const GroupedArgs& a, const Tables& tb, int nu) {
+// work, never read or write out of bounds.  A member with a valid list and no
+// valid slot keeps its list (blk NULL) and sets *absent.  All threads; the
+// caller synchronises.
+__device__ __forceinline__ void fill_tables(const GroupedArgs& a, const Tables& tb, int nu,
+                                            int* absent) {
   const RoutedSrc& r = a.r;
   for (int j = threadIdx.x; j < nu; j += kBlock) {
     Member m{nullptr, 0, 0, -1, 0};
@@ -382,10 +388,13 @@ __device__ __forceinline__ void fill_tables(const GroupedArgs& a, const Tables& 
     const int slot =
         (e >= 0 && e < r.n_experts) ? (r.slot_of_expert ? r.slot_of_expert[e] : e) : -1;
     const int off = r.offsets[j], end = r.offsets[j + 1];
-    if (slot >= 0 && slot < r.n_slots && off >= 0 && end >= off && end <= r.pairs_max) {
-      m.blk = r.base + (size_t)slot * r.stride;
+    if (off >= 0 && end >= off && end <= r.pairs_max) {
       m.off = off;
       m.ntok = end - off;
+      if (slot >= 0 && slot < r.n_slots)
+        m.blk = r.base + (size_t)slot * r.stride;
+      else if (m.ntok > 0)
+        *absent = 1;
     }
     tb.mem[j] = m;
   }
@@ -856,6 +865,8 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
   // Fused selection: the wave's first two positions' logits are loaded
   // before the staging so that their latency overlaps it.
   const bool sel = a.fuse_route && a.fuse_select;
+  __shared__ int s_absent;
+  if (threadIdx.x == 0) s_absent = 0;
   float z0[2][4];
 #pragma unroll
   for (int r = 0; r < 2; ++r) {
@@ -916,16 +927,20 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
     if (wave == 0) {
       build_union_wave(a.sel, v, blockIdx.x == 0, tb.tok, tb.gate);
       const int n = uni(v.misc[1]);
-      if (n > 0) members_from_union(a, tb, v, lane, kWave);
+      if (n > 0) members_from_union(a, tb, v, lane, kWave, &s_absent);
     }
     __syncthreads();
     nu = uni(v.misc[1]);
     nu = nu < 0 ? 0 : min(nu, a.r.max_union);
   } else {
     nu = routed_count(a);
-    if (a.has_routed) fill_tables(a, tb, nu);
+    __syncthreads();  // s_absent is initialised
+    if (a.has_routed) fill_tables(a, tb, nu, &s_absent);
     __syncthreads();
   }
+  // A needed member without a slot: reported once per launch.
+  if (blockIdx.x == 0 && threadIdx.x == 0 && s_absent && !a.r.absent_ok && a.r.status != nullptr)
+    *(DE_GLOBAL int32_t*)a.r.status |= kStatusNotResident;
   const Layout ly = make_layout<RT>(a, nu, true);
   run_tiles<WT, true, RT>(a, ly, tb, LDSX ? staged_stride<EPU>(a.H) : a.H, LDSX, lane, wave);
 }
@@ -941,9 +956,25 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
   const int lane = threadIdx.x & 63, wave = uni((int)(threadIdx.x >> 6));
   const int nu = routed_count(a);
   const Tables tb = tables_at(a, a.lds_floats);
-  fill_dense(a, tb);
-  if (a.has_routed) fill_tables(a, tb, nu);
+  __shared__ int s_absent;
+  if (threadIdx.x == 0) s_absent = 0;
   __syncthreads();
+  fill_dense(a, tb);
+  if (a.has_routed) fill_tables(a, tb, nu, &s_absent);
+  __syncthreads();
+  if (s_absent && !a.r.absent_ok) {
+    // A needed member without a slot contributes zero partials (the combine
+    // sums its pairs like any other), spread over the grid.
+    const size_t gstride = (size_t)gridDim.x * kBlock;
+    for (int j = 0; j < nu; ++j) {
+      const Member m = tb.mem[j];
+      if (m.blk != nullptr || m.ntok <= 0) continue;
+      float* p = a.r.p + (size_t)m.off * a.H;
+      const size_t n = (size_t)m.ntok * a.H;
+      for (size_t i = (size_t)blockIdx.x * kBlock + threadIdx.x; i < n; i += gstride)
+        *(DE_GLOBAL float*)(p + i) = 0.f;
+    }
+  }
   Layout ly = make_layout<RT>(a, nu, false);
   __shared__ int s_dact[3];
   __shared__ int s_list[kMaxStaged + 1];
@@ -1247,9 +1278,22 @@ hipError_t launch_down(const GroupedArgs& a, int wdtype, hipStream_t s) {
 
 bool combine_route_fits(int H) { return H <= kCombThreads * kCombPer && H % 4 == 0; }
 
+// True when the [T, H] fp32 rows at p and q share any byte.
+static bool rows_overlap(const float* p, const float* q, int T, int H) {
+  if (p == nullptr || q == nullptr) return false;
+  const uintptr_t a = reinterpret_cast<uintptr_t>(p), b = reinterpret_cast<uintptr_t>(q);
+  const uintptr_t n = (uintptr_t)T * H * sizeof(float);
+  return a < b + n && b < a + n;
+}
+
 hipError_t launch_combine_route(const CombineArgs& a, const RouteArgs& r, hipStream_t s) {
   // The normalised row is held in LDS: a row that does not fit is an error.
   if (!combine_route_fits(a.H) || r.H != a.H) return note_hip(hipErrorInvalidValue);
+  // Every block of a position re-reads its residual row while block 0 of the
+  // position writes y and the normalised row: none of them may share memory.
+  if (rows_overlap(a.residual, a.y, a.T, a.H) || rows_overlap(a.residual, a.normed, a.T, a.H) ||
+      rows_overlap(a.y, a.normed, a.T, a.H))
+    return note_hip(hipErrorInvalidValue);
   const dim3 grid(a.T, (r.sel.N + kCombThreads / kWave - 1) / (kCombThreads / kWave));
   hipLaunchKernelGGL(combine_route_kernel, grid, dim3(kCombThreads), (size_t)a.H * 4, s, a, r);
   return note_hip(hipGetLastError());

@@ -40,6 +40,8 @@ int dense_swiglu_chain(int T, int H, int I, int wdtype, const float* x, const vo
                        const de_epilogue* epi, void* ws, size_t ws_bytes, hipStream_t stream,
                        const de_moe_desc* next_desc, void* next_ws, const float* next_router);
 bool combine_route_fits(int H);
+int32_t* layer_status_word(void* ws);
+int take_status(int32_t* word, hipStream_t stream);
 }
 
 namespace {
@@ -63,7 +65,7 @@ struct ModelLayout {
   size_t dense_ws, dense_bytes;
   size_t misc;                // int32 [2]: acceptance output of the argmax-only calls
   size_t ridx, rgate;         // top-k lists of the cached step's routing [64, k]
-  size_t h, n0, n1, logits;   // residual stream, two normed buffers, logits
+  size_t h, h2, n0, n1, logits;  // residual stream (two buffers), two normed buffers, logits
   size_t uhat, tctl;          // truncation: predicted verifier set [L, words], decision [5]
   size_t zt, zd, logits2;     // distillation: router logits of both passes [L, T, N], draft logits
   size_t total;
@@ -79,7 +81,8 @@ ModelLayout model_layout(const de_model& m, int T) {
   };
   const size_t H = (size_t)m.moe.hidden;
   L.accept_bytes = de_accept_workspace_bytes(kMaxBlock - 1, m.vocab);
-  L.layer_bytes = m.n_layers > 0 ? de_workspace_bytes(&m.moe, T) : 0;
+  // At least the control area: its status word also serves the embedding.
+  L.layer_bytes = std::max<size_t>(de_workspace_bytes(&m.moe, T), 512);
   L.dense_bytes = m.dense_inter > 0 ? de_dense_workspace_bytes(T, (int)H, m.dense_inter) : 0;
   L.accept_ws = take(L.accept_bytes);
   L.layer_ws = take(L.layer_bytes);
@@ -88,6 +91,7 @@ ModelLayout model_layout(const de_model& m, int T) {
   L.ridx = take((size_t)kMaxBlock * m.moe.top_k * 4);
   L.rgate = take((size_t)kMaxBlock * m.moe.top_k * 4);
   L.h = take((size_t)T * H * 4);
+  L.h2 = take((size_t)T * H * 4);
   L.n0 = take((size_t)T * H * 4);
   L.n1 = take((size_t)T * H * 4);
   L.logits = take((size_t)T * m.vocab * 4);
@@ -131,8 +135,9 @@ struct ArgmaxOut {
 // the rest, each in ascending id); every chunk runs gate/up and down over its
 // members, the first also over the shared path, the last also the combine.
 int cached_layer(const de_model& m, de_cache* c, int l, int T, bool draft, const float* x,
-                 float* h, float* normed_out, int32_t* n_union, int32_t* pred_out, void* ws,
-                 const ModelLayout& L, hipStream_t s, std::vector<int32_t>* deferred) {
+                 const float* h_in, float* h_out, float* normed_out, int32_t* n_union,
+                 int32_t* pred_out, void* ws, const ModelLayout& L, hipStream_t s,
+                 std::vector<int32_t>* deferred) {
   const de_layer_weights& w = m.layers[l];
   const int k = m.moe.top_k, N = m.moe.n_experts;
   const int purpose = draft ? DE_NEED_DRAFT : DE_NEED_VERIFY;
@@ -154,7 +159,7 @@ int cached_layer(const de_model& m, de_cache* c, int l, int T, bool draft, const
     if (hb[i] < 0 || hb[i] >= N) return DE_ERR_INVALID;
   de_expert_table tab;
   if ((rc = de_cache_table(c, l, &tab)) != DE_OK) return rc;
-  const de_epilogue epi{h, normed_out, m.eps};
+  const de_epilogue epi{h_in, normed_out, m.eps};
   if (draft) {
     // The drafter's own experts: its r leading ones.
     const int r = draft_r(m);
@@ -164,7 +169,7 @@ int cached_layer(const de_model& m, de_cache* c, int l, int T, bool draft, const
     else if ((rc = de_cache_prefetch(c, l, hb, k)) != DE_OK)
       return rc;
     rc = de::layer_after_route(m.moe, 1, x, &tab, ridx, rgate, r, w.shared_w, w.draft_w, w.gamma,
-                               h, &epi, true, true, nullptr, lws, L.layer_bytes, s);
+                               h_out, &epi, true, true, nullptr, lws, L.layer_bytes, s);
     if (rc != DE_OK) return rc;
     if ((rc = de_cache_release(c, l, s)) != DE_OK) return rc;
     return de::cache_span(c, true, purpose, s);
@@ -182,7 +187,7 @@ int cached_layer(const de_model& m, de_cache* c, int l, int T, bool draft, const
     const int lo = ci * S, cnt = std::min(S, n - lo);
     if ((rc = de_cache_ensure(c, l, order.data() + lo, cnt, DE_NEED_VERIFY, s)) != DE_OK)
       return rc;
-    rc = de::layer_after_route(m.moe, T, x, &tab, ridx, rgate, k, w.shared_w, nullptr, 0.f, h,
+    rc = de::layer_after_route(m.moe, T, x, &tab, ridx, rgate, k, w.shared_w, nullptr, 0.f, h_out,
                                &epi, ci == 0, ci == chunks - 1, n_union ? n_union + l : nullptr,
                                lws, L.layer_bytes, s);
     if (rc != DE_OK) return rc;
@@ -208,12 +213,18 @@ int forward(const de_model& m, int T, const int32_t* tokens, int mode, float* lo
             void* ws, const ModelLayout& L, hipStream_t s, de_cache* cache = nullptr,
             std::vector<int32_t>* deferred = nullptr, const Capture& cap = Capture{}) {
   const int H = m.moe.hidden;
+  // The residual stream ping-pongs between two buffers: a layer reads h and
+  // writes h + F(RMSNorm(h)) to the other one.  In the chained launches every
+  // block of a position re-reads the residual row while one of them writes the
+  // output row, so the two must never be the same memory.
   float* h = at<float>(ws, L.h);
+  float* hnext = at<float>(ws, L.h2);
   float* ncur = at<float>(ws, L.n0);
   float* nnext = at<float>(ws, L.n1);
-  int rc = de_embed_gather(T, H, m.vocab, tokens, m.emb, h, ncur, m.eps, s);
-  if (rc != DE_OK) return rc;
   void* lws = at<void>(ws, L.layer_ws);
+  int rc = de_embed_gather(T, H, m.vocab, tokens, m.emb, h, ncur, m.eps,
+                           de::layer_status_word(lws), s);
+  if (rc != DE_OK) return rc;
   // Resident layers are chained: each layer's combine (and the dense layer's)
   // also computes the next layer's router logits, so no MoE layer launches its
   // own routing.  (Not with per-layer captures, which read each layer's own
@@ -222,11 +233,12 @@ int forward(const de_model& m, int T, const int32_t* tokens, int mode, float* lo
   const bool dense_chained = chain && m.dense_inter > 0 && m.n_layers > 0;
   if (m.dense_inter > 0) {
     const de_epilogue epi{h, nnext, m.eps};
-    rc = de::dense_swiglu_chain(T, H, m.dense_inter, m.dense_wdtype, ncur, m.dense_w, h, &epi,
+    rc = de::dense_swiglu_chain(T, H, m.dense_inter, m.dense_wdtype, ncur, m.dense_w, hnext, &epi,
                                 at<void>(ws, L.dense_ws), L.dense_bytes, s, &m.moe, lws,
                                 dense_chained ? m.layers[0].w_router : nullptr);
     if (rc != DE_OK) return rc;
     std::swap(ncur, nnext);
+    std::swap(h, hnext);
   }
   for (int l = 0; l < m.n_layers; ++l) {
     const de_layer_weights& w = m.layers[l];
@@ -234,17 +246,17 @@ int forward(const de_model& m, int T, const int32_t* tokens, int mode, float* lo
     const bool ready = chain && (l > 0 || dense_chained);
     const float* next = chain && l + 1 < m.n_layers ? m.layers[l + 1].w_router : nullptr;
     if (cache != nullptr) {
-      rc = cached_layer(m, cache, l, T, mode == DE_DRAFT, ncur, h, nnext,
+      rc = cached_layer(m, cache, l, T, mode == DE_DRAFT, ncur, h, hnext, nnext,
                         mode == DE_TARGET ? n_union : nullptr,
                         pred_idx ? pred_idx + l * pred_stride : nullptr, ws, L, s, deferred);
     } else if (mode == DE_TARGET) {
-      rc = de::verify_layer_chain(&m.moe, T, ncur, w.w_router, w.bias, &w.routed, w.shared_w, h,
-                                  nullptr, nullptr, n_union ? n_union + l : nullptr, nullptr,
+      rc = de::verify_layer_chain(&m.moe, T, ncur, w.w_router, w.bias, &w.routed, w.shared_w,
+                                  hnext, nullptr, nullptr, n_union ? n_union + l : nullptr, nullptr,
                                   nullptr, nullptr, nullptr, nullptr, &epi, lws, L.layer_bytes, s,
                                   ready, next);
     } else {
       rc = de::draft_layer_chain(&m.moe, T, ncur, w.w_router, w.bias, &w.routed, w.shared_w,
-                                 w.draft_w, w.gamma, draft_r(m), h,
+                                 w.draft_w, w.gamma, draft_r(m), hnext,
                                  pred_idx ? pred_idx + l * pred_stride : nullptr, nullptr, &epi,
                                  lws, L.layer_bytes, s, ready, next);
     }
@@ -258,6 +270,7 @@ int forward(const de_model& m, int T, const int32_t* tokens, int mode, float* lo
             DE_OK)
       return rc;
     std::swap(ncur, nnext);
+    std::swap(h, hnext);
   }
   rc = de_lm_head(T, H, m.vocab, ncur, m.lm_head, logits, s);
   if (rc != DE_OK || am.amax == nullptr) return rc;
@@ -303,6 +316,15 @@ int de_check_model(const de_model* m) {
 size_t de_model_workspace_bytes(const de_model* m, int T) {
   if (de_check_model(m) != DE_OK || T < 1 || T > kMaxBlock) return 0;
   return model_layout(*m, T).total;
+}
+
+int de_model_status(const de_model* m, void* ws, size_t ws_bytes, hipStream_t stream) {
+  int rc = de_check_model(m);
+  if (rc != DE_OK) return rc;
+  if ((rc = check_block(*m, 1, ws, ws_bytes)) != DE_OK) return rc;
+  // The layer scratch sits at an offset that does not depend on the block
+  // length, so its status word is found with the one-position layout.
+  return de::take_status(de::layer_status_word(at<void>(ws, model_layout(*m, 1).layer_ws)), stream);
 }
 
 int de_model_forward(const de_model* m, int T, const int32_t* tokens, int mode, float* logits,

@@ -33,7 +33,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_version_and_error_strings():
-    assert de.de_abi_version() == 1
+    assert de.de_abi_version() == 2
     for code in (0, -1, -2, -3, -4, -5):
         assert de.de_error_string(code) != "unknown error code"
     assert de.de_error_string(42) == "unknown error code"
@@ -129,10 +129,13 @@ def test_other_entry_points_reject_bad_arguments_on_host():
     assert L.de_workspace_init(FAKE, 16, None) == -4
     assert L.de_lm_head(9, 2044, 1000, FAKE, FAKE, FAKE, None) == -1
     assert L.de_rmsnorm(0, 16, FAKE, 1e-6, FAKE, None) == -1
-    assert L.de_embed_gather(1, 16, 0, FAKE, FAKE, FAKE, None, 1e-6, None) == -1
+    assert L.de_embed_gather(1, 16, 0, FAKE, FAKE, FAKE, None, 1e-6, None, None) == -1
     assert L.de_dense_swiglu(9, 2048, 10944, 3, FAKE, FAKE, FAKE, None, FAKE, 1 << 30, None) == -2
     assert L.de_dense_swiglu(9, 2048, 10944, 1, FAKE, FAKE, FAKE, None, FAKE, 64, None) == -4
     assert L.de_stream_probe(FAKE, 100, FAKE, None) == -1
+    assert L.de_layer_status(None, 1 << 20, None) == -4
+    assert L.de_layer_status(FAKE + 16, 1 << 20, None) == -4    # ws must be 256-B aligned
+    assert L.de_layer_status(FAKE, 256, None) == -4             # smaller than the control area
     assert de.de_dense_workspace_bytes(9, 2048, 10944) >= 9 * (10944 + 2048) * 4
 
 
@@ -196,3 +199,6 @@ def test_model_workspace_and_step_reject_bad_arguments_on_host():
     assert L.de_greedy_decode(mp, -1, FAKE, FAKE, big, None) == -1
     assert L.de_greedy_decode(mp, 4, FAKE, FAKE, 64, None) == -4
     assert L.de_check_model(None) == -1
+    assert L.de_model_status(None, FAKE, big, None) == -1
+    assert L.de_model_status(mp, FAKE, 64, None) == -4
+    assert L.de_model_status(ctypes.byref(fake_model(vocab=0)), FAKE, big, None) == -1

@@ -141,3 +141,66 @@ def test_full_stack_step_is_deterministic(full_model):
         torch.cuda.synchronize()
         res.append((block.cpu().tolist(), amax.cpu().tolist(), out.cpu().tolist(), nu.cpu().tolist()))
     assert res[0] == res[1]
+
+
+_CHAIN: dict = {}
+
+
+def _chain_model():
+    """The 2-layer V2-Lite stack for blocks of up to 64 positions, with its tensors."""
+    if "dm" not in _CHAIN:
+        import paper_2607_24434_amd as de
+        model = V2_SMALL
+        m = model.moe
+        t = wgpu.model_tensors(model)
+        desc = de.make_desc(m.hidden, m.n_experts, m.top_k, m.inter, m.shared_inter,
+                            m.draft_inter, m.score_func, m.norm_topk, m.routed_scale, m.wdtype)
+        _CHAIN.update(t=t, desc=desc, dm=de.DeviceModel(
+            desc, t["layers"], model.vocab, t["emb"], t["lm"], t["dense"], model.dense_inter,
+            de.DE_BF16, model.eps, m.gamma, 64))
+    return _CHAIN["t"], _CHAIN["desc"], _CHAIN["dm"]
+
+
+@pytest.mark.parametrize("mode", ["target", "draft"])
+@pytest.mark.parametrize("T", [4, 8, 16, 64])
+def test_chained_forward_equals_layer_calls(T, mode):
+    """The stacked forward chains its launches (each combine also computes the
+    next layer's router logits, in blocks that all read the position's
+    residual row while one of them writes the output row).  It must give the
+    same bits as the same stack run through the public layer calls one by
+    one, at block lengths whose blocks of one position can share an XCD."""
+    import paper_2607_24434_amd as de
+    t, desc, dm = _chain_model()
+    model, m = V2_SMALL, V2_SMALL.moe
+    H, V = m.hidden, model.vocab
+    dmode = de.DE_TARGET if mode == "target" else de.DE_DRAFT
+    toks = torch.from_numpy(np.random.default_rng(T).integers(0, V, T).astype(np.int32)).cuda()
+    chained = torch.empty(T, V, dtype=torch.float32, device="cuda")
+    dm.forward(toks, dmode, chained)
+    assert de.de_model_status(dm.model, dm.ws) == 0
+    # The same stack, one public call per stage, ping-pong buffers.
+    h = [torch.empty(T, H, dtype=torch.float32, device="cuda") for _ in range(2)]
+    n = [torch.empty(T, H, dtype=torch.float32, device="cuda") for _ in range(2)]
+    de.de_embed_gather(T, H, V, toks, t["emb"], h[0], n[0], model.eps)
+    dws = torch.zeros(de.de_dense_workspace_bytes(T, H, model.dense_inter), dtype=torch.uint8,
+                      device="cuda")
+    de.de_dense_swiglu(T, H, model.dense_inter, de.DE_BF16, n[0], t["dense"], h[1], dws,
+                       epi=de.make_epilogue(residual=h[0], normed=n[1], eps=model.eps))
+    cur = 1
+    ws = de.workspace(desc, T)
+    stride = m.expert_bytes()
+    for lw in t["layers"]:
+        tab = de.make_table(lw["routed"], stride, None, m.n_experts)
+        epi = de.make_epilogue(residual=h[cur], normed=n[1 - cur], eps=model.eps)
+        if mode == "target":
+            de.de_verify_layer(desc, T, n[cur], lw["router"], lw["bias"], tab, lw["shared"],
+                               h[1 - cur], ws=ws, epi=epi)
+        else:
+            de.de_draft_layer(desc, T, n[cur], lw["router"], lw["bias"], tab, lw["shared"],
+                              lw["draft"], m.gamma, h[1 - cur], None, None, ws, epi=epi)
+        cur = 1 - cur
+    calls = torch.empty(T, V, dtype=torch.float32, device="cuda")
+    de.de_lm_head(T, H, V, n[cur], t["lm"], calls)
+    torch.cuda.synchronize()
+    assert de.de_layer_status(ws) == 0
+    assert torch.equal(chained, calls)
