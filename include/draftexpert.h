@@ -212,6 +212,25 @@ int de_verify_layer(const de_moe_desc* d, int T, const float* x, const float* w_
                     int32_t* pair_pos, const de_epilogue* epi, void* ws, size_t ws_bytes,
                     hipStream_t stream);
 
+/* de_verify_layer for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * the same kernels and results, with the layer's scratch taken from a
+ * file-scope device array of de_noalloc_scratch_bytes() bytes (16 MiB) that
+ * each GPU holds until the process ends, instead of a caller workspace.  The
+ * call allocates nothing.  DE_ERR_WORKSPACE when de_workspace_bytes(d, T)
+ * exceeds that size.  Every call on one GPU shares that GPU's array: calls
+ * that overlap on one GPU (other streams, other host threads) race.  A needed
+ * routed expert without a valid slot has its term dropped as in
+ * de_verify_layer, but nothing reports it (use de_verify_layer and
+ * de_layer_status for that). */
+size_t de_noalloc_scratch_bytes(void);
+int de_verify_layer_noalloc(const de_moe_desc* d, int T, const float* x, const float* w_router,
+                            const float* bias, const de_expert_table* routed, const void* shared_w,
+                            float* y, int32_t* topk_idx, float* topk_gate, int32_t* n_union,
+                            int32_t* union_ids, int32_t* offsets, int32_t* tok_list,
+                            float* gate_list, int32_t* pair_pos, const de_epilogue* epi,
+                            hipStream_t stream);
+
 /* Greedy exact acceptance (Algorithm 1, verify and accept):
  *   target_argmax[j] = argmax_v target_logits[j, v] (ties to the lowest v,
  *   NaN treated as -inf), j = 0..K; out[0] = n = largest m <= K with

@@ -44,7 +44,7 @@ C_FUNCS = [
     "de_cache_table", "de_cache_stats", "de_cache_slots", "de_spec_step_cached",
     "de_confidence", "de_expansion", "de_spec_step_trunc", "de_draft_layer_topr",
     "de_residual_target", "de_layer_router_logits", "de_row_kl", "de_distill_signals",
-    "de_layer_status", "de_model_status",
+    "de_layer_status", "de_model_status", "de_noalloc_scratch_bytes", "de_verify_layer_noalloc",
 ]
 DE_PHASE_GATEUP = 0
 DE_PHASE_DOWN = 1
@@ -162,6 +162,8 @@ def _load(path: str = LIB_PATH, strict: bool = True):
         "de_rmsnorm": (I, [I, I, P, F, P, P]),
         "de_embed_gather": (I, [I, I, I, P, P, P, P, F, P, P]),
         "de_layer_status": (I, [P, SZ, P]),
+        "de_noalloc_scratch_bytes": (SZ, []),
+        "de_verify_layer_noalloc": (I, [DP, I, P, P, P, TP, P, P, P, P, P, P, P, P, P, P, EP, P]),
         "de_model_status": (I, [MP, P, SZ, P]),
         "de_dense_workspace_bytes": (SZ, [I, I, I]),
         "de_dense_swiglu": (I, [I, I, I, I, P, P, P, EP, P, SZ, P]),
@@ -315,6 +317,20 @@ def de_verify_layer(desc, T, x, w_router, bias, table, shared_w, y, topk_idx=Non
         _ptr(shared_w), _ptr(y), _ptr(topk_idx), _ptr(topk_gate), _ptr(n_union), _ptr(union_ids),
         _ptr(offsets), _ptr(tok_list), _ptr(gate_list), _ptr(pair_pos), _epi_arg(epi), _ptr(ws),
         ws.numel() if ws is not None else 0, _stream(stream)))
+
+
+def de_noalloc_scratch_bytes() -> int:
+    return LIB.de_noalloc_scratch_bytes()
+
+
+def de_verify_layer_noalloc(desc, T, x, w_router, bias, table, shared_w, y, topk_idx=None,
+                            topk_gate=None, n_union=None, union_ids=None, offsets=None,
+                            tok_list=None, gate_list=None, pair_pos=None, epi=None, stream=None):
+    _check("de_verify_layer_noalloc", LIB.de_verify_layer_noalloc(
+        ctypes.byref(desc), int(T), _ptr(x), _ptr(w_router), _ptr(bias), ctypes.byref(table),
+        _ptr(shared_w), _ptr(y), _ptr(topk_idx), _ptr(topk_gate), _ptr(n_union), _ptr(union_ids),
+        _ptr(offsets), _ptr(tok_list), _ptr(gate_list), _ptr(pair_pos), _epi_arg(epi),
+        _stream(stream)))
 
 
 def de_accept_workspace_bytes(K, V) -> int:
