@@ -2,8 +2,11 @@
 // HIP call), scratch layout, and the launch sequence of each layer call.
 #include "../../include/draftexpert.h"
 #include "de_common.h"
+#include "draft_persistent.h"
 
+#include <atomic>
 #include <cmath>
+#include <cstdlib>
 #include <cstring>
 
 namespace de {
@@ -103,12 +106,19 @@ int shared_chunks(int inter, int T, int max_chunks, int align, int width) {
   return best;
 }
 
-constexpr size_t kCtlBytes = 512;
+constexpr size_t kCtlBytes = 4096;
 constexpr size_t kStatusOff = 256;
+// The persistent draft pass's arrival flags: at an offset that does not
+// depend on the block length, which no other call writes (a call with
+// another block length lays its buffers out differently).
+constexpr size_t kPDFlagsOff = 1024;
+static_assert(kPDFlagsOff + (de::kPDMaxGrid + 32) * 8 <= kCtlBytes, "control area");
+
 
 struct Layout {
   size_t ctl, z, idx, gate, nu, uids, offs, tok, glist, ppos;
   size_t a_r, a_s, a_d, p_r, p_s, p_d;
+  size_t pd;  // persistent draft pass: gate/up outputs [Is + Id + I], row sums [H], logits [N]
   size_t total;
 };
 
@@ -122,8 +132,9 @@ Layout layout(const de_moe_desc& d, int T) {
   };
   const size_t tk = (size_t)T * d.top_k;
   // Control area: the routing launch's arrival counters [T] (zero after
-  // de_workspace_init and after every call), then the status word at byte 256
-  // (sticky until de_layer_status reads it).
+  // de_workspace_init and after every call), the status word at byte 256
+  // (sticky until de_layer_status reads it), the persistent draft pass's
+  // flags from byte 1024.
   L.ctl = take(kCtlBytes);
   L.z = take((size_t)T * d.n_experts * 4);
   L.idx = take(tk * 4);
@@ -140,6 +151,7 @@ Layout layout(const de_moe_desc& d, int T) {
   L.p_r = take(tk * d.hidden * 4);
   L.p_s = take((size_t)kMaxSharedChunks * T * d.hidden * 4);
   L.p_d = take((size_t)T * d.hidden * 4);
+  L.pd = take(((size_t)d.shared_inter + d.draft_inter + d.inter + d.hidden + d.n_experts) * 4);
   L.total = o;
   return L;
 }
@@ -345,6 +357,112 @@ int run_grouped(const de_moe_desc& d, int T, const float* x, const de::RoutedSrc
 namespace de {
 
 int32_t* layer_status_word(void* ws) { return at<int32_t>(ws, kStatusOff); }
+
+// The persistent draft pass is used unless DE_DRAFT_PERSISTENT is "0" (the
+// separate launches then run every draft layer; both give the same bits).
+bool draft_persistent_enabled() {
+  const char* e = std::getenv("DE_DRAFT_PERSISTENT");
+  return e == nullptr || e[0] != '0';
+}
+
+// Runs draft layers layers[0..n) (n >= 2) of one position (T = 1, the top-1
+// drafter of Eq. 5) in persistent launches of at most kPDMaxLayers layers.  x_in is the
+// first layer's input RMSNorm(h), h_in its residual (NULL: y = layer(x));
+// z_ready: the first layer's router logits are already in the workspace's
+// logit row.  Returns kPDNotApplicable, before enqueueing anything, when the
+// shape or the layers do not fit the kernel.
+int draft_persistent_run(const de_moe_desc& d, int n, const PDLayer* layers, const float* x_in,
+                         const float* h_in, bool z_ready, float* y_out, float* normed_out,
+                         int32_t* pred_idx, float* pred_gate, float eps, void* ws,
+                         size_t ws_bytes, hipStream_t s) {
+  // A single layer is faster as separate launches (no cooperative launch,
+  // no in-kernel routing).
+  if (!draft_persistent_enabled() || n < 2 || d.wdtype != DE_BF16) return kPDNotApplicable;
+  if (ws == nullptr || ws_bytes < layout(d, 1).total) return kPDNotApplicable;
+  if (n > kPDMaxLayers && normed_out == nullptr) return kPDNotApplicable;
+  // Every layer with a draft block, or none (then the term is dropped).
+  const bool has_draft = d.draft_inter > 0 && layers[0].draft != nullptr;
+  for (int l = 0; l < n; ++l)
+    if ((d.draft_inter > 0 && (layers[l].draft != nullptr) != has_draft) ||
+        (d.shared_inter > 0 && !layers[l].shared))
+      return kPDNotApplicable;
+  // The shared down projection in the chunks the separate launches use.
+  const int max_chunks = kMaxSharedChunks - (has_draft ? 1 : 0);
+  const int chunks =
+      d.shared_inter > 0 ? shared_chunks(d.shared_inter, 1, max_chunks, elem_align(d.wdtype), d.inter)
+                         : 0;
+  const PDShape sh{d.hidden, d.n_experts, d.top_k, d.inter, d.shared_inter,
+                   has_draft ? d.draft_inter : 0, chunks, chunks > 0 ? d.shared_inter / chunks : 0};
+  const int grid = dev_info().num_cus;
+  if (!draft_persistent_fits(sh, grid, nullptr, nullptr)) return kPDNotApplicable;
+  const Layout L = layout(d, 1);
+  PDArgs a{};
+  a.H = d.hidden;
+  a.N = d.n_experts;
+  a.k = d.top_k;
+  a.I = d.inter;
+  a.Is = d.shared_inter;
+  a.Id = sh.Id;
+  a.n_chunks = sh.n_chunks;
+  a.chunk = sh.chunk;
+  a.has_draft = has_draft ? 1 : 0;
+  a.score_func = d.score_func;
+  a.norm_topk = d.norm_topk;
+  a.routed_scale = d.routed_scale;
+  a.eps = eps;
+  a.grid = grid;
+  a.spin_limit = 1u << 20;
+  a.lds_bytes = draft_persistent_lds(sh);
+  a.a_buf = at<float>(ws, L.pd);
+  a.d_buf = a.a_buf + (sh.Is + sh.Id + sh.I);
+  a.z_buf = a.d_buf + d.hidden;
+  a.z_plain = at<float>(ws, L.z);
+  a.grid_flags = at<uint64_t>(ws, kPDFlagsOff);
+  a.sel_flags = a.grid_flags + kPDMaxGrid;
+  a.status = at<int32_t>(ws, kStatusOff);
+  for (int l0 = 0; l0 < n; l0 += kPDMaxLayers) {
+    const int cnt = n - l0 < kPDMaxLayers ? n - l0 : kPDMaxLayers;
+    a.L = cnt;
+    for (int i = 0; i < cnt; ++i) a.layers[i] = layers[l0 + i];
+    // Later launches continue from the previous one's output (read by every
+    // block before any block writes the output rows).
+    a.x_in = l0 == 0 ? x_in : normed_out;
+    a.h_in = l0 == 0 ? h_in : y_out;
+    a.z_in = (l0 == 0 && z_ready) ? a.z_plain : nullptr;
+    a.y_out = y_out;
+    a.normed_out = normed_out;
+    a.pred_idx = pred_idx ? pred_idx + (size_t)l0 * d.top_k : nullptr;
+    a.pred_gate = pred_gate ? pred_gate + (size_t)l0 * d.top_k : nullptr;
+    // Every launch gets its own epoch (see PDArgs); 0 never occurs, so a
+    // zeroed flag is always behind.
+    static std::atomic<uint32_t> epoch{1};
+    a.epoch = epoch.fetch_add(1);
+    if (a.epoch == 0) a.epoch = epoch.fetch_add(1);
+    const hipError_t e = launch_draft_persistent(a, s);
+    if (e != hipSuccess) {
+      // A launch that never started (the device cannot hold the grid, for
+      // instance) leaves the work to the separate launches.
+      if (l0 == 0 && (e == hipErrorCooperativeLaunchTooLarge || e == hipErrorNotSupported))
+        return kPDNotApplicable;
+      return DE_ERR_HIP;
+    }
+  }
+  return DE_OK;
+}
+
+PDLayer pd_layer(const de_layer_weights& w) {
+  PDLayer p{};
+  p.w_router = w.w_router;
+  p.bias = w.bias;
+  p.routed = static_cast<const char*>(w.routed.base);
+  p.stride = w.routed.slot_stride_bytes;
+  p.slot_of_expert = w.routed.slot_of_expert;
+  p.n_slots = w.routed.n_slots;
+  p.shared = static_cast<const char*>(w.shared_w);
+  p.draft = static_cast<const char*>(w.draft_w);
+  p.gamma = w.gamma;
+  return p;
+}
 
 // Reads the status word after the stream's work so far, clears it, and maps
 // its bits to a return code (a missing expert first).

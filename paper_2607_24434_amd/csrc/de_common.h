@@ -127,6 +127,7 @@ struct RoutedSrc {
 // Bits of the device status word of a workspace.
 constexpr int32_t kStatusNotResident = 1;
 constexpr int32_t kStatusBadToken = 2;
+constexpr int32_t kStatusSyncTimeout = 4;  // a bounded device-wide wait ran out
 
 struct TopkUnionArgs {
   int T, N, k;

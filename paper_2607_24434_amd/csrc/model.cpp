@@ -5,6 +5,7 @@
 // of the layer calls, enqueued on the caller's stream; the tokens never leave
 // device memory, so a whole step runs without a host synchronisation.
 #include "../../include/draftexpert.h"
+#include "draft_persistent.h"
 
 #include <algorithm>
 #include <cmath>
@@ -42,6 +43,11 @@ int dense_swiglu_chain(int T, int H, int I, int wdtype, const float* x, const vo
 bool combine_route_fits(int H);
 int32_t* layer_status_word(void* ws);
 int take_status(int32_t* word, hipStream_t stream);
+PDLayer pd_layer(const de_layer_weights& w);
+int draft_persistent_run(const de_moe_desc& d, int n, const PDLayer* layers, const float* x_in,
+                         const float* h_in, bool z_ready, float* y_out, float* normed_out,
+                         int32_t* pred_idx, float* pred_gate, float eps, void* ws,
+                         size_t ws_bytes, hipStream_t s);
 }
 
 namespace {
@@ -82,7 +88,7 @@ ModelLayout model_layout(const de_model& m, int T) {
   const size_t H = (size_t)m.moe.hidden;
   L.accept_bytes = de_accept_workspace_bytes(kMaxBlock - 1, m.vocab);
   // At least the control area: its status word also serves the embedding.
-  L.layer_bytes = std::max<size_t>(de_workspace_bytes(&m.moe, T), 512);
+  L.layer_bytes = std::max<size_t>(de_workspace_bytes(&m.moe, T), 4096);
   L.dense_bytes = m.dense_inter > 0 ? de_dense_workspace_bytes(T, (int)H, m.dense_inter) : 0;
   L.accept_ws = take(L.accept_bytes);
   L.layer_ws = take(L.layer_bytes);
@@ -240,7 +246,24 @@ int forward(const de_model& m, int T, const int32_t* tokens, int mode, float* lo
     std::swap(ncur, nnext);
     std::swap(h, hnext);
   }
-  for (int l = 0; l < m.n_layers; ++l) {
+  // A draft position through resident layers: every MoE layer in one
+  // persistent launch when the shapes allow it.
+  bool done = false;
+  if (mode == DE_DRAFT && chain && T == 1 && draft_r(m) == 1 && m.n_layers > 0 &&
+      (pred_idx == nullptr || pred_stride == (size_t)m.moe.top_k)) {
+    std::vector<de::PDLayer> pl(m.n_layers);
+    for (int l = 0; l < m.n_layers; ++l) pl[l] = de::pd_layer(m.layers[l]);
+    rc = de::draft_persistent_run(m.moe, m.n_layers, pl.data(), ncur, h, dense_chained, hnext,
+                                  nnext, pred_idx, nullptr, m.eps, lws, L.layer_bytes, s);
+    if (rc == DE_OK) {
+      std::swap(ncur, nnext);
+      std::swap(h, hnext);
+      done = true;
+    } else if (rc != de::kPDNotApplicable) {
+      return rc;
+    }
+  }
+  for (int l = 0; l < m.n_layers && !done; ++l) {
     const de_layer_weights& w = m.layers[l];
     const de_epilogue epi{h, nnext, m.eps};
     const bool ready = chain && (l > 0 || dense_chained);

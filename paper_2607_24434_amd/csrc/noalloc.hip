@@ -23,7 +23,7 @@ namespace {
 // call's shape and block length): the V2-Lite layer up to T = 64 needs about
 // 8.5 MB.
 constexpr size_t kScratchBytes = 16u << 20;
-constexpr size_t kCtlBytes = 1024;  // the layer scratch's control area (counters, status)
+constexpr size_t kCtlBytes = 4096;  // the layer scratch's control area (counters, status, flags)
 
 static __device__ __align__(256) unsigned char scratch[kScratchBytes];
 
