@@ -204,3 +204,54 @@ def test_chained_forward_equals_layer_calls(T, mode):
     torch.cuda.synchronize()
     assert de.de_layer_status(ws) == 0
     assert torch.equal(chained, calls)
+
+
+def test_full_stack_step_matches_oracle(full_model):
+    """The full-size step (dense layer 0 with I = 10944, 26 V2-Lite MoE layers,
+    K = 8, 102400-vocab head) against the fp64 oracle's step from the same
+    start token, stored by tests/golden/make_cfg4_step.py (the oracle alone;
+    about 3 minutes per candidate start token on the CPU).  Drafts, target
+    argmax, n, bonus, every layer's verify union size and the drafter's top-k
+    in every layer at every draft position are exact; sampled logits (each
+    row's 8 largest entries and 24 seeded columns) of the verify pass and of
+    the first draft position are within 1e-4 of the sample's largest
+    magnitude."""
+    import json
+    import os
+    import paper_2607_24434_amd as de
+    g = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "cfg4_step.json")))
+    model, dm = full_model
+    K, L, k = model.k_draft, model.n_moe_layers, model.moe.top_k
+    assert g["k_draft"] == K and g["model"] == model.name
+    block = dm.new_block(K, g["start"])
+    amax = torch.empty(K + 1, dtype=torch.int32, device="cuda")
+    out = torch.empty(2, dtype=torch.int32, device="cuda")
+    nu = torch.empty(L, dtype=torch.int32, device="cuda")
+    pred = torch.empty(K, L, k, dtype=torch.int32, device="cuda")
+    dm.spec_step(block, amax, out, nu, pred)
+    torch.cuda.synchronize()
+    print(f"start {g['start']}: drafts {block[1:].cpu().tolist()} n,bonus {out.cpu().tolist()}",
+          flush=True)
+    assert block[1:].cpu().tolist() == g["drafts"]
+    assert amax.cpu().tolist() == g["target_argmax"]
+    assert out.cpu().tolist() == [g["n"], g["bonus"]]
+    assert nu.cpu().tolist() == g["n_union"]
+    np.testing.assert_array_equal(pred.cpu().numpy(), np.asarray(g["pred_idx"]))
+
+    def check(logits, sample, what):
+        lg = logits.cpu().numpy()
+        worst = 0.0
+        for j, row in enumerate(sample):
+            got = lg[j, row["cols"]]
+            want = np.asarray(row["vals"])
+            worst = max(worst, float(np.max(np.abs(got - want)) / np.max(np.abs(want))))
+        print(f"{what}: sampled logits rel err {worst:.2e}", flush=True)
+        assert worst < 1e-4
+
+    lv = torch.empty(K + 1, model.vocab, dtype=torch.float32, device="cuda")
+    dm.forward(block, de.DE_TARGET, lv)
+    ld = torch.empty(1, model.vocab, dtype=torch.float32, device="cuda")
+    dm.forward(block[:1], de.DE_DRAFT, ld)
+    torch.cuda.synchronize()
+    check(lv, g["verify_logits"], "verify")
+    check(ld, g["draft0_logits"], "draft position 0")
