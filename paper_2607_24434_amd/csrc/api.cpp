@@ -358,6 +358,14 @@ namespace de {
 
 int32_t* layer_status_word(void* ws) { return at<int32_t>(ws, kStatusOff); }
 
+// The LM head of a block of positions runs on the matrix cores unless
+// DE_LMHEAD_MFMA is "0" (the vector-ALU row-dot then runs; the two differ only
+// in the fp32 summation order).
+bool lmhead_mfma_enabled() {
+  const char* e = std::getenv("DE_LMHEAD_MFMA");
+  return e == nullptr || e[0] != '0';
+}
+
 // The persistent draft pass is used unless DE_DRAFT_PERSISTENT is "0" (the
 // separate launches then run every draft layer; both give the same bits).
 bool draft_persistent_enabled() {
@@ -820,6 +828,10 @@ int de_lm_head(int T, int H, int V, const float* x, const void* w_lm, float* log
                hipStream_t stream) {
   if (check_T(T) != DE_OK || H < 8 || H % 8 || V < 1 || !x || !w_lm || !logits) return DE_ERR_INVALID;
   if (!aligned16(x) || !aligned16(w_lm)) return DE_ERR_INVALID;
+  // A block of positions on the matrix cores (the vector-ALU row-dot is
+  // arithmetic-bound there); one position streams at the HBM rate already.
+  if (de::rowdot_mfma_fits(T, H) && de::lmhead_mfma_enabled())
+    return hip_status(de::launch_rowdot_mfma(T, H, V, x, w_lm, logits, stream));
   de::GroupedArgs g{};
   g.T = T;
   g.H = H;

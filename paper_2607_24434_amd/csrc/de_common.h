@@ -211,6 +211,11 @@ hipError_t launch_combine_route(const CombineArgs& a, const RouteArgs& r, hipStr
 hipError_t launch_union(const TopkUnionArgs& a, hipStream_t s);
 
 hipError_t launch_gateup(const GroupedArgs& a, int wdtype, hipStream_t s);
+// The LM head row-dot on the matrix cores (bf16 weights [V, H], fp32 x [T, H],
+// out [T, V]) for the shapes rowdot_mfma_fits accepts.
+bool rowdot_mfma_fits(int T, int H);
+hipError_t launch_rowdot_mfma(int T, int H, int V, const float* x, const void* w, float* out,
+                              hipStream_t s);
 // Raises a kernel's dynamic LDS limit to `lds` bytes when above the default.
 hipError_t allow_lds(const void* fn, size_t lds);
 hipError_t launch_down(const GroupedArgs& a, int wdtype, hipStream_t s);
