@@ -85,6 +85,8 @@ def parse():
                    help="skip the Q4_0-weight layer measurement")
     p.add_argument("--no-draft-side", action="store_true",
                    help="skip the drafter comparison (top-r against DraftExpert) on the offload stack")
+    p.add_argument("--no-cfg3", action="store_true",
+                   help="skip the Moonlight-shaped block-length sweep (T = 1, 5, 9, 17)")
     return p.parse_args()
 
 
@@ -221,11 +223,12 @@ def main():
                 + (T * cfg.top_k * cfg.inter + T * cfg.shared_inter) * 4 + (T * cfg.top_k + T) * H * 4)
     dn_gbs = float(dn_bytes.sum() / (sum(dn_ms) * 1e-3) / 1e9)
 
+    del copies
+    torch.cuda.empty_cache()
     q4 = None
     if not args.no_q4:
-        del copies
-        torch.cuda.empty_cache()
         q4 = q4_layer(args, de, configs, gen, wgpu, torch, np, 1e3 * statistics.median(ver_ms))
+    sweep = None if args.no_cfg3 else cfg3_sweep(args, de, configs, gen, wgpu, torch, np)
     full = None if args.no_full_step else full_step(args, de, configs, gen, wgpu, torch, np)
     offload = None if args.no_offload else offload_step(args, de, configs, gen, wgpu, torch, np)
 
@@ -249,8 +252,10 @@ def main():
         del buf
 
     cpu = None
+    cpu_extra = None
     if not args.no_cpu:
         cpu = cpu_baseline(cfg, gen.x_rows(cfg, T, block=0), args.cpu_seconds)
+        cpu_extra = cpu_baseline_extras(configs, gen, args.cpu_seconds / 3)
 
     med = statistics.median
     out = {
@@ -275,6 +280,7 @@ def main():
             "shared_inter": cfg.shared_inter, "draft_inter": cfg.draft_inter, "k_draft": K,
             "verify_block": T, "vocab": V, "weights": "bf16",
         },
+        "union_hbm_frac": round(value / PEAK_HBM_GBS, 4),
         "verify_layer_us": round(1e3 * med(ver_ms), 2),
         "verify_layer_us_p10_p90": [round(1e3 * float(np.percentile(ver_ms, 10)), 2),
                                     round(1e3 * float(np.percentile(ver_ms, 90)), 2)],
@@ -298,9 +304,11 @@ def main():
             "algorithmic_bytes_per_launch": int(round(float(gu_bytes.mean()))),
         },
         "q4_layer": q4,
+        "cfg3_sweep": sweep,
         "full_step": full,
         "offload_step": offload,
         "cpu_baseline": cpu,
+        "cpu_baseline_extra": cpu_extra,
     }
     print(json.dumps(out), flush=True)
 
@@ -723,6 +731,218 @@ def draft_side(args, de, model, dm, layers, t, cache, gen, torch, np):
     for r in rows.values():
         r["draft_cost_vs_top1"] = round(r["draft_ms_per_token"] / top1, 3) if top1 > 0 else None
     return rows
+
+
+def cfg3_sweep(args, de, configs, gen, wgpu, torch, np):
+    """Union growth and verify bandwidth against block length (§2.3, Eq. 3) on
+    the Moonlight-shaped layer (sigmoid router with a selection bias, top-6
+    renormalised gates, bf16 experts): for T = 1 (one-token decoding) and each
+    block length K + 1 in {5, 9, 17}, the verify layer over blocks of fresh
+    activations on rotated weight copies (union mean, µs, GB/s over the
+    union's expert bytes, fraction of the 8 TB/s peak, cost relative to T = 1),
+    and the V2-Lite stack's dense layer 0 (I = 10944, bf16) at the same T,
+    whose weights are read once whatever the block length."""
+    cfg = configs.CFG3
+    dev = "cuda"
+    H, R = cfg.hidden, args.copies
+    desc = de.make_desc(H, cfg.n_experts, cfg.top_k, cfg.inter, cfg.shared_inter,
+                        cfg.draft_inter, cfg.score_func, cfg.norm_topk, cfg.routed_scale,
+                        cfg.wdtype)
+    eb = cfg.expert_bytes()
+    copies = []
+    for c in range(R):
+        routed = wgpu.routed_experts(cfg, 0, dev, redraw=c)
+        copies.append(dict(routed=routed, table=de.make_table(routed, eb, None, cfg.n_experts),
+                           shared=wgpu.shared_block(cfg, 0, dev, redraw=c),
+                           router=wgpu.router(cfg, 0, dev, redraw=c),
+                           bias=wgpu.to_device(gen.router_bias(cfg, 0, redraw=c), dev)))
+    n_blocks = 8
+    steps, warm = args.steps, args.warmup
+
+    def timed(T, call):
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(steps)]
+        for i in range(warm + steps):
+            if i >= warm:
+                evs[i - warm][0].record()
+            call(i)
+            if i >= warm:
+                evs[i - warm][1].record()
+        torch.cuda.synchronize()
+        return [a.elapsed_time(b) for a, b in evs]
+
+    moe_rows = []
+    for T in (1,) + tuple(configs.CFG3_T):
+        xs = [wgpu.to_device(gen.x_rows(cfg, T, block=100 + b), dev) for b in range(n_blocks)]
+        ws = de.workspace(desc, T, dev)
+        y = torch.empty(T, H, dtype=torch.float32, device=dev)
+        nrm = torch.empty(T, H, dtype=torch.float32, device=dev)
+        nu = torch.zeros(warm + steps, dtype=torch.int32, device=dev)
+
+        def call(i):
+            cp, x = copies[i % R], xs[i % n_blocks]
+            de.de_verify_layer(desc, T, x, cp["router"], cp["bias"], cp["table"], cp["shared"], y,
+                               n_union=nu[i:i + 1], ws=ws,
+                               epi=de.make_epilogue(residual=x, normed=nrm))
+
+        ms = timed(T, call)
+        n = nu[warm:].cpu().numpy().astype(np.int64)
+        gbs = float(n.sum() * eb / (sum(ms) * 1e-3) / 1e9)
+        moe_rows.append({"T": T, "union_mean": round(float(n.mean()), 2),
+                         "union_min_max": [int(n.min()), int(n.max())],
+                         "verify_us": round(1e3 * statistics.median(ms), 2),
+                         "union_gbs": round(gbs, 1), "frac_of_peak": round(gbs / PEAK_HBM_GBS, 4)})
+        del ws, xs
+    del copies
+    torch.cuda.empty_cache()
+    base = moe_rows[0]["verify_us"]
+    for r in moe_rows:
+        r["cost_vs_T1"] = round(r["verify_us"] / base, 3)
+
+    model = configs.CFG4
+    I = model.dense_inter
+    dense = [wgpu.dense_block(model, dev, redraw=c) for c in range(R)]
+    wbytes = 3 * I * H * 2
+    dense_rows = []
+    for T in (1,) + tuple(configs.CFG3_T):
+        x = wgpu.to_device(gen.x_rows(cfg, T, block=200), dev)
+        y = torch.empty(T, H, dtype=torch.float32, device=dev)
+        ws = torch.empty(de.de_dense_workspace_bytes(T, H, I), dtype=torch.uint8, device=dev)
+        ms = timed(T, lambda i: de.de_dense_swiglu(T, H, I, de.DE_BF16, x, dense[i % R], y, ws))
+        us = 1e3 * statistics.median(ms)
+        gbs = wbytes / (us * 1e-6) / 1e9
+        dense_rows.append({"T": T, "us": round(us, 2), "gbs": round(gbs, 1),
+                           "frac_of_peak": round(gbs / PEAK_HBM_GBS, 4)})
+    del dense
+    torch.cuda.empty_cache()
+    for r in dense_rows:
+        r["cost_vs_T1"] = round(r["us"] / dense_rows[0]["us"], 3)
+    return {
+        "workload": "moonlight-moe-layer: H=2048, 64 routed + 2 shared SwiGLU experts (I=1408), "
+                    "sigmoid router with a N(0, 0.1) selection bias, top-6 renormalised gates, "
+                    "bf16 experts; 8 blocks of fresh activations per T, 8 rotated weight copies; "
+                    "dense: V2-Lite layer 0 (I=10944, bf16, 134.5 MB)",
+        "moe_verify": moe_rows,
+        "dense_layer": dense_rows,
+    }
+
+
+def _time_runs(run, budget_s, max_runs=20):
+    """Median seconds of run() over repeated calls within budget_s (at least one)."""
+    times = []
+    t_end = time.perf_counter() + budget_s
+    while True:
+        t0 = time.perf_counter()
+        run()
+        times.append(time.perf_counter() - t0)
+        if time.perf_counter() > t_end or len(times) >= max_runs:
+            break
+    return statistics.median(times), len(times)
+
+
+def cpu_baseline_extras(configs, gen, budget_s):
+    """The oracle on the host cores for the other legs, each on a bounded
+    sample: the V2-Lite draft layer (one position, Eq. 5), the Moonlight-shaped
+    verify layer at T = 17 (Eq. 4), and one V2-Lite K = 8 decode step composed
+    from timed oracle parts (Algorithm 1: per draft position the dense layer,
+    26 draft layers and the LM head at T = 1; then the dense layer, 26 verify
+    layers and the LM head at T = 9)."""
+    import numpy as np
+
+    from oracle import moe
+
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:  # noqa: BLE001
+        cores = len(os.sched_getaffinity(0))
+
+    def layer_parts(cfg, x, with_draft):
+        w_router = gen.router_weight(cfg, 0).astype(np.float64)
+        bias = gen.router_bias(cfg, 0)
+        idx, _, _ = moe.route_topk(x, w_router, bias, cfg.top_k, cfg.score_func, cfg.norm_topk)
+        members = sorted(set(int(e) for e in np.asarray(idx).ravel()))
+        raw = {e: gen.routed_block(cfg, 0, e) for e in members}
+        shared_raw = gen.shared_block(cfg, 0)
+        draft_raw = gen.draft_block(cfg, 0) if with_draft else None
+        return w_router, bias, members, raw, shared_raw, draft_raw
+
+    def verify_run(cfg, x):
+        w_router, bias, members, raw, shared_raw, _ = layer_parts(cfg, x, False)
+
+        def run():
+            shared = moe.split_shared(shared_raw, cfg.n_shared, cfg.shared_each, cfg.hidden)
+            routed = {}
+
+            def get(e):
+                if e not in routed:
+                    routed[e] = moe.split_expert(raw[e], cfg.inter, cfg.hidden)
+                return routed[e]
+            moe.moe_target(x, w_router, bias, get, shared, cfg.top_k, cfg.score_func,
+                           cfg.norm_topk)
+        return run, len(members)
+
+    def draft_run(cfg, x):
+        w_router, bias, _, raw, shared_raw, draft_raw = layer_parts(cfg, x, True)
+
+        def run():
+            shared = moe.split_shared(shared_raw, cfg.n_shared, cfg.shared_each, cfg.hidden)
+            draft = moe.split_expert(draft_raw, cfg.draft_inter, cfg.hidden)
+            moe.moe_draft(x, w_router, bias, lambda e: moe.split_expert(raw[e], cfg.inter, cfg.hidden),
+                          shared, draft, cfg.gamma, cfg.top_k, cfg.score_func, cfg.norm_topk)
+        return run
+
+    out = {}
+    cfg2 = configs.CFG2
+    x1 = gen.x_rows(cfg2, 1, block=1).astype(np.float64)
+    t_draft, n = _time_runs(draft_run(cfg2, x1), budget_s / 3)
+    out["cfg2_draft_layer"] = {
+        "value": round(t_draft * 1e3, 2), "unit": "ms per draft layer", "cores": int(cores),
+        "kind": "oracle",
+        "sample": f"fp64 oracle draft layer (shared + top-1 + draft expert, one position) on the "
+                  f"V2-Lite shape, bf16 weights in host memory, median of {n} runs"}
+    cfg3 = configs.CFG3
+    x17 = gen.x_rows(cfg3, 17, block=100).astype(np.float64)
+    run17, nu17 = verify_run(cfg3, x17)
+    t17, n = _time_runs(run17, budget_s / 3)
+    out["cfg3_verify_T17"] = {
+        "value": round(nu17 * cfg3.expert_bytes() / t17 / 1e9, 4), "unit": "GB/s", "cores": int(cores),
+        "kind": "oracle",
+        "sample": f"fp64 oracle verify layer (T=17, |U|={nu17}) on the Moonlight shape, "
+                  f"median {t17 * 1e3:.1f} ms over {n} runs"}
+    # The V2-Lite step from its parts.
+    model = configs.CFG4
+    m = model.moe
+    x9 = gen.x_rows(m, 9, block=0).astype(np.float64)
+    run9, _ = verify_run(m, x9)
+    t9, _ = _time_runs(run9, budget_s / 6, max_runs=3)
+    t1, _ = _time_runs(draft_run(m, gen.x_rows(m, 1, block=1).astype(np.float64)), budget_s / 12,
+                       max_runs=5)
+    dense_raw = gen.dense_block(model)
+    lm = moe.to_f64(gen.lm_head(model.cfg_id, model.vocab, m.hidden, model.lm_std))
+
+    def dense_run(x):
+        def run():
+            g, u, d = moe.split_expert(dense_raw, model.dense_inter, m.hidden)
+            moe.swiglu(x, g, u, d)
+        return run
+
+    dense_run(x9[:1])()  # first touch of the dense weights
+    td1, _ = _time_runs(dense_run(x9[:1]), budget_s / 12, max_runs=3)
+    td9, _ = _time_runs(dense_run(x9), budget_s / 12, max_runs=3)
+    th1, _ = _time_runs(lambda: x9[:1] @ lm.T, budget_s / 12, max_runs=5)
+    th9, _ = _time_runs(lambda: x9 @ lm.T, budget_s / 12, max_runs=5)
+    L, K = model.n_moe_layers, model.k_draft
+    step = K * (td1 + L * t1 + th1) + td9 + L * t9 + th9
+    out["cfg4_step"] = {
+        "value": round(1.0 / step, 5), "unit": "tokens/s at one token per step", "cores": int(cores),
+        "kind": "oracle",
+        "step_s": round(step, 2),
+        "sample": f"composed from timed fp64 oracle parts: draft layer {t1 * 1e3:.1f} ms, verify "
+                  f"layer (T=9) {t9 * 1e3:.1f} ms, dense layer {td1 * 1e3:.1f} / {td9 * 1e3:.1f} ms "
+                  f"and LM head {th1 * 1e3:.1f} / {th9 * 1e3:.1f} ms at T=1 / 9; step = "
+                  f"{K} x (dense + {L} draft layers + head) + dense + {L} verify layers + head"}
+    return out
 
 
 def cpu_baseline(cfg, x, budget_s):
