@@ -459,10 +459,10 @@ def full_step(args, de, configs, gen, wgpu, torch, np):
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
     ev[0].record()
     for i in range(reps):
-        dm.forward(blocks[W + i, :1], de.DE_DRAFT, lg[:1], am[:1])
+        dm.forward(blocks[W + i % S, :1], de.DE_DRAFT, lg[:1], am[:1])
     ev[1].record()
     for i in range(reps):
-        dm.forward(blocks[W + i], de.DE_TARGET, lg, am)
+        dm.forward(blocks[W + i % S], de.DE_TARGET, lg, am)
     ev[2].record()
     torch.cuda.synchronize()
     draft_ms = ev[0].elapsed_time(ev[1]) / reps

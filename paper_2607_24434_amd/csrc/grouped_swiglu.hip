@@ -958,8 +958,11 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
   const Tables tb = tables_at(a, a.lds_floats);
   __shared__ int s_absent;
   if (threadIdx.x == 0) s_absent = 0;
-  __syncthreads();
+  // The dense descriptors are copied before the first barrier: copied after
+  // it, the compiler keeps the whole argument in per-lane scratch memory, and
+  // a launch that uses scratch costs several µs more.
   fill_dense(a, tb);
+  __syncthreads();  // s_absent is initialised
   if (a.has_routed) fill_tables(a, tb, nu, &s_absent);
   __syncthreads();
   if (s_absent && !a.r.absent_ok) {
