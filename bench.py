@@ -46,7 +46,7 @@ PMC_TRAFFIC = {
     "sources": ["paper_2607_24434_amd/csrc/grouped_swiglu.hip",
                 "paper_2607_24434_amd/csrc/topk_union.h",
                 "paper_2607_24434_amd/csrc/de_common.h"],
-    "sha256": "568db70214a5b68cc041ccdef9a97080abaa2ef520f23030270f05b255933f7a",
+    "sha256": "0b7157a76126b7d76e98d5ae50f9ff6f85f2fb40dbe0c2244e7fcdfed6294c02",
 }
 
 
