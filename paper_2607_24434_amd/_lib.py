@@ -17,7 +17,11 @@ import os
 import torch  # noqa: F401
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "libdraftexpert.so")
+# DE_LIBRARY may name another build of the same ABI, e.g. the host-only
+# sanitizer build of the expert cache, which exports a subset of the entry
+# points (only those are bound then).
+DEFAULT_LIB_PATH = os.path.join(HERE, "libdraftexpert.so")
+LIB_PATH = os.environ.get("DE_LIBRARY") or DEFAULT_LIB_PATH
 
 DE_SOFTMAX = 0
 DE_SIGMOID = 1
@@ -199,7 +203,7 @@ def _load(path: str = LIB_PATH, strict: bool = True):
     return lib
 
 
-LIB = _load()
+LIB = _load(LIB_PATH, strict=LIB_PATH == DEFAULT_LIB_PATH)
 
 
 def _ptr(t):

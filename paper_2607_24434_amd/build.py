@@ -19,7 +19,7 @@ LIB = os.path.join(HERE, "libdraftexpert.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
-SOURCES = ["api.cpp", "model.cpp", "cache.cpp", "router_topk.hip", "grouped_swiglu.hip", "glue.hip",
+SOURCES = ["api.cpp", "errors.cpp", "model.cpp", "cache.cpp", "router_topk.hip", "grouped_swiglu.hip", "glue.hip",
            "truncation.hip", "distill.hip", "noalloc.hip", "draft_persistent.hip", "rowdot_mfma.hip"]
 
 # Packed fp32 instructions are disabled for every device compile; the host

@@ -26,7 +26,7 @@ def declared_functions():
 def test_library_exports_every_declared_symbol():
     names = declared_functions()
     assert len(names) >= 14
-    lib = ctypes.CDLL(de.LIB_PATH)
+    lib = ctypes.CDLL(de._lib.DEFAULT_LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
     assert set(names) == set(de.C_FUNCS)
