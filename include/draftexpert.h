@@ -588,6 +588,7 @@ int de_stream_probe(const void* buf, size_t bytes, float* sink, hipStream_t stre
 /* Kernel phases that can be bracketed by caller-owned HIP events. */
 #define DE_PHASE_GATEUP 0 /* the grouped gate/up kernel (Eq. 4 first half) */
 #define DE_PHASE_DOWN 1   /* the grouped down-projection kernel */
+#define DE_PHASE_LAYER 2  /* the verify layer's single launch (de_verify_single_launch) */
 
 /* Arms a one-shot timer: the next layer call (de_grouped_swiglu,
  * de_draft_layer, de_verify_layer, de_dense_swiglu) made on this host thread
@@ -595,6 +596,17 @@ int de_stream_probe(const void* buf, size_t bytes, float* sink, hipStream_t stre
  * and `stop` right after it, then disarms.  Either event may be NULL.  The
  * events are created and read by the caller (e.g. hipEventElapsedTime). */
 int de_time_next_phase(int phase, hipEvent_t start, hipEvent_t stop);
+
+/* 1 when de_verify_layer (and the verify passes of the model calls without a
+ * chained router) runs the layer of this shape as one launch, else 0.  That launch covers Eq. 4 over the block's union (top-k selection
+ * from the router logits, union, grouped gate/up and down, shared path and
+ * the combine with its epilogue) and gives the same bits as the separate
+ * launches; every armed phase timer then brackets it.  It serves bf16
+ * weights and blocks of 2 or more positions whose staged rows fit a CU's LDS
+ * (the V2-Lite layer at T = 2..9).  It is off unless the environment
+ * variable DE_VERIFY_FUSED is "1": on MI355X it measures slower than the
+ * separate launches (235 against 158 us at T = 9). */
+int de_verify_single_launch(const de_moe_desc* d, int T);
 
 #ifdef __cplusplus
 }

@@ -49,9 +49,11 @@ C_FUNCS = [
     "de_confidence", "de_expansion", "de_spec_step_trunc", "de_draft_layer_topr",
     "de_residual_target", "de_layer_router_logits", "de_row_kl", "de_distill_signals",
     "de_layer_status", "de_model_status", "de_noalloc_scratch_bytes", "de_verify_layer_noalloc",
+    "de_verify_single_launch",
 ]
 DE_PHASE_GATEUP = 0
 DE_PHASE_DOWN = 1
+DE_PHASE_LAYER = 2
 DE_TARGET = 0
 DE_DRAFT = 1
 DE_NEED_DRAFT = 0
@@ -173,6 +175,7 @@ def _load(path: str = LIB_PATH, strict: bool = True):
         "de_dense_swiglu": (I, [I, I, I, I, P, P, P, EP, P, SZ, P]),
         "de_stream_probe": (I, [P, SZ, P, P]),
         "de_time_next_phase": (I, [I, P, P]),
+        "de_verify_single_launch": (I, [DP, I]),
         "de_check_model": (I, [MP]),
         "de_model_workspace_bytes": (SZ, [MP, I]),
         "de_model_forward": (I, [MP, I, P, I, P, P, P, P, SZ, P]),
@@ -399,6 +402,11 @@ def de_time_next_phase(phase, start_event, stop_event):
     _check("de_time_next_phase", LIB.de_time_next_phase(
         int(phase), None if start_event is None else start_event.cuda_event,
         None if stop_event is None else stop_event.cuda_event))
+
+
+def de_verify_single_launch(desc, T):
+    """True when the verify layer of this shape runs as one cooperative launch."""
+    return bool(LIB.de_verify_single_launch(ctypes.byref(desc), int(T)))
 
 
 def make_model(desc, layers, vocab, emb, lm_head, dense_w=None, dense_inter=0,

@@ -20,7 +20,8 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
 SOURCES = ["api.cpp", "errors.cpp", "model.cpp", "cache.cpp", "router_topk.hip", "grouped_swiglu.hip", "glue.hip",
-           "truncation.hip", "distill.hip", "noalloc.hip", "draft_persistent.hip", "rowdot_mfma.hip"]
+           "truncation.hip", "distill.hip", "noalloc.hip", "draft_persistent.hip", "rowdot_mfma.hip",
+           "verify_fused.hip"]
 
 # Packed fp32 instructions are disabled for every device compile; the host
 # pass warns that it does not know the feature, which is harmless.

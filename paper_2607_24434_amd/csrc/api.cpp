@@ -3,6 +3,7 @@
 #include "../../include/draftexpert.h"
 #include "de_common.h"
 #include "draft_persistent.h"
+#include "verify_fused.h"
 
 #include <atomic>
 #include <cmath>
@@ -106,6 +107,12 @@ int shared_chunks(int inter, int T, int max_chunks, int align, int width) {
   return best;
 }
 
+int verify_chunks(const de_moe_desc& d, int T) {
+  return d.shared_inter > 0 ? shared_chunks(d.shared_inter, T, kMaxSharedChunks, elem_align(d.wdtype),
+                                            d.inter)
+                            : 0;
+}
+
 constexpr size_t kCtlBytes = 4096;
 constexpr size_t kStatusOff = 256;
 // The persistent draft pass's arrival flags: at an offset that does not
@@ -119,8 +126,28 @@ struct Layout {
   size_t ctl, z, idx, gate, nu, uids, offs, tok, glist, ppos;
   size_t a_r, a_s, a_d, p_r, p_s, p_d;
   size_t pd;  // persistent draft pass: gate/up outputs [Is + Id + I], row sums [H], logits [N]
+  // The single-launch verify layer (only for the shapes it serves, else
+  // fused = false): (value, epoch) words of A_r, A_s, P_r and the shared
+  // down chunks' partials.
+  bool fused;
+  int chunks;     // shared down chunks of that launch
+  size_t lds;     // its LDS bytes per block
+  size_t t_ar, t_as, t_pr, t_ps, t_pub;
   size_t total;
 };
+
+// True when the verify layer of this shape can run as one launch; chunks and
+// lds receive the launch's shared down chunks and LDS bytes per block.
+bool fused_shape(const de_moe_desc& d, int T, int* chunks, size_t* lds) {
+  if (d.wdtype != DE_BF16 || T < 2 || T > kMaxT) return false;
+  const int c = verify_chunks(d, T);
+  const size_t b = de::verify_fused_lds(T, d.hidden, d.n_experts, d.top_k, d.inter,
+                                        d.shared_inter, c);
+  if (b == 0) return false;
+  if (chunks) *chunks = c;
+  if (lds) *lds = b;
+  return true;
+}
 
 Layout layout(const de_moe_desc& d, int T) {
   Layout L{};
@@ -152,6 +179,14 @@ Layout layout(const de_moe_desc& d, int T) {
   L.p_s = take((size_t)kMaxSharedChunks * T * d.hidden * 4);
   L.p_d = take((size_t)T * d.hidden * 4);
   L.pd = take(((size_t)d.shared_inter + d.draft_inter + d.inter + d.hidden + d.n_experts) * 4);
+  L.fused = fused_shape(d, T, &L.chunks, &L.lds);
+  if (L.fused) {
+    L.t_ar = take(tk * d.inter * 8);
+    L.t_as = take((size_t)T * d.shared_inter * 8);
+    L.t_pr = take(tk * d.hidden * 8);
+    L.t_ps = take((size_t)kMaxSharedChunks * T * d.hidden * 8);
+    L.t_pub = take(de::verify_fused_pub_words(T, d.n_experts, d.top_k) * 8);
+  }
   L.total = o;
   return L;
 }
@@ -190,8 +225,8 @@ hipError_t route(const de_moe_desc& d, int T, const float* x, const float* w_rou
 }
 
 // One-shot phase timers armed by de_time_next_phase (per host thread).
-thread_local hipEvent_t t_start[2] = {nullptr, nullptr};
-thread_local hipEvent_t t_stop[2] = {nullptr, nullptr};
+thread_local hipEvent_t t_start[3] = {nullptr, nullptr, nullptr};
+thread_local hipEvent_t t_stop[3] = {nullptr, nullptr, nullptr};
 
 // Launches one phase with its armed events (if any) around it.
 template <typename F>
@@ -202,6 +237,25 @@ hipError_t timed_phase(int phase, hipStream_t s, F launch) {
   const hipError_t e = launch();
   if (e != hipSuccess) return e;
   if (b != nullptr && hipEventRecord(b, s) != hipSuccess) return hipErrorInvalidValue;
+  return hipSuccess;
+}
+
+// The single-launch verify layer: every armed phase timer brackets it (the
+// gate/up and down phases both run inside it).
+template <typename F>
+hipError_t timed_layer(hipStream_t s, F launch) {
+  hipEvent_t a[3], b[3];
+  for (int i = 0; i < 3; ++i) {
+    a[i] = t_start[i];
+    b[i] = t_stop[i];
+    t_start[i] = t_stop[i] = nullptr;
+  }
+  for (int i = 0; i < 3; ++i)
+    if (a[i] != nullptr && hipEventRecord(a[i], s) != hipSuccess) return hipErrorInvalidValue;
+  const hipError_t e = launch();
+  if (e != hipSuccess) return e;
+  for (int i = 0; i < 3; ++i)
+    if (b[i] != nullptr && hipEventRecord(b[i], s) != hipSuccess) return hipErrorInvalidValue;
   return hipSuccess;
 }
 
@@ -237,6 +291,83 @@ de::RoutedSrc routed_src(const de_moe_desc& d, int T, int kk, const de_expert_ta
   return r;
 }
 
+// The verify layer as one launch (verify_fused.hip): the same outputs as the
+// gate/up, down and combine launches, bit for bit.
+int run_fused(const de_moe_desc& d, int T, const float* x, const de::RoutedSrc& r, int kk,
+              const void* shared_w, float* y, const de_epilogue* epi, const Layout& L, void* ws,
+              const de::TopkUnionArgs& sel, hipStream_t s) {
+  static std::atomic<uint32_t> epoch{1};
+  uint32_t ep = epoch.fetch_add(1);
+  if (ep == 0) ep = epoch.fetch_add(1);  // 0 never tags a word (a zeroed word is always stale)
+  de::FusedArgs f{};
+  de::GroupedArgs& g = f.gu;
+  g.T = T;
+  g.H = d.hidden;
+  g.x = x;
+  g.has_routed = 1;
+  g.r = r;
+  g.r.a = nullptr;  // A_r only as tagged words
+  g.r.a_tag = at<uint64_t>(ws, L.t_ar);
+  g.r.p_tag = at<uint64_t>(ws, L.t_pr);
+  g.fuse_route = 1;
+  g.fuse_select = 1;
+  g.sel = sel;
+  g.epoch = ep;
+  g.n_dense = 0;
+  if (shared_w != nullptr && d.shared_inter > 0) {
+    de::DenseSrc& ds = g.dense[g.n_dense++];
+    ds.w = shared_w;
+    ds.inter = d.shared_inter;
+    ds.out = nullptr;
+    ds.out_tag = at<uint64_t>(ws, L.t_as);
+  }
+  de::GroupedArgs& h = f.dn;
+  h = g;
+  h.fuse_route = 0;
+  h.fuse_select = 0;
+  h.n_dense = 0;
+  h.r.p = r.p;  // the plain P_r too (the residual target reads it)
+  // Every down input is read from LDS after it is staged; the plain buffers
+  // only keep a stray read in bounds.
+  h.r.a = r.a;
+  de::CombineArgs& c = f.c;
+  c.T = T;
+  c.H = d.hidden;
+  c.n_dense = 0;
+  if (shared_w != nullptr && d.shared_inter > 0) {
+    const int chunks = L.chunks;
+    const int cl = d.shared_inter / chunks;
+    const char* D = static_cast<const char*>(shared_w) +
+                    2 * de::mat_bytes(d.wdtype, d.shared_inter, d.hidden);
+    for (int i = 0; i < chunks; ++i) {
+      de::DenseSrc& ds = h.dense[h.n_dense++];
+      ds.w = D + (size_t)i * cl * 2;
+      ds.inter = cl;
+      ds.ld = d.shared_inter;
+      ds.rows = d.hidden;
+      ds.gate = 1.0f;
+      ds.vin = at<float>(ws, L.a_s) + (size_t)i * cl;
+      ds.vin_tag = at<uint64_t>(ws, L.t_as) + (size_t)i * cl;
+      ds.vin_stride = d.shared_inter;
+      ds.out = nullptr;
+      ds.out_tag = at<uint64_t>(ws, L.t_ps) + (size_t)i * T * d.hidden;
+      ds.out_stride = d.hidden;
+      ++c.n_dense;
+    }
+  }
+  c.kk = kk;
+  c.pairs_max = r.pairs_max;
+  c.y = y;
+  c.residual = epi ? epi->residual : nullptr;
+  c.normed = epi ? epi->normed : nullptr;
+  c.eps = epi ? epi->eps : 0.f;
+  f.region_floats = de::verify_fused_region(T, d.hidden, d.inter, d.shared_inter, L.chunks);
+  f.status = r.status;
+  f.pub = at<uint64_t>(ws, L.t_pub);
+  const hipError_t e = timed_layer(s, [&] { return de::launch_verify_fused(f, L.lds, s); });
+  return e == hipSuccess ? DE_OK : DE_ERR_HIP;
+}
+
 // gate/up + down + combine over the union (kk entries per position) and the
 // dense sources (shared path with gate 1, optionally the draft expert).
 // With dense_on false the dense sources are left out of the two grouped
@@ -248,6 +379,10 @@ int run_grouped(const de_moe_desc& d, int T, const float* x, const de::RoutedSrc
                 const de::TopkUnionArgs* fused_sel, hipStream_t s, bool dense_on = true,
                 bool combine_on = true, bool fuse_select = false,
                 const float* next_router = nullptr) {
+  if (fused_sel != nullptr && fuse_select && dense_on && combine_on && next_router == nullptr &&
+      draft_w == nullptr && !r.absent_ok && L.fused && de::verify_fused_enabled()) {
+    return run_fused(d, T, x, r, kk, shared_w, y, epi, L, ws, *fused_sel, s);
+  }
   const bool q4 = d.wdtype == DE_Q4_0;
   const size_t esz = q4 ? 0 : elem_bytes(d.wdtype);
   de::GroupedArgs g{};
@@ -364,6 +499,15 @@ int32_t* layer_status_word(void* ws) { return at<int32_t>(ws, kStatusOff); }
 bool lmhead_mfma_enabled() {
   const char* e = std::getenv("DE_LMHEAD_MFMA");
   return e == nullptr || e[0] != '0';
+}
+
+// The verify layer runs as one launch, where its shape allows, only when
+// DE_VERIFY_FUSED is "1": the down blocks wait for gate/up outputs that the
+// last gate/up waves write, so the launch is slower than the separate
+// launches (both give the same bits).
+bool verify_fused_enabled() {
+  const char* e = std::getenv("DE_VERIFY_FUSED");
+  return e != nullptr && e[0] == '1';
 }
 
 // The persistent draft pass is used unless DE_DRAFT_PERSISTENT is "0" (the
@@ -957,8 +1101,14 @@ int dense_swiglu_chain(int T, int H, int I, int wdtype, const float* x, const vo
 
 extern "C" {
 
+int de_verify_single_launch(const de_moe_desc* d, int T) {
+  if (de_check_desc(d) != DE_OK || check_T(T) != DE_OK || !de::verify_fused_enabled()) return 0;
+  return fused_shape(*d, T, nullptr, nullptr) ? 1 : 0;
+}
+
 int de_time_next_phase(int phase, hipEvent_t start, hipEvent_t stop) {
-  if (phase != DE_PHASE_GATEUP && phase != DE_PHASE_DOWN) return DE_ERR_INVALID;
+  if (phase != DE_PHASE_GATEUP && phase != DE_PHASE_DOWN && phase != DE_PHASE_LAYER)
+    return DE_ERR_INVALID;
   t_start[phase] = start;
   t_stop[phase] = stop;
   return DE_OK;

@@ -96,6 +96,11 @@ struct DenseSrc {
   float* out;        // gate/up: A [T, inter]; down: P [T, out_stride]
   int out_stride;
   const void* ws;    // down, Q4_0 weights: the scales of the matrix's first row
+  // The single-launch verify layer only: every output value also goes to
+  // out_tag (same indexing as out) as a 64-bit (value, launch epoch) pair, and
+  // the down pass reads its input pairs from vin_tag (same indexing as vin).
+  uint64_t* out_tag;
+  const uint64_t* vin_tag;
 };
 
 // The routed part of a grouped launch: the union members and their lists.
@@ -122,6 +127,10 @@ struct RoutedSrc {
   // kStatusNotResident into *status (when not NULL).
   int absent_ok;
   int32_t* status;
+  // The single-launch verify layer only: (value, launch epoch) pairs of A_r and
+  // P_r, indexed as a and p.
+  uint64_t* a_tag;
+  uint64_t* p_tag;
 };
 
 // Bits of the device status word of a workspace.
@@ -180,6 +189,7 @@ struct GroupedArgs {
   int fuse_route;
   int fuse_select;
   TopkUnionArgs sel;
+  uint32_t epoch;      // the single-launch verify layer: this launch's tag
 };
 
 // ---------------------------------------------------------------- launchers (HIP side)
