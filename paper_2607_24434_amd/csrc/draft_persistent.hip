@@ -11,11 +11,16 @@
 //   S2   every gate/up output A of the layer is written;
 //   S3   every row of the layer's down projection is written.
 //
-// The next layer's router rows and its shared and draft rows (gate/up and
-// down), which depend on no result, go out between S3's arrival and its
-// wait; only the top-1 expert's rows wait for the selection.  The run pays
-// off for two or more layers (a draft position through the stack); a single
-// layer is faster as separate launches.
+// The next layer's router rows and each wave's first shared or draft
+// gate/up pair, which depend on no result, go out between S3's arrival and
+// its wait; the other gate/up pairs when the wave reaches them, the down
+// rows of the shared and draft experts at S2 with the top-1 expert's.  A
+// wave's loads complete in issue order and the memory queues are shared, so
+// every byte in flight at a device-wide point delays that point's polls:
+// prefetching less (one pair instead of two, the down rows at S2 instead of
+// S3) made a V2-Lite draft position 14% faster.  The run pays off for two or
+// more layers (a draft position through the stack); a single layer is
+// faster as separate launches.
 //
 // The arithmetic is the one of the separate launches, operation for
 // operation (lane l owns the 16-byte weight units l, l + 64, ...; fp32 FMAs in
@@ -42,7 +47,7 @@ constexpr int kPB = 512;           // threads per block: one block per CU
 constexpr int kPW = kPB / kWave;   // waves per block
 constexpr int kSelWave = kPW - 1;  // the wave that selects the top-k in each block
 constexpr int kGUSlots = 3;        // (G, U) row pairs per wave and layer
-constexpr int kGUPre = 2;          // of which issued ahead of the layer's input
+constexpr int kGUPre = 1;          // of which issued ahead of the layer's input
 constexpr int kDnSlots = 4;        // (row, source) down dot products per wave and layer
 // The combine reproduces the 1024-thread combine launch: virtual thread v
 // holds elements v and v + 1024, virtual wave w its 64 threads; real thread t
@@ -362,17 +367,12 @@ __global__ __launch_bounds__(kPB) void draft_persistent_kernel(PDArgs a) {
     if (gr[t].src == 0) issue_gu<GU_IT>(a, ld.shared, a.Is, gr[t].row, r, lane);
     if (gr[t].src == 1) issue_gu<GU_IT>(a, ld.draft, a.Id, gr[t].row, r, lane);
   };
-  // The wave's first kGUPre dense gate/up row pairs and its dense down rows
-  // of a layer are issued ahead of the layer's input.
+  // The wave's first kGUPre dense gate/up row pairs of a layer are issued
+  // ahead of the layer's input.
   const auto issue_dense = [&](int l) {
     const PDLayer ld = layer_at(l);
 #pragma unroll
     for (int t = 0; t < kGUPre; ++t) issue_gu_slot(t, ld, gw[t]);
-#pragma unroll
-    for (int q = 0; q < kDnSlots; ++q) {
-      if (dd[q].i < 0 || dd[q].src == nsrc - 1) continue;
-      issue_dn<DN_IT>(dn_row(a, ld, b + G * dd[q].i, dd[q].src, nullptr), dw[q], lane);
-    }
   };
   const int H4 = H >> 2;
   // A logit block's router rows (expert b * kPW + wave) of layer l, loaded
@@ -406,7 +406,7 @@ __global__ __launch_bounds__(kPB) void draft_persistent_kernel(PDArgs a) {
     return ld.routed + (size_t)slot * ld.stride;
   };
 
-  // ---- prologue: layer 0's dense rows in flight, its input in LDS, its logits
+  // ---- prologue: layer 0's first gate/up pairs in flight, its input in LDS, its logits
   issue_dense(0);
   if (logit_block && a.z_in == nullptr) issue_router(0);
   for (int i = threadIdx.x; i < H; i += kPB) {
@@ -491,8 +491,16 @@ __global__ __launch_bounds__(kPB) void draft_persistent_kernel(PDArgs a) {
     }
     if (wave == kSelWave && !selected) select();
 
-    // ---- S2: arrive, put the top-1 expert's down rows in flight, wait
+    // ---- S2: arrive, put the shared / draft and top-1 down rows in flight, wait
     grid_arrive(a, 2 * l + 1);
+    {
+      const PDLayer ldl = layer_at(l);
+#pragma unroll
+      for (int q = 0; q < kDnSlots; ++q) {
+        if (dd[q].i < 0 || dd[q].src == nsrc - 1) continue;
+        issue_dn<DN_IT>(dn_row(a, ldl, b + G * dd[q].i, dd[q].src, nullptr), dw[q], lane);
+      }
+    }
     bool need_e1 = false;
 #pragma unroll
     for (int q = 0; q < kDnSlots; ++q) need_e1 |= dd[q].i >= 0 && dd[q].src == nsrc - 1;
@@ -536,7 +544,7 @@ __global__ __launch_bounds__(kPB) void draft_persistent_kernel(PDArgs a) {
       st_coherent(a.d_buf + b + G * threadIdx.x, x);
     }
 
-    // ---- S3: arrive, put the next layer's router and dense rows in flight, wait
+    // ---- S3: arrive, put the next layer's router rows and first gate/up pair in flight, wait
     grid_arrive(a, 2 * l + 2);
     if (more) {
       if (logit_block) issue_router(l + 1);
