@@ -589,9 +589,12 @@ int de_stream_probe(const void* buf, size_t bytes, float* sink, hipStream_t stre
 #define DE_PHASE_GATEUP 0 /* the grouped gate/up kernel (Eq. 4 first half) */
 #define DE_PHASE_DOWN 1   /* the grouped down-projection kernel */
 #define DE_PHASE_LAYER 2  /* the verify layer's single launch (de_verify_single_launch) */
+#define DE_PHASE_DRAFT_PASS 3 /* the persistent launch that runs a draft position's MoE
+                               * layers (the first launch, for stacks of more than 32) */
 
-/* Arms a one-shot timer: the next layer call (de_grouped_swiglu,
- * de_draft_layer, de_verify_layer, de_dense_swiglu) made on this host thread
+/* Arms a one-shot timer: the next layer or model call (de_grouped_swiglu,
+ * de_draft_layer, de_verify_layer, de_dense_swiglu, the model forward and
+ * step calls) made on this host thread
  * records `start` on its stream right before launching the kernel of `phase`
  * and `stop` right after it, then disarms.  Either event may be NULL.  The
  * events are created and read by the caller (e.g. hipEventElapsedTime). */

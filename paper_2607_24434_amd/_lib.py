@@ -54,6 +54,7 @@ C_FUNCS = [
 DE_PHASE_GATEUP = 0
 DE_PHASE_DOWN = 1
 DE_PHASE_LAYER = 2
+DE_PHASE_DRAFT_PASS = 3
 DE_TARGET = 0
 DE_DRAFT = 1
 DE_NEED_DRAFT = 0
@@ -405,7 +406,7 @@ def de_time_next_phase(phase, start_event, stop_event):
 
 
 def de_verify_single_launch(desc, T):
-    """True when the verify layer of this shape runs as one cooperative launch."""
+    """True when the verify layer of this shape runs as one launch."""
     return bool(LIB.de_verify_single_launch(ctypes.byref(desc), int(T)))
 
 

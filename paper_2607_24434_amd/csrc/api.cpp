@@ -225,8 +225,8 @@ hipError_t route(const de_moe_desc& d, int T, const float* x, const float* w_rou
 }
 
 // One-shot phase timers armed by de_time_next_phase (per host thread).
-thread_local hipEvent_t t_start[3] = {nullptr, nullptr, nullptr};
-thread_local hipEvent_t t_stop[3] = {nullptr, nullptr, nullptr};
+thread_local hipEvent_t t_start[4] = {nullptr, nullptr, nullptr, nullptr};
+thread_local hipEvent_t t_stop[4] = {nullptr, nullptr, nullptr, nullptr};
 
 // Launches one phase with its armed events (if any) around it.
 template <typename F>
@@ -590,7 +590,8 @@ int draft_persistent_run(const de_moe_desc& d, int n, const PDLayer* layers, con
     static std::atomic<uint32_t> epoch{1};
     a.epoch = epoch.fetch_add(1);
     if (a.epoch == 0) a.epoch = epoch.fetch_add(1);
-    const hipError_t e = launch_draft_persistent(a, s);
+    const hipError_t e =
+        timed_phase(DE_PHASE_DRAFT_PASS, s, [&] { return launch_draft_persistent(a, s); });
     if (e != hipSuccess) {
       // A launch that never started (the device cannot hold the grid, for
       // instance) leaves the work to the separate launches.
@@ -1107,7 +1108,8 @@ int de_verify_single_launch(const de_moe_desc* d, int T) {
 }
 
 int de_time_next_phase(int phase, hipEvent_t start, hipEvent_t stop) {
-  if (phase != DE_PHASE_GATEUP && phase != DE_PHASE_DOWN && phase != DE_PHASE_LAYER)
+  if (phase != DE_PHASE_GATEUP && phase != DE_PHASE_DOWN && phase != DE_PHASE_LAYER &&
+      phase != DE_PHASE_DRAFT_PASS)
     return DE_ERR_INVALID;
   t_start[phase] = start;
   t_stop[phase] = stop;

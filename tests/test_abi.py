@@ -154,6 +154,15 @@ def test_binding_raises_on_error_codes():
     assert ei.value.code == -1
 
 
+def test_phase_timer_accepts_every_declared_phase():
+    for phase in (de.DE_PHASE_GATEUP, de.DE_PHASE_DOWN, de.DE_PHASE_LAYER, de.DE_PHASE_DRAFT_PASS):
+        de.de_time_next_phase(phase, None, None)  # arms nothing: both events NULL
+    for phase in (-1, 4):
+        with pytest.raises(de.DEError) as ei:
+            de.de_time_next_phase(phase, None, None)
+        assert ei.value.code == -1
+
+
 def fake_model(n_layers=3, layer_kw=None, **kw):
     tab = de.make_table(FAKE, 3 * 1408 * 2048 * 2, None, 64)
     lay = dict(w_router=FAKE, bias=None, table=tab, shared_w=FAKE, draft_w=FAKE, gamma=1.0)

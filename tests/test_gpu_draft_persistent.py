@@ -139,3 +139,27 @@ def test_persistent_draft_full_stack_equals_separate_launches():
     print(f"full stack: drafts {block.cpu().tolist()} n,bonus {out.cpu().tolist()}", flush=True)
     del dm
     torch.cuda.empty_cache()
+
+
+def test_draft_pass_phase_timer():
+    """DE_PHASE_DRAFT_PASS brackets the persistent launch of a draft forward
+    (and nothing when the separate launches run)."""
+    model = V2_SMALL
+    dm = device_model(model, model.k_draft + 1)
+    tok = torch.tensor([gen.start_token(model)], dtype=torch.int32, device="cuda")
+    lg = torch.empty(1, model.vocab, dtype=torch.float32, device="cuda")
+    os.environ["DE_DRAFT_PERSISTENT"] = "1"
+    e = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+    for ev in e:
+        ev.record()  # torch reads only events it has recorded once
+    e[0].record()
+    de.de_time_next_phase(de.DE_PHASE_DRAFT_PASS, e[1], e[2])
+    dm.forward(tok, de.DE_DRAFT, lg)
+    e[3].record()
+    torch.cuda.synchronize()
+    inner = e[1].elapsed_time(e[2])
+    outer = e[0].elapsed_time(e[3])
+    print(f"draft pass {1e3 * inner:.1f} us of a {1e3 * outer:.1f} us forward", flush=True)
+    assert 0.0 < inner < outer
+    del dm
+    torch.cuda.empty_cache()
