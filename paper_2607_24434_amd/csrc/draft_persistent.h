@@ -46,13 +46,15 @@ struct PDArgs {
   float* pred_gate;               // [L, k] their gates, or NULL
   float* a_buf;                   // [Is + Id + I] gate/up outputs
   float* d_buf;                   // [H] per-row sums of the down partials
-  float* z_buf;                   // [N] router logits
+  // [N] router logits as 64-bit words (value, tag): the tag in the high half
+  // is (epoch << 6) + layer + 1, so a word of another layer or launch is never
+  // taken for this one's.
+  uint64_t* z_tag;
   float* z_plain;                 // [N] the last selected layer's logits (the workspace's logit row)
   // Arrival flags, one 64-bit word per block: (epoch << 32) | arrivals so
   // far.  The epoch grows with every launch, so flags left by earlier
   // launches are always below this launch's values and nothing is reset.
   uint64_t* grid_flags;           // [grid]
-  uint64_t* sel_flags;            // [logit blocks]: router logits written, per layer
   uint32_t epoch;
   int32_t* status;                // device status word
   PDLayer layers[kPDMaxLayers];

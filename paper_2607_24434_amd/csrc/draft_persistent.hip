@@ -7,7 +7,8 @@
 // prologues and tails.  Here one block per CU stays resident for all the
 // layers, and three device-wide points order the work of a layer:
 //
-//   sel  the layer's router logits are written (the logit blocks' flags);
+//   sel  the layer's router logits are written: each is a 64-bit word
+//        (value, layer tag) that the selecting wave of every block polls;
 //   S2   every gate/up output A of the layer is written;
 //   S3   every row of the layer's down projection is written.
 //
@@ -18,9 +19,12 @@
 // wave's loads complete in issue order and the memory queues are shared, so
 // every byte in flight at a device-wide point delays that point's polls:
 // prefetching less (one pair instead of two, the down rows at S2 instead of
-// S3) made a V2-Lite draft position 14% faster.  The run pays off for two or
-// more layers (a draft position through the stack); a single layer is
-// faster as separate launches.
+// S3) made a V2-Lite draft position 14% faster.  On the same path, the
+// selecting wave selects before its own gate/up work, and publishes the
+// top-1 expert (the top-k's first entry) before it completes the list and
+// the gates, so that the top-1 rows load while it finishes.  The run pays
+// off for two or more layers (a draft position through the stack); a single
+// layer is faster as separate launches.
 //
 // The arithmetic is the one of the separate launches, operation for
 // operation (lane l owns the 16-byte weight units l, l + 64, ...; fp32 FMAs in
@@ -30,8 +34,8 @@
 //
 // Blocks exchange data through agent-scope atomic loads and stores, which
 // stay coherent across the XCDs' L2 caches without a cache-wide write-back,
-// and per-block arrival flags tagged with the launch's epoch (nothing is
-// reset between launches).  Every wait is bounded: a wait that runs out
+// and per-block arrival flags and logit words tagged with the launch's epoch
+// (nothing is reset between launches).  Every wait is bounded: a wait that runs out
 // records kStatusSyncTimeout in the status word, and every later wait of the
 // block returns at once, so the launch always ends.
 #include "de_common.h"
@@ -61,6 +65,16 @@ constexpr int kPDMaxLogit = 32;    // blocks computing router logits (one expert
 
 typedef __attribute__((address_space(4))) const char kchar;
 
+// Values that are the same in every lane, moved to scalar registers.
+__device__ __forceinline__ int uni(int v) { return __builtin_amdgcn_readfirstlane(v); }
+template <typename P>
+__device__ __forceinline__ P* uni(P* p) {
+  const uint64_t v = reinterpret_cast<uint64_t>(p);
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+  return reinterpret_cast<P*>(((uint64_t)hi << 32) | lo);
+}
+
 // Layer l's descriptor, read from the kernel argument segment with a uniform
 // index (scalar loads; a run-time index into a by-value argument would make a
 // per-lane copy of the whole argument).
@@ -83,16 +97,6 @@ __device__ __forceinline__ PDLayer layer_at(int l) {
   d.n_slots = karg<int32_t>(p + offsetof(PDLayer, n_slots));
   d.gamma = karg<float>(p + offsetof(PDLayer, gamma));
   return d;
-}
-
-// Values that are the same in every lane, moved to scalar registers.
-__device__ __forceinline__ int uni(int v) { return __builtin_amdgcn_readfirstlane(v); }
-template <typename P>
-__device__ __forceinline__ P* uni(P* p) {
-  const uint64_t v = reinterpret_cast<uint64_t>(p);
-  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
-  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
-  return reinterpret_cast<P*>(((uint64_t)hi << 32) | lo);
 }
 
 __device__ __forceinline__ float ld_coherent(const float* p) {
@@ -152,6 +156,48 @@ __device__ void grid_wait(const PDArgs& a, unsigned n, int* s_abort) {
   if (threadIdx.x < kWave)
     wait_flags(a, a.grid_flags, gridDim.x, ((uint64_t)a.epoch << 32) | n, s_abort);
   __syncthreads();
+}
+
+// The tag of layer l's logit words in this launch: never 0 (a zeroed word is
+// never taken) and different for every layer of the last 2^26 launches.
+__device__ __forceinline__ uint32_t z_tag_of(const PDArgs& a, int l) {
+  return (a.epoch << 6) + (uint32_t)l + 1u;
+}
+
+// Layer l's N logits (z[0][q]: expert lane + 64 q), once every word carries
+// the layer's tag (one wave).  Bounded: a timeout is recorded and the words
+// are used as they are.
+__device__ void wait_logits(const PDArgs& a, int l, float (&z)[1][4], int* s_abort) {
+  const int lane = threadIdx.x & 63;
+  const uint32_t tag = z_tag_of(a, l);
+  uint64_t w[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int e = lane + q * kWave;
+    w[q] = e < a.N ? ld_coherent64(a.z_tag + e) : (uint64_t)tag << 32;
+  }
+  for (unsigned it = 0;; ++it) {
+    bool ok = true;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) ok = ok && (uint32_t)(w[q] >> 32) == tag;
+    if (__builtin_amdgcn_ballot_w64(!ok) == 0ull) break;
+    if (*(volatile int*)s_abort) break;
+    if (it >= a.spin_limit) {
+      if (lane == 0) give_up(a, s_abort);
+      break;
+    }
+    __builtin_amdgcn_s_sleep(2);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int e = lane + q * kWave;
+      if ((uint32_t)(w[q] >> 32) != tag && e < a.N) w[q] = ld_coherent64(a.z_tag + e);
+    }
+  }
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int e = lane + q * kWave;
+    z[0][q] = e < a.N ? __uint_as_float((uint32_t)w[q]) : 0.f;
+  }
 }
 
 // A (G, U) row pair of the layer: which source, and its row.
@@ -333,7 +379,6 @@ __global__ __launch_bounds__(kPB) void draft_persistent_kernel(PDArgs a) {
   const int rpb = (H + G - 1) / G;
   const int nlogit = (a.N + kPW - 1) / kPW;  // blocks computing router logits
   const bool logit_block = b < nlogit;
-  const uint64_t ep = (uint64_t)a.epoch << 32;
 
   if (threadIdx.x == 0) {
     s_sel_layer = 0;
@@ -384,21 +429,20 @@ __global__ __launch_bounds__(kPB) void draft_persistent_kernel(PDArgs a) {
 #pragma unroll
     for (int j = 0; j < 8; ++j) wr[j] = w4[min(lane + j * kWave, H4 - 1)];
   };
-  // Router logits of layer l from s_x (logit blocks), then the block's flag.
+  // Router logits of layer l from s_x (logit blocks), each published as a
+  // (value, tag) word: no drain and no flag, so the logits do not wait for
+  // the wave's weight loads in flight.
   const auto logits = [&](int l) {
     const int e = b * kPW + wave;
     if (e < a.N) {
       const float4* xs4 = reinterpret_cast<const float4*>(s_x);
       const float z = router_dot_pre(wr, H4, lane, [&](int h) { return xs4[h]; });
-      if (lane == 0) st_coherent(a.z_buf + e, z);
+      if (lane == 0)
+        st_flag(a.z_tag + e, ((uint64_t)z_tag_of(a, l) << 32) | __float_as_uint(z));
     }
-    drain();
-    __syncthreads();
-    if (threadIdx.x == 0) st_flag(a.sel_flags + b, ep | (unsigned)(l + 1));
   };
   // The top-1 expert of layer l's weight block, or NULL when it has no valid slot.
-  const auto e1_block = [&](int l) -> const char* {
-    const PDLayer ld = layer_at(l);
+  const auto e1_block = [&](const PDLayer& ld) -> const char* {
     const int e1 = uni(s_e1);
     const int slot =
         uni((e1 >= 0 && e1 < a.N) ? (ld.slot_of_expert ? ld.slot_of_expert[e1] : e1) : -1);
@@ -421,31 +465,59 @@ __global__ __launch_bounds__(kPB) void draft_persistent_kernel(PDArgs a) {
     // every layer instead of being kept live across the whole run.
     asm volatile("" : "+v"(lane));
     const bool more = l + 1 < a.L;
+    const PDLayer ld = layer_at(l);
     // Top-k of the layer (one wave per block), published in LDS.  Layer 0's
     // logits may come from the previous launch (z_in).
     const auto select = [&]() {
-      if (l > 0 || a.z_in == nullptr)
-        wait_flags(a, a.sel_flags, nlogit, ep | (unsigned)(l + 1), &s_abort);
-      const float* zsrc = (l == 0 && a.z_in != nullptr) ? a.z_in : a.z_buf;
+      const bool given = l == 0 && a.z_in != nullptr;  // layer 0's logits from the caller
       TopkUnionArgs sel{};
       sel.T = 1;
       sel.N = a.N;
       sel.k = a.k;
-      sel.bias = layer_at(l).bias;
+      sel.bias = ld.bias;
       sel.score_func = a.score_func;
       sel.norm_topk = a.norm_topk;
       sel.routed_scale = a.routed_scale;
       float z[1][4];
+      if (given) {
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int e = lane + q * kWave;
-        z[0][q] = e < a.N ? ld_coherent(zsrc + e) : 0.f;
-      }
-      if (b == 0 && zsrc == a.z_buf) {
+        for (int q = 0; q < 4; ++q) {
+          const int e = lane + q * kWave;
+          z[0][q] = e < a.N ? ld_coherent(a.z_in + e) : 0.f;
+        }
+      } else {
+        wait_logits(a, l, z, &s_abort);
+        if (b == 0) {
 #pragma unroll
-        for (int q = 0; q < 4; ++q)
-          if (lane + q * kWave < a.N) a.z_plain[lane + q * kWave] = z[0][q];
+          for (int q = 0; q < 4; ++q)
+            if (lane + q * kWave < a.N) a.z_plain[lane + q * kWave] = z[0][q];
+        }
       }
+      // The top-1 expert first, published at once so that its rows load while
+      // the rest of the selection runs: the first round of topk_regs (the
+      // largest key, ties to the lower id), computed the same way, so it is
+      // the list's first entry.
+      {
+        float bk = -INFINITY;
+        int bid = INT_MAX;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int e = lane + q * kWave;
+          if (e >= a.N) continue;
+          const float bias = sel.bias != nullptr ? sel.bias[e] : 0.f;
+          float kk = sel.score_func == 0 ? z[0][q] + bias : 1.0f / (1.0f + expf(-z[0][q])) + bias;
+          if (!(kk == kk)) kk = -INFINITY;
+          if (kk > bk || (kk == bk && e < bid)) {
+            bk = kk;
+            bid = e;
+          }
+        }
+        const float m = wave_max(bk);
+        const int win = wave_min_i32(bk == m ? bid : INT_MAX);
+        if (lane == 0) s_e1 = win;
+        __hip_atomic_store(&s_sel_layer, l + 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+      }
+      // The whole list and the gates (g1 is read after the S2 barrier).
       topk_regs<1>(sel, z, s_idx, s_sc);
       if (lane < a.k) {
         const float g = topk_gate(sel, s_sc, lane);
@@ -453,8 +525,6 @@ __global__ __launch_bounds__(kPB) void draft_persistent_kernel(PDArgs a) {
         if (b == 0 && a.pred_idx != nullptr) a.pred_idx[(size_t)l * a.k + lane] = s_idx[lane];
         if (b == 0 && a.pred_gate != nullptr) a.pred_gate[(size_t)l * a.k + lane] = g;
       }
-      if (lane == 0) s_e1 = s_idx[0];
-      __hip_atomic_store(&s_sel_layer, l + 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
     };
     const auto wait_selected = [&]() {
       for (unsigned i = 0; i < 16 * a.spin_limit; ++i) {
@@ -465,51 +535,45 @@ __global__ __launch_bounds__(kPB) void draft_persistent_kernel(PDArgs a) {
       if (lane == 0) give_up(a, &s_abort);
     };
 
-    // ---- gate/up: dense rows (already in flight), then the top-1 expert's
-    bool selected = false;
+    // ---- the selection first (the selecting wave's own gate/up loads would
+    // delay it), then gate/up: dense rows, then the top-1 expert's
+    if (wave == kSelWave) select();
 #pragma unroll
     for (int t = 0; t < kGUSlots; ++t) {
       if (gr[t].src < 0) continue;
       if (gr[t].src == 2) {
-        if (wave == kSelWave) {
-          if (!selected) select();
-          selected = true;
-        } else {
-          wait_selected();
-        }
-        const char* blk = e1_block(l);
+        if (wave != kSelWave) wait_selected();
+        const char* blk = e1_block(ld);
         if (blk == nullptr) {
           if (lane == 0) st_coherent(a.a_buf + gr[t].p, 0.f);
           continue;
         }
         issue_gu<GU_IT>(a, blk, a.I, gr[t].row, gw[t % kGUPre], lane);
       } else if (t >= kGUPre) {
-        issue_gu_slot(t, layer_at(l), gw[t % kGUPre]);
+        issue_gu_slot(t, ld, gw[t % kGUPre]);
       }
       const float v = fma_gu<GU_IT>(a, gw[t % kGUPre], s_x, lane);
       if (lane == 0) st_coherent(a.a_buf + gr[t].p, v);
     }
-    if (wave == kSelWave && !selected) select();
 
     // ---- S2: arrive, put the shared / draft and top-1 down rows in flight, wait
     grid_arrive(a, 2 * l + 1);
     {
-      const PDLayer ldl = layer_at(l);
 #pragma unroll
       for (int q = 0; q < kDnSlots; ++q) {
         if (dd[q].i < 0 || dd[q].src == nsrc - 1) continue;
-        issue_dn<DN_IT>(dn_row(a, ldl, b + G * dd[q].i, dd[q].src, nullptr), dw[q], lane);
+        issue_dn<DN_IT>(dn_row(a, ld, b + G * dd[q].i, dd[q].src, nullptr), dw[q], lane);
       }
     }
     bool need_e1 = false;
 #pragma unroll
     for (int q = 0; q < kDnSlots; ++q) need_e1 |= dd[q].i >= 0 && dd[q].src == nsrc - 1;
-    const char* e1blk = e1_block(l);  // selected: every wave passed the block barrier
+    const char* e1blk = e1_block(ld);  // selected: every wave passed the block barrier
     if (need_e1 && e1blk != nullptr) {
 #pragma unroll
       for (int q = 0; q < kDnSlots; ++q) {
         if (dd[q].i < 0 || dd[q].src != nsrc - 1) continue;
-        issue_dn<DN_IT>(dn_row(a, layer_at(l), b + G * dd[q].i, dd[q].src, e1blk), dw[q], lane);
+        issue_dn<DN_IT>(dn_row(a, ld, b + G * dd[q].i, dd[q].src, e1blk), dw[q], lane);
       }
     }
     grid_wait(a, 2 * l + 1, &s_abort);
@@ -527,11 +591,11 @@ __global__ __launch_bounds__(kPB) void draft_persistent_kernel(PDArgs a) {
 #pragma unroll
     for (int q = 0; q < kDnSlots; ++q) {
       if (dd[q].i < 0) continue;
-      const DnRow r = dn_row(a, layer_at(l), b + G * dd[q].i, dd[q].src, e1blk);
+      const DnRow r = dn_row(a, ld, b + G * dd[q].i, dd[q].src, e1blk);
       float v = 0.f;
       if (r.w != nullptr) {
         const float dot = fma_dn<DN_IT>(r, dw[q], s_a, lane);
-        const float gm = r.routed ? g1 : (dd[q].src < a.n_chunks ? 1.0f : layer_at(l).gamma);
+        const float gm = r.routed ? g1 : (dd[q].src < a.n_chunks ? 1.0f : ld.gamma);
         v = gm * dot;
       }
       if (lane == 0) s_part[dd[q].i * nsrc + dd[q].src] = v;
