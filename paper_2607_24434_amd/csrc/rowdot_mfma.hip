@@ -18,10 +18,11 @@
 // positions); D holds rows 4g .. 4g + 3 of position l % 16.  A and B use the
 // same column assignment, which is all the product needs.
 //
-// A wave owns tiles of 16 weight rows and streams them as one flat sequence
-// of 32-column steps with kMRing steps of loads in flight, across tile
-// boundaries.  The grid has just enough waves for every wave to own the same
-// number of tiles, so no wave has a partial last round.
+// A block owns a contiguous range of tiles of 16 weight rows, one block per
+// CU on every CU; its waves take the tiles round-robin and stream them as one
+// flat sequence of 32-column steps with kMRing steps of loads in flight,
+// across tile boundaries.  (Giving every wave the same number of tiles
+// instead left 56 of 256 CUs idle at V = 102400.)
 #include "de_common.h"
 
 namespace de {
@@ -46,7 +47,7 @@ __device__ __forceinline__ float bf16_value(uint32_t b) { return __uint_as_float
 __global__ __launch_bounds__(kMThreads) void rowdot_mfma_kernel(const uint16_t* __restrict__ w,
                                                                 const float* __restrict__ x,
                                                                 float* __restrict__ out, int T,
-                                                                int H, int V, int tiles_per_wave) {
+                                                                int H, int V, int tiles_per_block) {
   extern __shared__ __align__(16) uint16_t xs[];  // [3][T][H + kMPad]
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int ld = H + kMPad;
@@ -71,15 +72,17 @@ __global__ __launch_bounds__(kMThreads) void rowdot_mfma_kernel(const uint16_t* 
   const bool has_pos = n < T;
   const int nk = H / 32;
   const int tiles = (V + 15) / 16;
-  const int wid = blockIdx.x * kMWaves + wave;
-  const int t0 = wid * tiles_per_wave;
-  const int ntile = min(tiles_per_wave, tiles - t0);
+  // The block's tiles [b0, b1); the wave's are t0, t0 + kMWaves, ...
+  const int b0 = blockIdx.x * tiles_per_block;
+  const int b1 = min(b0 + tiles_per_block, tiles);
+  const int t0 = b0 + wave;
+  const int ntile = t0 < b1 ? (b1 - t0 + kMWaves - 1) / kMWaves : 0;
   if (ntile <= 0) return;
   const int steps = ntile * nk;
   // Lane's weight row pointer for the tile of step s (rows clamped into the
   // matrix; rows past V are computed and not stored).
   const auto row_ptr = [&](int s) {
-    const int tile = t0 + s / nk;
+    const int tile = t0 + (s / nk) * kMWaves;
     const int row = min(tile * 16 + n, V - 1);
     return w + (size_t)row * H + (size_t)(s % nk) * 32 + 8 * g;
   };
@@ -113,7 +116,7 @@ __global__ __launch_bounds__(kMThreads) void rowdot_mfma_kernel(const uint16_t* 
           ring[q] = __builtin_nontemporal_load((const DE_GLOBAL u32x4*)row_ptr(s + kMRing));
         if (s % nk == nk - 1) {
           // Rows 4g .. 4g + 3 of the tile, position n.
-          const int r = (t0 + s / nk) * 16 + 4 * g;
+          const int r = (t0 + (s / nk) * kMWaves) * 16 + 4 * g;
           if (has_pos) {
             float* o = out + (size_t)n * V + r;
             if (r + 3 < V) {
@@ -154,11 +157,11 @@ hipError_t launch_rowdot_mfma(int T, int H, int V, const float* x, const void* w
     return note_hip(e);
   }
   const int tiles = (V + 15) / 16;
-  const int waves = dev_info().num_cus * kMWaves;
-  const int tpw = (tiles + waves - 1) / waves;
-  const int blocks = (tiles + tpw * kMWaves - 1) / (tpw * kMWaves);
+  const int cus = dev_info().num_cus;
+  const int tpb = (tiles + cus - 1) / cus;
+  const int blocks = (tiles + tpb - 1) / tpb;
   hipLaunchKernelGGL(rowdot_mfma_kernel, dim3(blocks), dim3(kMThreads), lds, s,
-                     static_cast<const uint16_t*>(w), x, out, T, H, V, tpw);
+                     static_cast<const uint16_t*>(w), x, out, T, H, V, tpb);
   return note_hip(hipGetLastError());
 }
 
