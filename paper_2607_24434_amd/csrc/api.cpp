@@ -125,7 +125,7 @@ static_assert(kPDFlagsOff + (de::kPDMaxGrid + 32) * 8 <= kCtlBytes, "control are
 struct Layout {
   size_t ctl, z, idx, gate, nu, uids, offs, tok, glist, ppos;
   size_t a_r, a_s, a_d, p_r, p_s, p_d;
-  size_t pd;  // persistent draft pass: gate/up outputs [Is + Id + I], row sums [H], logit words [N] (8 bytes)
+  size_t pd;  // persistent draft pass: gate/up outputs [Is + Id + I], row words [H], logit words [N] (8 bytes)
   // The single-launch verify layer (only for the shapes it serves, else
   // fused = false): (value, epoch) words of A_r, A_s, P_r and the shared
   // down chunks' partials.
@@ -163,6 +163,12 @@ Layout layout(const de_moe_desc& d, int T) {
   // (sticky until de_layer_status reads it), the persistent draft pass's
   // flags from byte 1024.
   L.ctl = take(kCtlBytes);
+  // The persistent draft pass's buffers (its logit and down-row words are
+  // tagged), at the same offset in every layout, so that no call of another
+  // block length writes there (a value left there by another buffer could
+  // carry a matching tag).
+  L.pd = take(((size_t)d.shared_inter + d.draft_inter + d.inter) * 4 +
+              ((size_t)d.hidden + d.n_experts) * 8);
   L.z = take((size_t)T * d.n_experts * 4);
   L.idx = take(tk * 4);
   L.gate = take(tk * 4);
@@ -178,7 +184,6 @@ Layout layout(const de_moe_desc& d, int T) {
   L.p_r = take(tk * d.hidden * 4);
   L.p_s = take((size_t)kMaxSharedChunks * T * d.hidden * 4);
   L.p_d = take((size_t)T * d.hidden * 4);
-  L.pd = take(((size_t)d.shared_inter + d.draft_inter + d.inter + d.hidden + 2 * d.n_experts) * 4);
   L.fused = fused_shape(d, T, &L.chunks, &L.lds);
   if (L.fused) {
     L.t_ar = take(tk * d.inter * 8);
@@ -566,8 +571,9 @@ int draft_persistent_run(const de_moe_desc& d, int n, const PDLayer* layers, con
   a.spin_limit = 1u << 20;
   a.lds_bytes = draft_persistent_lds(sh);
   a.a_buf = at<float>(ws, L.pd);
-  a.d_buf = a.a_buf + (sh.Is + sh.Id + sh.I);
-  a.z_tag = reinterpret_cast<uint64_t*>(a.d_buf + d.hidden);  // 8-byte aligned: Is, Id, I, H are multiples of 8
+  // 8-byte aligned: Is, Id and I are multiples of 8.
+  a.d_tag = reinterpret_cast<uint64_t*>(a.a_buf + (sh.Is + sh.Id + sh.I));
+  a.z_tag = a.d_tag + d.hidden;
   a.z_plain = at<float>(ws, L.z);
   a.grid_flags = at<uint64_t>(ws, kPDFlagsOff);
   a.status = at<int32_t>(ws, kStatusOff);

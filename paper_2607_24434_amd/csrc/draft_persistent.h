@@ -45,7 +45,9 @@ struct PDArgs {
   int32_t* pred_idx;              // [L, k] the top-k of every layer, or NULL
   float* pred_gate;               // [L, k] their gates, or NULL
   float* a_buf;                   // [Is + Id + I] gate/up outputs
-  float* d_buf;                   // [H] per-row sums of the down partials
+  // [H] per-row sums of the down partials as (value, tag) words, tagged like
+  // the logit words.
+  uint64_t* d_tag;
   // [N] router logits as 64-bit words (value, tag): the tag in the high half
   // is (epoch << 6) + layer + 1, so a word of another layer or launch is never
   // taken for this one's.

@@ -10,7 +10,8 @@
 //   sel  the layer's router logits are written: each is a 64-bit word
 //        (value, layer tag) that the selecting wave of every block polls;
 //   S2   every gate/up output A of the layer is written;
-//   S3   every row of the layer's down projection is written.
+//   S3   every row of the layer's down projection is written: each row is a
+//        (value, layer tag) word that every block's combine polls.
 //
 // The next layer's router rows and each wave's first shared or draft
 // gate/up pair, which depend on no result, go out between S3's arrival and
@@ -34,8 +35,8 @@
 //
 // Blocks exchange data through agent-scope atomic loads and stores, which
 // stay coherent across the XCDs' L2 caches without a cache-wide write-back,
-// and per-block arrival flags and logit words tagged with the launch's epoch
-// (nothing is reset between launches).  Every wait is bounded: a wait that runs out
+// and per-block arrival flags, logit and down-row words tagged with the
+// launch's epoch (nothing is reset between launches).  Every wait is bounded: a wait that runs out
 // records kStatusSyncTimeout in the status word, and every later wait of the
 // block returns at once, so the launch always ends.
 #include "de_common.h"
@@ -158,9 +159,10 @@ __device__ void grid_wait(const PDArgs& a, unsigned n, int* s_abort) {
   __syncthreads();
 }
 
-// The tag of layer l's logit words in this launch: never 0 (a zeroed word is
-// never taken) and different for every layer of the last 2^26 launches.
-__device__ __forceinline__ uint32_t z_tag_of(const PDArgs& a, int l) {
+// The tag of layer l's logit and down-row words in this launch: never 0 (a
+// zeroed word is never taken) and different for every layer of the last
+// 2^26 launches.
+__device__ __forceinline__ uint32_t layer_tag(const PDArgs& a, int l) {
   return (a.epoch << 6) + (uint32_t)l + 1u;
 }
 
@@ -169,7 +171,7 @@ __device__ __forceinline__ uint32_t z_tag_of(const PDArgs& a, int l) {
 // are used as they are.
 __device__ void wait_logits(const PDArgs& a, int l, float (&z)[1][4], int* s_abort) {
   const int lane = threadIdx.x & 63;
-  const uint32_t tag = z_tag_of(a, l);
+  const uint32_t tag = layer_tag(a, l);
   uint64_t w[4];
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
@@ -438,7 +440,7 @@ __global__ __launch_bounds__(kPB) void draft_persistent_kernel(PDArgs a) {
       const float4* xs4 = reinterpret_cast<const float4*>(s_x);
       const float z = router_dot_pre(wr, H4, lane, [&](int h) { return xs4[h]; });
       if (lane == 0)
-        st_flag(a.z_tag + e, ((uint64_t)z_tag_of(a, l) << 32) | __float_as_uint(z));
+        st_flag(a.z_tag + e, ((uint64_t)layer_tag(a, l) << 32) | __float_as_uint(z));
     }
   };
   // The top-1 expert of layer l's weight block, or NULL when it has no valid slot.
@@ -605,16 +607,19 @@ __global__ __launch_bounds__(kPB) void draft_persistent_kernel(PDArgs a) {
     if (threadIdx.x < rpb && b + G * (int)threadIdx.x < H) {
       float x = 0.f;
       for (int s = 0; s < nsrc; ++s) x += s_part[threadIdx.x * nsrc + s];
-      st_coherent(a.d_buf + b + G * threadIdx.x, x);
+      st_flag(a.d_tag + b + G * threadIdx.x,
+              ((uint64_t)layer_tag(a, l) << 32) | __float_as_uint(x));
     }
 
-    // ---- S3: arrive, put the next layer's router rows and first gate/up pair in flight, wait
-    grid_arrive(a, 2 * l + 2);
+    // ---- S3 (every down row written) is the row words' tags: put the next
+    // layer's router rows and first gate/up pair in flight, then gather.  The
+    // words also order the reuse of A: a block writes the next layer's A only
+    // after its combine, which needs every block's rows, which each block
+    // writes after it staged this layer's A.
     if (more) {
       if (logit_block) issue_router(l + 1);
       issue_dense(l + 1);
     }
-    grid_wait(a, 2 * l + 2, &s_abort);
 
     // ---- combine: y = residual + the row sums; RMSNorm(y) (the combine
     // launch's element order and reduction order).  Virtual thread
@@ -623,6 +628,38 @@ __global__ __launch_bounds__(kPB) void draft_persistent_kernel(PDArgs a) {
     const bool has_res = l > 0 || a.h_in != nullptr;
     const bool want_norm = more || a.normed_out != nullptr;
     constexpr int kVT = kCombVT / kPB, kPer = kPDMaxH / kCombVT;
+    uint64_t dwd[kVT][kPer];
+    {
+      const uint32_t tag = layer_tag(a, l);
+#pragma unroll
+      for (int j = 0; j < kVT; ++j)
+#pragma unroll
+        for (int i = 0; i < kPer; ++i) {
+          const int h = threadIdx.x + kPB * j + kCombVT * i;
+          dwd[j][i] = h < H ? ld_coherent64(a.d_tag + h) : (uint64_t)tag << 32;
+        }
+      for (unsigned it = 0;; ++it) {
+        bool ok = true;
+#pragma unroll
+        for (int j = 0; j < kVT; ++j)
+#pragma unroll
+          for (int i = 0; i < kPer; ++i) ok = ok && (uint32_t)(dwd[j][i] >> 32) == tag;
+        if (__builtin_amdgcn_ballot_w64(!ok) == 0ull) break;
+        if (*(volatile int*)&s_abort) break;
+        if (it >= a.spin_limit) {
+          if (lane == 0) give_up(a, &s_abort);
+          break;
+        }
+        __builtin_amdgcn_s_sleep(2);
+#pragma unroll
+        for (int j = 0; j < kVT; ++j)
+#pragma unroll
+          for (int i = 0; i < kPer; ++i) {
+            const int h = threadIdx.x + kPB * j + kCombVT * i;
+            if ((uint32_t)(dwd[j][i] >> 32) != tag && h < H) dwd[j][i] = ld_coherent64(a.d_tag + h);
+          }
+      }
+    }
     float v[kVT][kPer];
     float ss[kVT];
 #pragma unroll
@@ -633,7 +670,7 @@ __global__ __launch_bounds__(kPB) void draft_persistent_kernel(PDArgs a) {
         const int h = threadIdx.x + kPB * j + kCombVT * i;
         v[j][i] = 0.f;
         if (h < H) {
-          float x = ld_coherent(a.d_buf + h);
+          float x = __uint_as_float((uint32_t)dwd[j][i]);
           if (has_res) x = s_h[h] + x;
           v[j][i] = x;
           ss[j] = fmaf(x, x, ss[j]);
