@@ -618,7 +618,9 @@ __global__ __launch_bounds__(kPB) void draft_persistent_kernel(PDArgs a) {
     // writes after it staged this layer's A.
     if (more) {
       if (logit_block) issue_router(l + 1);
-      issue_dense(l + 1);
+      // A logit block's gate/up pair goes out after its logits (below): its
+      // logit words then do not queue behind it.
+      if (!logit_block) issue_dense(l + 1);
     }
 
     // ---- combine: y = residual + the row sums; RMSNorm(y) (the combine
@@ -705,7 +707,10 @@ __global__ __launch_bounds__(kPB) void draft_persistent_kernel(PDArgs a) {
       }
     }
     __syncthreads();
-    if (more && logit_block) logits(l + 1);
+    if (more && logit_block) {
+      logits(l + 1);
+      issue_dense(l + 1);
+    }
   }
 
   if (b == 0 && threadIdx.x == 0 && s_missing)
