@@ -311,15 +311,18 @@ __global__ __launch_bounds__(kCombThreads) void combine_kernel(CombineArgs a) {
 }
 
 // The combine of one layer and the router logits of the next (Eq. 1) in one
-// launch.  Block (t, g) combines position t (the g = 0 blocks write y and
+// launch.  Block L = t G + g combines position t (the g = 0 blocks write y and
 // RMSNorm(y); every block keeps the normalised row in LDS) and computes the
 // next layer's logits of experts 16 g .. 16 g + 15, one per wave, with the
-// same arithmetic as the routing launch.
+// same arithmetic as the routing launch.  (The expert group varies fastest:
+// workgroups go to the XCDs round-robin, so one group's router rows are read
+// from memory by a few XCDs' L2 caches instead of one per position.)
 __global__ __launch_bounds__(kCombThreads) void combine_route_kernel(CombineArgs a, RouteArgs r) {
   __shared__ float red[kCombThreads / 64];
-  const int t = blockIdx.x;
+  const int G = (r.sel.N + kCombThreads / kWave - 1) / (kCombThreads / kWave);
+  const int t = blockIdx.x / G, grp = blockIdx.x - t * G;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int e = blockIdx.y * (kCombThreads / kWave) + wave;
+  const int e = grp * (kCombThreads / kWave) + wave;
   const int H4 = r.H >> 2;
   const float4* w4 = reinterpret_cast<const float4*>(r.w) + (size_t)min(e, r.sel.N - 1) * H4;
   // A router row of at most 2048 floats is loaded before the combine (it does
@@ -328,7 +331,7 @@ __global__ __launch_bounds__(kCombThreads) void combine_route_kernel(CombineArgs
   float4 wp[8];
 #pragma unroll
   for (int j = 0; j < 8; ++j) wp[j] = pre ? w4[min(lane + j * kWave, H4 - 1)] : float4{};
-  combine_row<kCombThreads>(a, t, red, s_dyn, blockIdx.y == 0);
+  combine_row<kCombThreads>(a, t, red, s_dyn, grp == 0);
   __syncthreads();
   if (e < r.sel.N) {
     const float4* xs4 = reinterpret_cast<const float4*>(s_dyn);
@@ -467,8 +470,9 @@ hipError_t launch_combine_route(const CombineArgs& a, const RouteArgs& r, hipStr
   if (rows_overlap(a.residual, a.y, a.T, a.H) || rows_overlap(a.residual, a.normed, a.T, a.H) ||
       rows_overlap(a.y, a.normed, a.T, a.H))
     return note_hip(hipErrorInvalidValue);
-  const dim3 grid(a.T, (r.sel.N + kCombThreads / kWave - 1) / (kCombThreads / kWave));
-  hipLaunchKernelGGL(combine_route_kernel, grid, dim3(kCombThreads), (size_t)a.H * 4, s, a, r);
+  const int G = (r.sel.N + kCombThreads / kWave - 1) / (kCombThreads / kWave);
+  hipLaunchKernelGGL(combine_route_kernel, dim3(a.T * G), dim3(kCombThreads), (size_t)a.H * 4, s,
+                     a, r);
   return note_hip(hipGetLastError());
 }
 

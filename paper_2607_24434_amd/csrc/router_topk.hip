@@ -38,8 +38,8 @@ __device__ inline SelView view_of(SelShared& s) {
   return SelView{s.idx, s.sc, s.gate, s.mask, s.off, s.upos, s.misc};
 }
 
-// Block (t, g): router logits of position t (Eq. 1) for experts
-// 16g .. 16g+15, one per wave, each router row's and x_t's loads in flight
+// Block (t, g) (see the index map below): router logits of position t
+// (Eq. 1) for experts 16g .. 16g+15, one per wave, each router row's and x_t's loads in flight
 // together.  The logits go to z.  With r.select, the last of the position's
 // blocks to finish (device-scope counter, release / acquire fences so logits
 // written on other XCDs are visible; the counter is left at zero) selects the
@@ -49,11 +49,16 @@ __global__ __launch_bounds__(kRsThreads) void route_split_kernel(RouteArgs r) {
   __shared__ float lsc[kMaxK];
   __shared__ int s_last;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int t = blockIdx.x;
+  // Block L is (position L / G, expert group L % G): workgroups go to the
+  // XCDs round-robin by index, so the blocks of one expert group share a
+  // few XCDs' L2 caches and read its router rows from memory once per XCD
+  // instead of once per position.
+  const int G = (r.sel.N + kRsWaves - 1) / kRsWaves;
+  const int t = blockIdx.x / G, grp = blockIdx.x - t * G;
   const int H4 = r.H >> 2, N = r.sel.N, k = r.sel.k;
   const float4* xg = reinterpret_cast<const float4*>(r.x) + (size_t)t * H4;
   const float4* w4 = reinterpret_cast<const float4*>(r.w);
-  const int e = blockIdx.y * kRsWaves + wave;
+  const int e = grp * kRsWaves + wave;
   if (e < N) {
     const float acc = router_dot(w4 + (size_t)e * H4, H4, lane, [&](int h) { return xg[h]; });
     if (lane == 0) r.z[(size_t)t * N + e] = acc;
@@ -64,7 +69,7 @@ __global__ __launch_bounds__(kRsThreads) void route_split_kernel(RouteArgs r) {
     __threadfence();
     const unsigned prev = __hip_atomic_fetch_add(r.counter + t, 1u, __ATOMIC_ACQ_REL,
                                                  __HIP_MEMORY_SCOPE_AGENT);
-    s_last = prev == gridDim.y - 1;
+    s_last = prev == (unsigned)G - 1;
     if (s_last) __hip_atomic_store(r.counter + t, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
   __syncthreads();
@@ -96,8 +101,8 @@ __global__ __launch_bounds__(kSelThreads) void union_kernel(TopkUnionArgs a) {
 // so all the router rows of a position stream in parallel and each position's
 // selection (when r.select) runs in its own last block.
 hipError_t launch_route(const RouteArgs& r, hipStream_t s) {
-  const dim3 grid(r.sel.T, (r.sel.N + kRsWaves - 1) / kRsWaves);
-  hipLaunchKernelGGL(route_split_kernel, grid, dim3(kRsThreads), 0, s, r);
+  const int G = (r.sel.N + kRsWaves - 1) / kRsWaves;
+  hipLaunchKernelGGL(route_split_kernel, dim3(r.sel.T * G), dim3(kRsThreads), 0, s, r);
   return note_hip(hipGetLastError());
 }
 
