@@ -390,9 +390,13 @@ bool small_launch(const GroupedArgs& a, bool gateup) {
   return max_tiles(a, gateup, kNS) < dev_info().num_cus * 2 * kWavesPB;
 }
 
+// Two-row tiles for small launches and for a single position (read from
+// global memory): the 2 x 10944 gate/up rows of a dense layer at T = 1 are
+// 1.34 rounds of four-row tiles over the grid's waves (a second round a
+// third full) and 1.78 rounds of two-row tiles.
 template <typename WT, bool LDSX>
 hipError_t gateup_tiles(const GroupedArgs& a, size_t lds, hipStream_t s) {
-  if (small_launch(a, true))
+  if (small_launch(a, true) || !LDSX)
     return launch_persistent(gateup_kernel<WT, LDSX, 2>, max_tiles(a, true, 2), lds, a, s);
   return launch_persistent(gateup_kernel<WT, LDSX, kNS>, max_tiles(a, true, kNS), lds, a, s);
 }
