@@ -39,7 +39,7 @@ size_t verify_fused_pub_words(int T, int N, int k);
 // CU resident).
 hipError_t launch_verify_fused(const FusedArgs& f, size_t lds, hipStream_t s);
 
-// Host side (api.cpp): false when DE_VERIFY_FUSED is "0".
+// Host side (api.cpp): true only when DE_VERIFY_FUSED is "1".
 bool verify_fused_enabled();
 
 }  // namespace de
