@@ -522,7 +522,14 @@ bool draft_persistent_enabled() {
   return e == nullptr || e[0] != '0';
 }
 
-// Runs draft layers layers[0..n) (n >= 2) of one position (T = 1, the top-1
+// The single draft layer calls (T = 1, r = 1) through the persistent kernel
+// as well; DE_PD_SINGLE=0 keeps them on the separate launches.
+bool pd_single_enabled() {
+  const char* e = std::getenv("DE_PD_SINGLE");
+  return e == nullptr || e[0] != '0';
+}
+
+// Runs draft layers layers[0..n) (n >= 1) of one position (T = 1, the top-1
 // drafter of Eq. 5) in persistent launches of at most kPDMaxLayers layers.  x_in is the
 // first layer's input RMSNorm(h), h_in its residual (NULL: y = layer(x));
 // z_ready: the first layer's router logits are already in the workspace's
@@ -532,9 +539,7 @@ int draft_persistent_run(const de_moe_desc& d, int n, const PDLayer* layers, con
                          const float* h_in, bool z_ready, float* y_out, float* normed_out,
                          int32_t* pred_idx, float* pred_gate, float eps, void* ws,
                          size_t ws_bytes, hipStream_t s) {
-  // A single layer is faster as separate launches (no cooperative launch,
-  // no in-kernel routing).
-  if (!draft_persistent_enabled() || n < 2 || d.wdtype != DE_BF16) return kPDNotApplicable;
+  if (!draft_persistent_enabled() || n < 1 || d.wdtype != DE_BF16) return kPDNotApplicable;
   if (ws == nullptr || ws_bytes < layout(d, 1).total) return kPDNotApplicable;
   if (n > kPDMaxLayers && normed_out == nullptr) return kPDNotApplicable;
   // Every layer with a draft block, or none (then the term is dropped).
@@ -873,6 +878,25 @@ int draft_layer_chain(const de_moe_desc* d, int T, const float* x, const float* 
   a.z = at<float>(ws, L.z);
   // Logits only; the gate/up prologue selects the top-k in every block.
   if (next_router != nullptr && (epi == nullptr || epi->normed == nullptr)) return DE_ERR_INVALID;
+  // One position with its leading expert: the persistent kernel runs the
+  // whole layer (routing, gate/up, down, combine) in one launch, with the
+  // same bits.
+  if (T == 1 && r == 1 && !logits_ready && next_router == nullptr && pd_single_enabled()) {
+    PDLayer pl{};
+    pl.w_router = w_router;
+    pl.bias = bias;
+    pl.routed = static_cast<const char*>(routed->base);
+    pl.stride = routed->slot_stride_bytes;
+    pl.slot_of_expert = routed->slot_of_expert;
+    pl.n_slots = routed->n_slots;
+    pl.shared = static_cast<const char*>(shared_w);
+    pl.draft = static_cast<const char*>(draft_w);
+    pl.gamma = gamma;
+    rc = draft_persistent_run(*d, 1, &pl, x, epi ? epi->residual : nullptr, false, y,
+                              epi ? epi->normed : nullptr, pred_idx, pred_gate,
+                              epi ? epi->eps : 0.f, ws, ws_bytes, stream);
+    if (rc != kPDNotApplicable) return rc;
+  }
   if (!logits_ready && route(*d, T, x, w_router, L, ws, a, stream, false) != hipSuccess)
     return DE_ERR_HIP;
   const de::RoutedSrc rs = routed_src(*d, T, r, routed, a.n_union, a.union_ids, a.offsets,
@@ -927,6 +951,11 @@ int verify_layer_chain(const de_moe_desc* d, int T, const float* x, const float*
                      stream, true, true, true, next_router);
 }
 
+int accept_len_embed(int K, int V, const float* target_logits, const int32_t* draft_tokens,
+                     int32_t* target_argmax, int32_t* out, void* ws, size_t ws_bytes,
+                     const void* emb, int H, float* h, float* normed, float eps,
+                     hipStream_t stream);
+
 }  // namespace de
 
 extern "C" {
@@ -940,13 +969,33 @@ size_t de_accept_workspace_bytes(int K, int V) {
 int de_accept_len(int K, int V, const float* target_logits, const int32_t* draft_tokens,
                   int32_t* target_argmax, int32_t* out, void* ws, size_t ws_bytes,
                   hipStream_t stream) {
+  return de::accept_len_embed(K, V, target_logits, draft_tokens, target_argmax, out, ws, ws_bytes,
+                              nullptr, 0, nullptr, nullptr, 0.f, stream);
+}
+
+}  // extern "C"
+
+namespace de {
+
+// de_accept_len that also writes the bonus token's embedding row to h [H] and
+// its RMSNorm to normed when emb (bf16 [V, H]) is not NULL.
+int accept_len_embed(int K, int V, const float* target_logits, const int32_t* draft_tokens,
+                     int32_t* target_argmax, int32_t* out, void* ws, size_t ws_bytes,
+                     const void* emb, int H, float* h, float* normed, float eps,
+                     hipStream_t stream) {
   if (K < 0 || K > 1024 || V < 1 || !target_logits || !target_argmax || !out) return DE_ERR_INVALID;
   if (K > 0 && draft_tokens == nullptr) return DE_ERR_INVALID;
+  if (emb != nullptr && (H < 1 || h == nullptr || normed == nullptr)) return DE_ERR_INVALID;
   if (ws == nullptr || (reinterpret_cast<uintptr_t>(ws) & 255u) != 0 ||
       ws_bytes < de_accept_workspace_bytes(K, V))
     return DE_ERR_WORKSPACE;
   const size_t rows = (size_t)K + 1, ch = (size_t)de::accept_chunks(V);
   de::AcceptArgs a{};
+  a.emb = static_cast<const uint16_t*>(emb);
+  a.H = H;
+  a.h = h;
+  a.normed = normed;
+  a.eps = eps;
   a.K = K;
   a.V = V;
   a.logits = target_logits;
@@ -959,6 +1008,10 @@ int de_accept_len(int K, int V, const float* target_logits, const int32_t* draft
   a.part_i = at<int32_t>(ws, 256 + up256(rows * 4) + up256(rows * ch * 4));
   return hip_status(de::launch_argmax_accept(a, stream));
 }
+
+}  // namespace de
+
+extern "C" {
 
 int de_lm_head(int T, int H, int V, const float* x, const void* w_lm, float* logits,
                hipStream_t stream) {

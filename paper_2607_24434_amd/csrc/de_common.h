@@ -246,6 +246,13 @@ struct AcceptArgs {
   int32_t* part_i;
   unsigned* row_cnt;       // [K+1], zero between calls
   unsigned* done_cnt;      // [1], zero between calls
+  // Optional (emb not NULL): the bonus token's bf16 embedding row [H] goes to
+  // h and its RMSNorm (eps) to normed, as one position of the embedding gather.
+  const uint16_t* emb;
+  float* h;
+  float* normed;
+  float eps;
+  int H;
 };
 int accept_chunks(int V);
 hipError_t launch_argmax_accept(const AcceptArgs& a, hipStream_t s);

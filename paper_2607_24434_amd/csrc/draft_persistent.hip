@@ -44,6 +44,7 @@
 #include "topk_union.h"
 
 #include <cstddef>
+#include <cstdlib>
 
 namespace de {
 namespace {
@@ -731,7 +732,16 @@ hipError_t launch_typed(const PDArgs& a, hipStream_t s) {
   if (occ < 1 || a.grid > occ * dev_info().num_cus) return note_hip(hipErrorCooperativeLaunchTooLarge);
   PDArgs args = a;
   void* params[] = {&args};
-  e = hipLaunchCooperativeKernel(fn, dim3(a.grid), dim3(kPB), params, (unsigned)lds, s);
+  // The grid is one block per CU with at least half of a CU's LDS each, so on
+  // a device the stream has to itself every block is resident at once, and
+  // every wait is bounded in any case.  A cooperative launch guarantees
+  // residency also beside other streams' kernels, at the cost of a
+  // synchronisation before and after the launch; DE_PD_COOPERATIVE=1 asks
+  // for it.
+  const char* env = std::getenv("DE_PD_COOPERATIVE");
+  const bool coop = env != nullptr && env[0] == '1';
+  e = coop ? hipLaunchCooperativeKernel(fn, dim3(a.grid), dim3(kPB), params, (unsigned)lds, s)
+           : hipLaunchKernel(fn, dim3(a.grid), dim3(kPB), params, lds, s);
   if (e != hipSuccess) {
     (void)hipGetLastError();
     return note_hip(e);

@@ -8,105 +8,28 @@ namespace de {
 namespace {
 
 constexpr int kAmThreads = 256;
-constexpr int kAmPer = 16;                        // logits per thread
-constexpr int kAmChunk = kAmThreads * kAmPer;     // logits per block
+constexpr int kAmVec = 4;                         // 16-byte loads per thread
+constexpr int kAmChunk = kAmThreads * kAmVec * 4; // logits per block
 
 // (value, index) ordering for argmax: larger value, then lower index; a NaN
-// counts as -infinity; index INT_MAX marks "none".
+// counts as -infinity; index INT_MAX marks "none".  It is a total order, so
+// the maximum does not depend on the order in which candidates meet.
 __device__ __forceinline__ bool am_better(float va, int ia, float vb, int ib) {
   if (ia == INT_MAX) return false;
   if (ib == INT_MAX) return true;
   return va > vb || (va == vb && ia < ib);
 }
 
-constexpr int kRowThreads = 1024;
-
-// K = 0: the argmax of the single row by one block (each thread scans a
-// strided slice in 16-byte loads when the row allows), with no cross-block
-// step; out = (0, argmax).
-__global__ __launch_bounds__(kRowThreads) void argmax_row_kernel(AcceptArgs a) {
-  __shared__ float sv[kRowThreads / 64];
-  __shared__ int si[kRowThreads / 64];
-  const float* p = a.logits;
-  float bv = -INFINITY;
-  int bi = INT_MAX;
-  const auto offer = [&](float xv, int v) {
-    if (!(xv == xv)) xv = -INFINITY;
-    if (am_better(xv, v, bv, bi)) {
-      bv = xv;
-      bi = v;
-    }
-  };
-  if ((a.V & 3) == 0 && (reinterpret_cast<uintptr_t>(p) & 15u) == 0) {
-    const float4* p4 = reinterpret_cast<const float4*>(p);
-    const int n4 = a.V >> 2;
-#pragma unroll 4
-    for (int j = threadIdx.x; j < n4; j += kRowThreads) {
-      const float4 q = p4[j];
-      offer(q.x, 4 * j);
-      offer(q.y, 4 * j + 1);
-      offer(q.z, 4 * j + 2);
-      offer(q.w, 4 * j + 3);
-    }
-  } else {
-    for (int v = threadIdx.x; v < a.V; v += kRowThreads) offer(p[v], v);
+__device__ __forceinline__ void am_offer(float xv, int v, float& bv, int& bi) {
+  if (!(xv == xv)) xv = -INFINITY;
+  if (am_better(xv, v, bv, bi)) {
+    bv = xv;
+    bi = v;
   }
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    const float ov = __shfl_xor(bv, o, kWave);
-    const int oi = __shfl_xor(bi, o, kWave);
-    if (am_better(ov, oi, bv, bi)) {
-      bv = ov;
-      bi = oi;
-    }
-  }
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  if (lane == 0) {
-    sv[wave] = bv;
-    si[wave] = bi;
-  }
-  __syncthreads();
-  if (threadIdx.x != 0) return;
-  for (int w = 1; w < kRowThreads / 64; ++w)
-    if (am_better(sv[w], si[w], sv[0], si[0])) {
-      sv[0] = sv[w];
-      si[0] = si[w];
-    }
-  const int t = si[0] == INT_MAX ? 0 : si[0];
-  a.amax[0] = t;
-  a.out[0] = 0;
-  a.out[1] = t;
 }
 
-// Grid (chunks, K+1).  Each block finds the argmax of one 4096-logit chunk of
-// one row; the last block of a row (device-scope counter) reduces the row's
-// chunk results in chunk order, and the last row to finish applies the greedy
-// accept rule.  Counters are left at zero.
-__global__ __launch_bounds__(kAmThreads) void argmax_accept_kernel(AcceptArgs a) {
-  __shared__ float sv[kAmThreads / 64];
-  __shared__ int si[kAmThreads / 64];
-  __shared__ int s_flag;
-  const int row = blockIdx.y, chunk = blockIdx.x, nch = gridDim.x;
-  const float* p = a.logits + (size_t)row * a.V;
-  const int base = chunk * kAmChunk;
-  float x[kAmPer];
-#pragma unroll
-  for (int i = 0; i < kAmPer; ++i) {
-    const int v = base + threadIdx.x + i * kAmThreads;
-    x[i] = v < a.V ? p[v] : -INFINITY;
-  }
-  float bv = -INFINITY;
-  int bi = INT_MAX;
-#pragma unroll
-  for (int i = 0; i < kAmPer; ++i) {
-    const int v = base + threadIdx.x + i * kAmThreads;
-    float xv = x[i];
-    if (!(xv == xv)) xv = -INFINITY;
-    if (v < a.V && am_better(xv, v, bv, bi)) {
-      bv = xv;
-      bi = v;
-    }
-  }
+// The block's best (value, index), returned to every thread.
+__device__ void block_argmax(float& bv, int& bi, float* sv, int* si) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) {
     const float ov = __shfl_xor(bv, o, kWave);
@@ -116,45 +39,32 @@ __global__ __launch_bounds__(kAmThreads) void argmax_accept_kernel(AcceptArgs a)
       bi = oi;
     }
   }
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  if (lane == 0) {
-    sv[wave] = bv;
-    si[wave] = bi;
+  if ((threadIdx.x & 63) == 0) {
+    sv[threadIdx.x >> 6] = bv;
+    si[threadIdx.x >> 6] = bi;
   }
   __syncthreads();
-  if (threadIdx.x != 0) return;
+  bv = sv[0];
+  bi = si[0];
+#pragma unroll
   for (int w = 1; w < kAmThreads / 64; ++w)
-    if (am_better(sv[w], si[w], sv[0], si[0])) {
-      sv[0] = sv[w];
-      si[0] = si[w];
+    if (am_better(sv[w], si[w], bv, bi)) {
+      bv = sv[w];
+      bi = si[w];
     }
-  a.part_v[row * nch + chunk] = sv[0];
-  a.part_i[row * nch + chunk] = si[0];
-  __threadfence();
-  const unsigned prev = __hip_atomic_fetch_add(&a.row_cnt[row], 1u, __ATOMIC_ACQ_REL,
-                                               __HIP_MEMORY_SCOPE_AGENT);
-  if (prev != (unsigned)nch - 1) return;
-  __threadfence();
-  float v = -INFINITY;
-  int i = INT_MAX;
-  for (int c = 0; c < nch; ++c)
-    if (am_better(a.part_v[row * nch + c], a.part_i[row * nch + c], v, i)) {
-      v = a.part_v[row * nch + c];
-      i = a.part_i[row * nch + c];
-    }
-  a.amax[row] = i == INT_MAX ? 0 : i;
-  __hip_atomic_store(&a.row_cnt[row], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  __threadfence();
-  const unsigned done = __hip_atomic_fetch_add(a.done_cnt, 1u, __ATOMIC_ACQ_REL,
-                                               __HIP_MEMORY_SCOPE_AGENT);
-  if (done != (unsigned)gridDim.y - 1) return;
-  __threadfence();
-  __hip_atomic_store(a.done_cnt, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  int n = 0;
-  while (n < a.K && a.drafts[n] == a.amax[n]) ++n;
-  a.out[0] = n;
-  a.out[1] = a.amax[n];
-  (void)s_flag;
+  __syncthreads();
+}
+
+__device__ int block_min_int(int v, int* si) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = min(v, __shfl_xor(v, o, kWave));
+  if ((threadIdx.x & 63) == 0) si[threadIdx.x >> 6] = v;
+  __syncthreads();
+  int r = si[0];
+#pragma unroll
+  for (int w = 1; w < kAmThreads / 64; ++w) r = min(r, si[w]);
+  __syncthreads();
+  return r;
 }
 
 __device__ float block_sum256(float v, float* red) {
@@ -164,6 +74,201 @@ __device__ float block_sum256(float v, float* red) {
   const float t = red[0] + red[1] + red[2] + red[3];
   __syncthreads();
   return t;
+}
+
+// One bf16 embedding row into h [H] (fp32) and, when normed is not NULL,
+// RMSNorm(h) into normed.  Threads 0-255 do the work in the same order for
+// every block size (so every caller writes the same bits); the others only
+// join the barriers.
+__device__ void embed_row(int H, const uint16_t* __restrict__ row, float* h, float* normed,
+                          float eps, float* red) {
+  const bool act = threadIdx.x < 256;
+  float ss = 0.f;
+  if (act)
+    for (int i = threadIdx.x; i < H; i += 256) {
+      const float v = __uint_as_float((uint32_t)row[i] << 16);
+      h[i] = v;
+      ss = fmaf(v, v, ss);
+    }
+  if (normed) {
+    ss = wave_sum(ss);
+    if (act && (threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
+    __syncthreads();
+    const float r = 1.0f / sqrtf((red[0] + red[1] + red[2] + red[3]) / (float)H + eps);
+    if (act)
+      for (int i = threadIdx.x; i < H; i += 256) normed[i] = h[i] * r;
+  }
+}
+
+constexpr int kRowThreads = 1024;
+constexpr int kRowVec = 16;  // 16-byte loads in flight per thread
+
+// K = 0 (one row): the argmax by one block, every thread's loads of a 256 KB
+// stretch in flight together, with no cross-block step; out = (0, argmax).
+// With an embedding table given, the block then writes the winner's
+// embedding row and its RMSNorm, as argmax_accept_kernel does.
+__global__ __launch_bounds__(kRowThreads) void argmax_row_kernel(AcceptArgs a) {
+  __shared__ float sv[kRowThreads / 64];
+  __shared__ int si[kRowThreads / 64];
+  __shared__ float red[4];
+  const float* p = a.logits;
+  float bv = -INFINITY;
+  int bi = INT_MAX;
+  if ((a.V & 3) == 0 && (reinterpret_cast<uintptr_t>(p) & 15u) == 0) {
+    const float4* p4 = reinterpret_cast<const float4*>(p);
+    const int n4 = a.V >> 2;
+    for (int j0 = 0; j0 < n4; j0 += kRowThreads * kRowVec) {
+      float4 q[kRowVec];
+#pragma unroll
+      for (int i = 0; i < kRowVec; ++i) {
+        const int j = j0 + threadIdx.x + i * kRowThreads;
+        q[i] = j < n4 ? p4[j] : make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+#pragma unroll
+      for (int i = 0; i < kRowVec; ++i) {
+        const int j = j0 + threadIdx.x + i * kRowThreads;
+        if (j < n4) {
+          am_offer(q[i].x, 4 * j, bv, bi);
+          am_offer(q[i].y, 4 * j + 1, bv, bi);
+          am_offer(q[i].z, 4 * j + 2, bv, bi);
+          am_offer(q[i].w, 4 * j + 3, bv, bi);
+        }
+      }
+    }
+  } else {
+    for (int v = threadIdx.x; v < a.V; v += kRowThreads) am_offer(p[v], v, bv, bi);
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const float ov = __shfl_xor(bv, o, kWave);
+    const int oi = __shfl_xor(bi, o, kWave);
+    if (am_better(ov, oi, bv, bi)) {
+      bv = ov;
+      bi = oi;
+    }
+  }
+  if ((threadIdx.x & 63) == 0) {
+    sv[threadIdx.x >> 6] = bv;
+    si[threadIdx.x >> 6] = bi;
+  }
+  __syncthreads();
+  bv = sv[0];
+  bi = si[0];
+#pragma unroll
+  for (int w = 1; w < kRowThreads / 64; ++w)
+    if (am_better(sv[w], si[w], bv, bi)) {
+      bv = sv[w];
+      bi = si[w];
+    }
+  const int t = bi == INT_MAX ? 0 : bi;
+  if (threadIdx.x == 0) {
+    a.amax[0] = t;
+    a.out[0] = 0;
+    a.out[1] = t;
+  }
+  if (a.emb != nullptr) embed_row(a.H, a.emb + (size_t)t * a.H, a.h, a.normed, a.eps, red);
+}
+
+// Grid (chunks, K+1), K >= 1.  Each block finds the argmax of one 4096-logit
+// chunk of one row (16-byte loads when every row is 16-byte aligned); the last
+// block of a row (device-scope counter) reduces the row's chunk results with
+// all of its threads, and the last row to finish applies the greedy accept
+// rule: n = the first j < K with drafts[j] != amax[j], else K.  With an
+// embedding table given, that block also writes the bonus token's embedding
+// row and its RMSNorm (the next draft position's input).  Counters are left
+// at zero.
+__global__ __launch_bounds__(kAmThreads) void argmax_accept_kernel(AcceptArgs a) {
+  __shared__ float sv[kAmThreads / 64];
+  __shared__ int si[kAmThreads / 64];
+  __shared__ float red[kAmThreads / 64];
+  __shared__ int s_last;
+  const int row = blockIdx.y, chunk = blockIdx.x, nch = gridDim.x, rows = gridDim.y;
+  const float* p = a.logits + (size_t)row * a.V;
+  const int base = chunk * kAmChunk;
+  float bv = -INFINITY;
+  int bi = INT_MAX;
+  if ((a.V & 3) == 0 && (reinterpret_cast<uintptr_t>(a.logits) & 15u) == 0) {
+    const float4* p4 = reinterpret_cast<const float4*>(p);
+    const int n4 = a.V >> 2, b4 = base >> 2;
+    float4 q[kAmVec];
+#pragma unroll
+    for (int i = 0; i < kAmVec; ++i) {
+      const int j = b4 + threadIdx.x + i * kAmThreads;
+      q[i] = j < n4 ? p4[j] : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+#pragma unroll
+    for (int i = 0; i < kAmVec; ++i) {
+      const int j = b4 + threadIdx.x + i * kAmThreads;
+      if (j < n4) {
+        am_offer(q[i].x, 4 * j, bv, bi);
+        am_offer(q[i].y, 4 * j + 1, bv, bi);
+        am_offer(q[i].z, 4 * j + 2, bv, bi);
+        am_offer(q[i].w, 4 * j + 3, bv, bi);
+      }
+    }
+  } else {
+    constexpr int kPer = kAmChunk / kAmThreads;
+    float x[kPer];
+#pragma unroll
+    for (int i = 0; i < kPer; ++i) {
+      const int v = base + threadIdx.x + i * kAmThreads;
+      x[i] = v < a.V ? p[v] : 0.f;
+    }
+#pragma unroll
+    for (int i = 0; i < kPer; ++i) {
+      const int v = base + threadIdx.x + i * kAmThreads;
+      if (v < a.V) am_offer(x[i], v, bv, bi);
+    }
+  }
+  block_argmax(bv, bi, sv, si);
+  if (threadIdx.x == 0) {
+    a.part_v[row * nch + chunk] = bv;
+    a.part_i[row * nch + chunk] = bi;
+    __threadfence();
+    const unsigned prev = __hip_atomic_fetch_add(&a.row_cnt[row], 1u, __ATOMIC_ACQ_REL,
+                                                 __HIP_MEMORY_SCOPE_AGENT);
+    s_last = prev == (unsigned)nch - 1;
+  }
+  __syncthreads();
+  if (!s_last) return;
+  __threadfence();
+  bv = -INFINITY;
+  bi = INT_MAX;
+  for (int c = threadIdx.x; c < nch; c += kAmThreads) {
+    const float v = a.part_v[row * nch + c];
+    const int i = a.part_i[row * nch + c];
+    if (am_better(v, i, bv, bi)) {
+      bv = v;
+      bi = i;
+    }
+  }
+  block_argmax(bv, bi, sv, si);
+  if (threadIdx.x == 0) {
+    a.amax[row] = bi == INT_MAX ? 0 : bi;
+    __hip_atomic_store(&a.row_cnt[row], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __threadfence();
+    const unsigned done = __hip_atomic_fetch_add(a.done_cnt, 1u, __ATOMIC_ACQ_REL,
+                                                 __HIP_MEMORY_SCOPE_AGENT);
+    s_last = done == (unsigned)rows - 1;
+  }
+  __syncthreads();
+  if (!s_last) return;
+  __threadfence();
+  // Each thread's first mismatch in its strided share is its smallest one.
+  int first = a.K;
+  for (int j = threadIdx.x; j < a.K; j += kAmThreads)
+    if (a.drafts[j] != a.amax[j]) {
+      first = j;
+      break;
+    }
+  const int n = block_min_int(first, si);
+  const int bonus = a.amax[n];
+  if (threadIdx.x == 0) {
+    __hip_atomic_store(a.done_cnt, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    a.out[0] = n;
+    a.out[1] = bonus;
+  }
+  if (a.emb != nullptr) embed_row(a.H, a.emb + (size_t)bonus * a.H, a.h, a.normed, a.eps, red);
 }
 
 __global__ __launch_bounds__(256) void rmsnorm_kernel(int H, const float* __restrict__ x, float eps,
@@ -195,18 +300,7 @@ __global__ __launch_bounds__(256) void embed_kernel(int H, int V, const int32_t*
       __hip_atomic_fetch_or(status, kStatusBadToken, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     return;
   }
-  const uint16_t* row = emb + (size_t)tok * H;
-  float ss = 0.f;
-  for (int i = threadIdx.x; i < H; i += 256) {
-    const float v = __uint_as_float((uint32_t)row[i] << 16);
-    h[off + i] = v;
-    ss = fmaf(v, v, ss);
-  }
-  if (normed) {
-    ss = block_sum256(ss, red);
-    const float r = 1.0f / sqrtf(ss / (float)H + eps);
-    for (int i = threadIdx.x; i < H; i += 256) normed[off + i] = h[off + i] * r;
-  }
+  embed_row(H, emb + (size_t)tok * H, h + off, normed ? normed + off : nullptr, eps, red);
 }
 
 __global__ __launch_bounds__(256) void stream_probe_kernel(const u32x4* __restrict__ p, size_t n,

@@ -31,6 +31,10 @@ int draft_layer_chain(const de_moe_desc* d, int T, const float* x, const float* 
                       const void* draft_w, float gamma, int r, float* y, int32_t* pred_idx,
                       float* pred_gate, const de_epilogue* epi, void* ws, size_t ws_bytes,
                       hipStream_t stream, bool logits_ready, const float* next_router);
+int accept_len_embed(int K, int V, const float* target_logits, const int32_t* draft_tokens,
+                     int32_t* target_argmax, int32_t* out, void* ws, size_t ws_bytes,
+                     const void* emb, int H, float* h, float* normed, float eps,
+                     hipStream_t stream);
 int verify_layer_chain(const de_moe_desc* d, int T, const float* x, const float* w_router,
                        const float* bias, const de_expert_table* routed, const void* shared_w,
                        float* y, int32_t* topk_idx, float* topk_gate, int32_t* n_union,
@@ -130,6 +134,10 @@ struct ArgmaxOut {
   int32_t* amax;          // [T]
   int32_t* out;           // [2]: (n, bonus) against `drafts`
   const int32_t* drafts;  // [T-1] (NULL when T is 1)
+  // The acceptance launch also gathers the bonus token's embedding into the
+  // residual and normed buffers a forward starts from, so that the next
+  // position's forward (called with `embedded`) skips its own gather.
+  bool embed_next = false;
 };
 
 // MoE layer l with its routed experts behind the cache.  The routing runs
@@ -217,7 +225,8 @@ struct Capture {
 int forward(const de_model& m, int T, const int32_t* tokens, int mode, float* logits,
             const ArgmaxOut& am, int32_t* n_union, int32_t* pred_idx, size_t pred_stride,
             void* ws, const ModelLayout& L, hipStream_t s, de_cache* cache = nullptr,
-            std::vector<int32_t>* deferred = nullptr, const Capture& cap = Capture{}) {
+            std::vector<int32_t>* deferred = nullptr, const Capture& cap = Capture{},
+            bool embedded = false) {
   const int H = m.moe.hidden;
   // The residual stream ping-pongs between two buffers: a layer reads h and
   // writes h + F(RMSNorm(h)) to the other one.  In the chained launches every
@@ -228,9 +237,13 @@ int forward(const de_model& m, int T, const int32_t* tokens, int mode, float* lo
   float* ncur = at<float>(ws, L.n0);
   float* nnext = at<float>(ws, L.n1);
   void* lws = at<void>(ws, L.layer_ws);
-  int rc = de_embed_gather(T, H, m.vocab, tokens, m.emb, h, ncur, m.eps,
-                           de::layer_status_word(lws), s);
-  if (rc != DE_OK) return rc;
+  // A single position whose token the previous acceptance launch chose finds
+  // its embedding and its RMSNorm already in h and ncur.
+  int rc = DE_OK;
+  if (!(embedded && T == 1) &&
+      (rc = de_embed_gather(T, H, m.vocab, tokens, m.emb, h, ncur, m.eps,
+                            de::layer_status_word(lws), s)) != DE_OK)
+    return rc;
   // Resident layers are chained: each layer's combine (and the dense layer's)
   // also computes the next layer's router logits, so no MoE layer launches its
   // own routing.  (Not with per-layer captures, which read each layer's own
@@ -297,8 +310,11 @@ int forward(const de_model& m, int T, const int32_t* tokens, int mode, float* lo
   }
   rc = de_lm_head(T, H, m.vocab, ncur, m.lm_head, logits, s);
   if (rc != DE_OK || am.amax == nullptr) return rc;
-  return de_accept_len(T - 1, m.vocab, logits, am.drafts, am.amax, am.out,
-                       at<void>(ws, L.accept_ws), L.accept_bytes, s);
+  const bool emb = am.embed_next;
+  return de::accept_len_embed(T - 1, m.vocab, logits, am.drafts, am.amax, am.out,
+                              at<void>(ws, L.accept_ws), L.accept_bytes, emb ? m.emb : nullptr, H,
+                              emb ? at<float>(ws, L.h) : nullptr,
+                              emb ? at<float>(ws, L.n0) : nullptr, m.eps, s);
 }
 
 }  // namespace
@@ -379,9 +395,10 @@ int de_spec_step(const de_model* m, int K, int32_t* block, int32_t* target_argma
   const size_t k = (size_t)m->moe.top_k;
   // Draft loop: position i's token is block[i]; its drafter argmax is block[i+1].
   for (int i = 0; i < K; ++i) {
-    const ArgmaxOut am{block + i + 1, at<int32_t>(ws, L.misc), nullptr};
+    const ArgmaxOut am{block + i + 1, at<int32_t>(ws, L.misc), nullptr, i + 1 < K};
     rc = forward(*m, 1, block + i, DE_DRAFT, logits, am, nullptr,
-                 pred_idx ? pred_idx + (size_t)i * m->n_layers * k : nullptr, k, ws, L, stream);
+                 pred_idx ? pred_idx + (size_t)i * m->n_layers * k : nullptr, k, ws, L, stream,
+                 nullptr, nullptr, Capture{}, i > 0);
     if (rc != DE_OK) return rc;
   }
   // Verify the block [c, d_1..d_K] and accept.
@@ -398,8 +415,9 @@ int de_greedy_decode(const de_model* m, int n_steps, int32_t* tokens, void* ws, 
   const ModelLayout L = model_layout(*m, 1);
   float* logits = at<float>(ws, L.logits);
   for (int i = 0; i < n_steps; ++i) {
-    const ArgmaxOut am{tokens + i + 1, at<int32_t>(ws, L.misc), nullptr};
-    rc = forward(*m, 1, tokens + i, DE_TARGET, logits, am, nullptr, nullptr, 0, ws, L, stream);
+    const ArgmaxOut am{tokens + i + 1, at<int32_t>(ws, L.misc), nullptr, i + 1 < n_steps};
+    rc = forward(*m, 1, tokens + i, DE_TARGET, logits, am, nullptr, nullptr, 0, ws, L, stream,
+                 nullptr, nullptr, Capture{}, i > 0);
     if (rc != DE_OK) return rc;
   }
   return DE_OK;

@@ -1,11 +1,12 @@
-"""The persistent draft pass (one cooperative launch for a draft position's
-MoE layers, Eq. 5) against the separate gate/up, down and combine launches,
-on the GPU.
+"""The persistent draft pass (one launch for a draft position's MoE layers,
+Eq. 5) against the separate gate/up, down and combine launches, on the GPU.
 
 Both paths do the same fp32 operations in the same order, so every output
 must be identical bit for bit: the draft logits of a position, its argmax,
 the drafter's top-k in every layer, and a whole draft-then-verify step.  The
-environment variable DE_DRAFT_PERSISTENT=0 selects the separate launches.
+environment variable DE_DRAFT_PERSISTENT=0 selects the separate launches,
+and DE_PD_COOPERATIVE=1 a cooperative launch of the persistent kernel (same
+bits as the default plain launch).
 Stacks: the 2-layer V2-Lite stack (also against the fp64 oracle), the same
 stack without draft experts, a Moonlight-style stack (sigmoid router with a
 selection bias, renormalised gates), a 34-layer stack of small bf16 layers
@@ -44,12 +45,14 @@ DEEP = configs.scaled_model(
 @pytest.fixture(autouse=True)
 def _restore_env():
     require_gpu()
-    old = os.environ.get("DE_DRAFT_PERSISTENT")
+    names = ("DE_DRAFT_PERSISTENT", "DE_PD_COOPERATIVE")
+    old = {n: os.environ.get(n) for n in names}
     yield
-    if old is None:
-        os.environ.pop("DE_DRAFT_PERSISTENT", None)
-    else:
-        os.environ["DE_DRAFT_PERSISTENT"] = old
+    for n, v in old.items():
+        if v is None:
+            os.environ.pop(n, None)
+        else:
+            os.environ[n] = v
 
 
 def device_model(model, max_block, no_draft=False):
@@ -137,6 +140,35 @@ def test_persistent_draft_full_stack_equals_separate_launches():
     toks = [gen.start_token(model, redraw=r) for r in range(2)]
     _, (block, amax, out, nu, pred, lg2) = draft_and_step(model, dm, toks)
     print(f"full stack: drafts {block.cpu().tolist()} n,bonus {out.cpu().tolist()}", flush=True)
+    del dm
+    torch.cuda.empty_cache()
+
+
+def test_cooperative_launch_equals_plain_launch():
+    """The persistent kernel launched cooperatively (DE_PD_COOPERATIVE=1) and
+    plainly (the default) writes the same bits: a whole step and the draft
+    logits of a second start token."""
+    model = V2_SMALL
+    dm = device_model(model, model.k_draft + 1)
+    os.environ["DE_DRAFT_PERSISTENT"] = "1"
+    K, L, k = model.k_draft, model.n_moe_layers, model.moe.top_k
+    res = []
+    for coop in ("0", "1"):
+        os.environ["DE_PD_COOPERATIVE"] = coop
+        block = dm.new_block(K, gen.start_token(model))
+        amax = torch.empty(K + 1, dtype=torch.int32, device="cuda")
+        out = torch.empty(2, dtype=torch.int32, device="cuda")
+        nu = torch.empty(L, dtype=torch.int32, device="cuda")
+        pred = torch.empty(K, L, k, dtype=torch.int32, device="cuda")
+        dm.spec_step(block, amax, out, nu, pred)
+        lg = torch.empty(1, model.vocab, dtype=torch.float32, device="cuda")
+        dm.forward(torch.tensor([gen.start_token(model, redraw=1)], dtype=torch.int32,
+                                device="cuda"), de.DE_DRAFT, lg)
+        torch.cuda.synchronize()
+        assert de.de_model_status(dm.model, dm.ws) == 0
+        res.append((block, amax, out, nu, pred, lg))
+    for a, b in zip(*res):
+        assert torch.equal(a, b)
     del dm
     torch.cuda.empty_cache()
 

@@ -311,6 +311,42 @@ def test_draft_layer_without_predictions(name, cfg, T):
     assert torch.equal(y0, y1)
 
 
+@pytest.mark.parametrize("name,cfg", [("cfg2", configs.CFG2), ("cfg3", configs.CFG3)],
+                         ids=["cfg2", "cfg3"])
+@pytest.mark.parametrize("variant", ["draft", "no-draft", "in-place"])
+def test_single_draft_layer_persistent_equals_separate(name, cfg, variant, monkeypatch):
+    """A one-position draft layer runs as one persistent launch unless
+    DE_PD_SINGLE=0: both paths write the same bits (output, RMSNorm epilogue,
+    predicted lists and gates, the router logits left in the workspace)."""
+    orc, dev = layer_pair(cfg)
+    x, _ = gapped_x(orc, 1, block=2)
+    h = gen.x_rows(cfg, 1, block=6)
+    ws = dev.ws(1)
+    draft = None if variant == "no-draft" else dev.draft
+    res = []
+    for flag in ("1", "0"):
+        monkeypatch.setenv("DE_PD_SINGLE", flag)
+        res_in = f32(h)
+        y = res_in if variant == "in-place" else torch.empty(1, cfg.hidden, dtype=torch.float32,
+                                                             device="cuda")
+        normed = torch.empty(1, cfg.hidden, dtype=torch.float32, device="cuda")
+        pidx = torch.empty(1, cfg.top_k, dtype=torch.int32, device="cuda")
+        pgate = torch.empty(1, cfg.top_k, dtype=torch.float32, device="cuda")
+        z = torch.empty(1, cfg.n_experts, dtype=torch.float32, device="cuda")
+        epi = de.make_epilogue(residual=res_in, normed=normed)
+        de.de_draft_layer(dev.desc, 1, f32(x), dev.router, dev.bias, dev.table, dev.shared, draft,
+                          cfg.gamma, y, pidx, pgate, ws, epi=epi)
+        de.de_layer_router_logits(dev.desc, 1, ws, z)
+        torch.cuda.synchronize()
+        assert de.de_layer_status(ws) == 0
+        res.append((y.clone(), normed, pidx, pgate, z))
+    for a, b in zip(*res):
+        assert torch.equal(a, b)
+    y_o, idx_o, _ = orc.draft_out(x, with_draft=draft is not None)
+    np.testing.assert_array_equal(res[0][2].cpu().numpy(), idx_o)
+    assert rel_err(res[0][0].cpu().numpy() - h, y_o) <= y_tol(cfg)
+
+
 def test_draft_layer_zero_draft_expert_equals_no_draft():
     cfg = configs.CFG2
     orc, dev = layer_pair(cfg)
@@ -401,6 +437,30 @@ def test_accept_len_planted_prefix(K, V):
             drafts[m] = (drafts[m] + 1) % V
         n_o, bonus_o, t_o = moe.accept_len(logits, drafts)
         de.de_accept_len(K, V, lg, i32(drafts) if K else None, amax, out, ws)
+        o = out.cpu().numpy()
+        assert (int(o[0]), int(o[1])) == (n_o, bonus_o) == (m, int(t[m]))
+        np.testing.assert_array_equal(amax.cpu().numpy(), t_o)
+
+
+@pytest.mark.parametrize("V", [1003, 8192])
+def test_accept_len_more_drafts_than_threads(V):
+    """K = 300 drafts: the first mismatch is found by a block of 256 threads
+    over strided shares, so mismatches on either side of 256 are checked."""
+    K = 300
+    r = np.random.default_rng(V)
+    logits = r.standard_normal((K + 1, V)).astype(np.float32)
+    t = np.argmax(logits, axis=1)
+    lg = f32(logits)
+    amax = torch.empty(K + 1, dtype=torch.int32, device="cuda")
+    out = torch.empty(2, dtype=torch.int32, device="cuda")
+    ws = de.accept_workspace(K, V)
+    for m in (0, 1, 255, 256, 257, 299, 300):
+        drafts = t[:K].copy()
+        if m < K:
+            drafts[m] = (drafts[m] + 1) % V
+            drafts[min(m + 7, K - 1)] = (drafts[min(m + 7, K - 1)] + 1) % V
+        n_o, bonus_o, t_o = moe.accept_len(logits, drafts)
+        de.de_accept_len(K, V, lg, i32(drafts), amax, out, ws)
         o = out.cpu().numpy()
         assert (int(o[0]), int(o[1])) == (n_o, bonus_o) == (m, int(t[m]))
         np.testing.assert_array_equal(amax.cpu().numpy(), t_o)
