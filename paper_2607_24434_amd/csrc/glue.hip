@@ -100,80 +100,13 @@ __device__ void embed_row(int H, const uint16_t* __restrict__ row, float* h, flo
   }
 }
 
-constexpr int kRowThreads = 1024;
-constexpr int kRowVec = 16;  // 16-byte loads in flight per thread
-
-// K = 0 (one row): the argmax by one block, every thread's loads of a 256 KB
-// stretch in flight together, with no cross-block step; out = (0, argmax).
-// With an embedding table given, the block then writes the winner's
-// embedding row and its RMSNorm, as argmax_accept_kernel does.
-__global__ __launch_bounds__(kRowThreads) void argmax_row_kernel(AcceptArgs a) {
-  __shared__ float sv[kRowThreads / 64];
-  __shared__ int si[kRowThreads / 64];
-  __shared__ float red[4];
-  const float* p = a.logits;
-  float bv = -INFINITY;
-  int bi = INT_MAX;
-  if ((a.V & 3) == 0 && (reinterpret_cast<uintptr_t>(p) & 15u) == 0) {
-    const float4* p4 = reinterpret_cast<const float4*>(p);
-    const int n4 = a.V >> 2;
-    for (int j0 = 0; j0 < n4; j0 += kRowThreads * kRowVec) {
-      float4 q[kRowVec];
-#pragma unroll
-      for (int i = 0; i < kRowVec; ++i) {
-        const int j = j0 + threadIdx.x + i * kRowThreads;
-        q[i] = j < n4 ? p4[j] : make_float4(0.f, 0.f, 0.f, 0.f);
-      }
-#pragma unroll
-      for (int i = 0; i < kRowVec; ++i) {
-        const int j = j0 + threadIdx.x + i * kRowThreads;
-        if (j < n4) {
-          am_offer(q[i].x, 4 * j, bv, bi);
-          am_offer(q[i].y, 4 * j + 1, bv, bi);
-          am_offer(q[i].z, 4 * j + 2, bv, bi);
-          am_offer(q[i].w, 4 * j + 3, bv, bi);
-        }
-      }
-    }
-  } else {
-    for (int v = threadIdx.x; v < a.V; v += kRowThreads) am_offer(p[v], v, bv, bi);
-  }
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    const float ov = __shfl_xor(bv, o, kWave);
-    const int oi = __shfl_xor(bi, o, kWave);
-    if (am_better(ov, oi, bv, bi)) {
-      bv = ov;
-      bi = oi;
-    }
-  }
-  if ((threadIdx.x & 63) == 0) {
-    sv[threadIdx.x >> 6] = bv;
-    si[threadIdx.x >> 6] = bi;
-  }
-  __syncthreads();
-  bv = sv[0];
-  bi = si[0];
-#pragma unroll
-  for (int w = 1; w < kRowThreads / 64; ++w)
-    if (am_better(sv[w], si[w], bv, bi)) {
-      bv = sv[w];
-      bi = si[w];
-    }
-  const int t = bi == INT_MAX ? 0 : bi;
-  if (threadIdx.x == 0) {
-    a.amax[0] = t;
-    a.out[0] = 0;
-    a.out[1] = t;
-  }
-  if (a.emb != nullptr) embed_row(a.H, a.emb + (size_t)t * a.H, a.h, a.normed, a.eps, red);
-}
-
-// Grid (chunks, K+1), K >= 1.  Each block finds the argmax of one 4096-logit
+// Grid (chunks, K+1), K >= 0.  Each block finds the argmax of one 4096-logit
 // chunk of one row (16-byte loads when every row is 16-byte aligned); the last
 // block of a row (device-scope counter) reduces the row's chunk results with
 // all of its threads, and the last row to finish applies the greedy accept
-// rule: n = the first j < K with drafts[j] != amax[j], else K.  With an
+// rule: n = the first j < K with drafts[j] != amax[j], else K.  A single row
+// (K = 0) is finished by its last block at once: n = 0 and the bonus is the
+// row's argmax.  With an
 // embedding table given, that block also writes the bonus token's embedding
 // row and its RMSNorm (the next draft position's input).  Counters are left
 // at zero.
@@ -243,6 +176,17 @@ __global__ __launch_bounds__(kAmThreads) void argmax_accept_kernel(AcceptArgs a)
     }
   }
   block_argmax(bv, bi, sv, si);
+  if (rows == 1) {
+    const int t = bi == INT_MAX ? 0 : bi;
+    if (threadIdx.x == 0) {
+      a.amax[0] = t;
+      __hip_atomic_store(&a.row_cnt[0], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      a.out[0] = 0;
+      a.out[1] = t;
+    }
+    if (a.emb != nullptr) embed_row(a.H, a.emb + (size_t)t * a.H, a.h, a.normed, a.eps, red);
+    return;
+  }
   if (threadIdx.x == 0) {
     a.amax[row] = bi == INT_MAX ? 0 : bi;
     __hip_atomic_store(&a.row_cnt[row], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -328,10 +272,6 @@ __global__ __launch_bounds__(256) void stream_probe_kernel(const u32x4* __restri
 int accept_chunks(int V) { return (V + kAmChunk - 1) / kAmChunk; }
 
 hipError_t launch_argmax_accept(const AcceptArgs& a, hipStream_t s) {
-  if (a.K == 0) {
-    hipLaunchKernelGGL(argmax_row_kernel, dim3(1), dim3(kRowThreads), 0, s, a);
-    return note_hip(hipGetLastError());
-  }
   hipLaunchKernelGGL(argmax_accept_kernel, dim3(accept_chunks(a.V), a.K + 1), dim3(kAmThreads), 0,
                      s, a);
   return note_hip(hipGetLastError());
