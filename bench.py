@@ -47,7 +47,7 @@ PMC_TRAFFIC = {
                 "paper_2607_24434_amd/csrc/grouped_core.h",
                 "paper_2607_24434_amd/csrc/topk_union.h",
                 "paper_2607_24434_amd/csrc/de_common.h"],
-    "sha256": "2e1747228494e81b04b6fd033943517ab8ec98e75c139b3aef848fd3ba2b1ced",
+    "sha256": "78517f1cb34d8723a90f25a4733bd5c33814995653eab568ff8ae4885e407f86",
 }
 
 
