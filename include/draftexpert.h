@@ -182,7 +182,12 @@ int de_grouped_swiglu(const de_moe_desc* d, int T, const float* x, const de_expe
  * e1 the top-1 expert and g_{t,e1} its target gate.  Only e1 of the routed
  * experts is read.  pred_idx / pred_gate [T, k] (may be NULL) receive the full
  * top-k of the draft router: the predicted verifier experts (Section 3.4).
- * draft_w NULL (or desc.draft_inter 0) drops the draft-expert term. */
+ * draft_w NULL (or desc.draft_inter 0) drops the draft-expert term.
+ * With bf16 weights and T = 1 the whole layer runs as one launch of the
+ * persistent draft kernel (routing, gate/up, down and the combine with its
+ * epilogue), with the same bits as the separate launches; the environment
+ * variable DE_PD_SINGLE set to "0" keeps the separate launches.  The
+ * epilogue's residual may be y itself. */
 int de_draft_layer(const de_moe_desc* d, int T, const float* x, const float* w_router,
                    const float* bias, const de_expert_table* routed, const void* shared_w,
                    const void* draft_w, float gamma, float* y, int32_t* pred_idx,
