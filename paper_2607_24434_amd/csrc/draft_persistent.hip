@@ -1,5 +1,5 @@
 // The fixed-footprint draft pass (Eq. 5) of one block position through a run
-// of consecutive MoE layers in a single cooperative launch.
+// of consecutive MoE layers in a single launch.
 //
 // A draft layer streams about 70 MB (V2-Lite: router 0.5 MB, two shared
 // experts, the top-1 expert and the draft expert), which the separate
@@ -23,9 +23,9 @@
 // S3) made a V2-Lite draft position 14% faster.  On the same path, the
 // selecting wave selects before its own gate/up work, and publishes the
 // top-1 expert (the top-k's first entry) before it completes the list and
-// the gates, so that the top-1 rows load while it finishes.  The run pays
-// off for two or more layers (a draft position through the stack); a single
-// layer is faster as separate launches.
+// the gates, so that the top-1 rows load while it finishes.  A draft
+// position runs the whole stack in one launch; a single layer call runs as a
+// one-layer launch, which is also faster than its separate launches.
 //
 // The arithmetic is the one of the separate launches, operation for
 // operation (lane l owns the 16-byte weight units l, l + 64, ...; fp32 FMAs in
