@@ -47,7 +47,7 @@ PMC_TRAFFIC = {
                 "paper_2607_24434_amd/csrc/grouped_core.h",
                 "paper_2607_24434_amd/csrc/topk_union.h",
                 "paper_2607_24434_amd/csrc/de_common.h"],
-    "sha256": "78517f1cb34d8723a90f25a4733bd5c33814995653eab568ff8ae4885e407f86",
+    "sha256": "87cb95446bf41797167802e6d934f5cf9c65f6a9e217c7886e25d26cd1eb4193",
 }
 
 

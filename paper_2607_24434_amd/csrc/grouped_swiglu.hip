@@ -385,7 +385,8 @@ size_t staged_bytes(int rows, int len) {
 // holds more than one position.
 // Small launches (fewer full tiles than the device has waves) use tiles of
 // one (G, U) pair or two rows, so that more waves share the rows (one row per
-// down tile measured slower: every block then stages every source's input).
+// down tile measured slower, also for a single position, whose input is not
+// staged: the dense layer at T = 1 took 54 instead of 48 us).
 bool small_launch(const GroupedArgs& a, bool gateup) {
   return max_tiles(a, gateup, kNS) < dev_info().num_cus * 2 * kWavesPB;
 }
